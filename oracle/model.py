@@ -1,0 +1,242 @@
+"""fp64 CPU oracle of the OUTLETS draft backbone and length head.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this module.  It shares no
+code with the HIP library and imports nothing from it.
+
+Everything is float64, one request at a time, in the order the paper
+describes (Section 4.1 backbone, Section 4.2 heads, Section 3.2 static and
+dynamic prediction).  Where the paper leaves a detail open the reading used
+here is stated next to the code:
+
+* Fusion (Eq. 1): f_ctx = W_proj Concat(h_low, h_mid, h_high), no bias, the
+  concatenation in low, mid, high order.
+* Draft decoder layer (Section 4.1): a Llama-style pre-norm layer.  The
+  residual stream starts at f_ctx; RMSNorm (eps 1e-5) before attention and
+  before the SwiGLU MLP; bias-free linears; rotate-half RoPE with frequencies
+  theta^(-2c/hd) and no frequency rescaling; grouped-query attention where
+  query head h reads key/value head floor(h / (n_q / n_kv)); causal within
+  a request.  The paper's Gated Attention is not used (plain GQA).
+* h^draft is the final RMSNorm of the layer output (both heads read it).
+* Length head (Section 4.2): the pooled state p = [mean over the request's
+  tokens of h^draft ; h^draft of the newest token] goes through
+  Linear(2d, H1) + ReLU + Linear(H1, 1), both with biases; the output z_hat
+  estimates log(1 + remaining length) (natural log).
+* Dynamic prediction (Section 3.2): a decode step appends one token at
+  position n + t - 1, attends over every cached key plus itself, updates the
+  running mean over all tokens so far (prompt and generated), and re-runs the
+  head.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .formats import decode_states, decode_weight
+
+WEIGHT_KEYS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down",
+               "gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1",
+               "head_w2", "head_b2")
+
+
+@dataclasses.dataclass(frozen=True)
+class OracleShape:
+    d: int
+    n_q: int
+    n_kv: int
+    head_dim: int
+    ffn: int
+    head_hidden: int
+    rope_theta: float
+    rms_eps: float = 1e-5
+
+
+def decode_weights(stored: Dict[str, object]) -> Dict[str, np.ndarray]:
+    """Stored weights (as the seeded generator returns them) -> float64."""
+    fmt = stored["_fmt"]
+    return {k: decode_weight(stored[k], fmt[k]) for k in WEIGHT_KEYS}
+
+
+# ------------------------------------------------------------------ layers
+
+def fuse(w_proj: np.ndarray, h_low: np.ndarray, h_mid: np.ndarray,
+         h_high: np.ndarray) -> np.ndarray:
+    """Eq. 1: f_ctx = W_proj . Concat(h_low, h_mid, h_high); rows are tokens."""
+    x = np.concatenate([h_low, h_mid, h_high], axis=1)
+    return x @ w_proj.T
+
+
+def rms_norm(x: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
+    """RMSNorm over the last axis: x / sqrt(mean(x^2) + eps) * gamma."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * gamma
+
+
+def rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
+    """Rotate-half rotary embedding of x [n, heads, hd] at integer positions.
+
+    Channel pair (c, c + hd/2) is rotated by the angle p * theta^(-2c/hd)."""
+    hd = x.shape[-1]
+    half = hd // 2
+    c = np.arange(half, dtype=np.float64)
+    omega = theta ** (-2.0 * c / hd)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * omega[None, :]
+    cos = np.cos(ang)[:, None, :]
+    sin = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                         q_pos: np.ndarray, k_pos: np.ndarray,
+                         chunk: int = 1024) -> np.ndarray:
+    """softmax(q k^T / sqrt(hd)) v per query head, keys with position > the
+    query's position masked out.  q [nq_tok, Hq, hd]; k, v [nk_tok, Hkv, hd].
+
+    Query rows are independent, so they are processed ``chunk`` at a time only
+    to bound memory."""
+    n_tok, n_q, hd = q.shape
+    n_kv = k.shape[1]
+    group = n_q // n_kv
+    out = np.empty_like(q)
+    scale = 1.0 / np.sqrt(hd)
+    for h in range(n_q):
+        g = h // group
+        kg, vg = k[:, g, :], v[:, g, :]
+        for s in range(0, n_tok, chunk):
+            e = min(n_tok, s + chunk)
+            scores = (q[s:e, h, :] @ kg.T) * scale
+            allowed = k_pos[None, :] <= q_pos[s:e, None]
+            scores = np.where(allowed, scores, -np.inf)
+            m = scores.max(axis=1, keepdims=True)
+            p = np.exp(scores - m)
+            p /= p.sum(axis=1, keepdims=True)
+            out[s:e, h, :] = p @ vg
+    return out
+
+
+def silu(u: np.ndarray) -> np.ndarray:
+    return u / (1.0 + np.exp(-u))
+
+
+def swiglu_mlp(b: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray,
+               w_down: np.ndarray) -> np.ndarray:
+    """(silu(b W_gate^T) * (b W_up^T)) W_down^T."""
+    return (silu(b @ w_gate.T) * (b @ w_up.T)) @ w_down.T
+
+
+def length_head(p: np.ndarray, w1: np.ndarray, b1: np.ndarray, w2: np.ndarray,
+                b2: np.ndarray) -> np.ndarray:
+    """MLP_len of Section 4.2: z_hat = w2 . relu(W1 p + b1) + b2, rows of p."""
+    u = np.maximum(p @ w1.T + b1, 0.0)
+    return u @ w2 + b2[0]
+
+
+def predicted_remaining(z_hat: np.ndarray) -> np.ndarray:
+    """r_hat = max(0, exp(z_hat) - 1): inverts the z = log(1 + length) target."""
+    return np.maximum(0.0, np.expm1(z_hat))
+
+
+# ------------------------------------------------------------------ model
+
+@dataclasses.dataclass
+class RequestState:
+    """Per-request draft KV cache and running pool, as dynamic prediction needs."""
+    k: np.ndarray          # [n, Hkv, hd], keys after RoPE
+    v: np.ndarray          # [n, Hkv, hd]
+    pool_sum: np.ndarray   # [d], sum of h^draft over every token so far
+    count: int             # tokens so far (prompt + generated)
+
+
+class OracleModel:
+    def __init__(self, shape: OracleShape, weights: Dict[str, np.ndarray]):
+        self.s = shape
+        self.w = weights
+
+    # one pass of the draft layer over new tokens at known positions
+    def _layer(self, h_low, h_mid, h_high, positions, k_prev, v_prev, k_pos_prev):
+        s, w = self.s, self.w
+        n = h_low.shape[0]
+        f = fuse(w["w_proj"], h_low, h_mid, h_high)
+        a = rms_norm(f, w["gamma_attn"], s.rms_eps)
+        q = (a @ w["w_q"].T).reshape(n, s.n_q, s.head_dim)
+        k = (a @ w["w_k"].T).reshape(n, s.n_kv, s.head_dim)
+        v = (a @ w["w_v"].T).reshape(n, s.n_kv, s.head_dim)
+        q = rope(q, positions, s.rope_theta)
+        k = rope(k, positions, s.rope_theta)
+        k_all = np.concatenate([k_prev, k], axis=0)
+        v_all = np.concatenate([v_prev, v], axis=0)
+        k_pos = np.concatenate([k_pos_prev, positions])
+        o = causal_gqa_attention(q, k_all, v_all, positions, k_pos)
+        x1 = f + o.reshape(n, s.n_q * s.head_dim) @ w["w_o"].T
+        b = rms_norm(x1, w["gamma_mlp"], s.rms_eps)
+        x2 = x1 + swiglu_mlp(b, w["w_gate"], w["w_up"], w["w_down"])
+        h_draft = rms_norm(x2, w["gamma_final"], s.rms_eps)
+        return h_draft, k_all, v_all
+
+    def _head(self, pooled: np.ndarray) -> np.ndarray:
+        w = self.w
+        return length_head(pooled, w["head_w1"], w["head_b1"], w["head_w2"], w["head_b2"])
+
+    def prefill_one(self, h_low, h_mid, h_high) -> Tuple[float, np.ndarray, RequestState]:
+        """Static prediction (Section 3.2, t = 0) for one prompt of n tokens."""
+        s = self.s
+        n = h_low.shape[0]
+        empty = np.zeros((0, s.n_kv, s.head_dim))
+        pos = np.arange(n)
+        h_draft, k, v = self._layer(h_low, h_mid, h_high, pos, empty, empty,
+                                    np.zeros(0, dtype=np.int64))
+        pool_sum = h_draft.sum(axis=0)
+        pooled = np.concatenate([pool_sum / n, h_draft[n - 1]])[None, :]
+        z = float(self._head(pooled)[0])
+        return z, h_draft, RequestState(k, v, pool_sum, n)
+
+    def step_one(self, st: RequestState, h_low, h_mid, h_high) -> Tuple[float, np.ndarray]:
+        """Dynamic prediction (Section 3.2, t >= 1): one new token for one request.
+        Updates ``st`` in place."""
+        p = st.count
+        pos = np.array([p])
+        h_draft, k, v = self._layer(h_low[None, :], h_mid[None, :], h_high[None, :], pos,
+                                    st.k, st.v, np.arange(p))
+        st.k, st.v = k, v
+        st.pool_sum = st.pool_sum + h_draft[0]
+        st.count = p + 1
+        pooled = np.concatenate([st.pool_sum / st.count, h_draft[0]])[None, :]
+        return float(self._head(pooled)[0]), h_draft[0]
+
+    # batched API: requests one by one, packed outputs
+    def prefill(self, lens: Sequence[int], h_low, h_mid, h_high):
+        """Packed prompts -> (z [B], h_draft [T, d], states)."""
+        offs = np.concatenate([[0], np.cumsum(np.asarray(lens, dtype=np.int64))])
+        zs, hs, states = [], [], []
+        for i in range(len(lens)):
+            a, b = offs[i], offs[i + 1]
+            z, h, st = self.prefill_one(h_low[a:b], h_mid[a:b], h_high[a:b])
+            zs.append(z)
+            hs.append(h)
+            states.append(st)
+        hd = np.concatenate(hs, axis=0) if hs else np.zeros((0, self.s.d))
+        return np.array(zs), hd, states
+
+    def step(self, states: List[RequestState], h_low, h_mid, h_high):
+        """One decode step for every request in ``states`` (rows in order)."""
+        zs, hs = [], []
+        for i, st in enumerate(states):
+            z, h = self.step_one(st, h_low[i], h_mid[i], h_high[i])
+            zs.append(z)
+            hs.append(h)
+        return np.array(zs), (np.stack(hs) if hs else np.zeros((0, self.s.d)))
+
+
+def oracle_from_workload(wl, stored_weights) -> OracleModel:
+    """Build the oracle for a workload description (duck-typed: ``wl.shape``)."""
+    sh = wl.shape
+    shape = OracleShape(sh.d, sh.n_q, sh.n_kv, sh.head_dim, sh.ffn, sh.head_hidden,
+                        sh.rope_theta, sh.rms_eps)
+    return OracleModel(shape, decode_weights(stored_weights))
+
+
+def states_to_f64(arrs, act_fmt: str):
+    return [decode_states(a, act_fmt) for a in arrs]

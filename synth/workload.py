@@ -1,0 +1,248 @@
+"""Seeded synthetic workloads for the OUTLETS draft-backbone + length-head path.
+
+This module only draws random numbers and stores them in the storage formats
+the path consumes (fp32, bf16 bit patterns, OCP e4m3 codes with bf16 row
+scales).  It holds none of the method's arithmetic: no projection, norm,
+attention, pooling or head.  Both the fp64 oracle and the GPU path take their
+inputs from here and decode the stored formats independently.
+
+Recipe (the same for every consumer):
+
+* Every named tensor gets its own generator,
+  ``numpy.random.default_rng(SeedSequence([seed, cfg_id, stream, index]))``.
+* Linear weights are ``[out, in]`` row-major, drawn N(0, 0.02^2).  RMSNorm
+  gains are 1 + 0.02 N(0, 1) (a gain drawn around zero would shrink every
+  state and flip signs); head biases are N(0, 0.02^2).
+* Target hidden states (the three depths h^(2), h^(N/2), h^(N-2) of
+  Section 4.1) are N(0, 1) per element, multiplied by a per-depth scale
+  (1, 4, 16 for the 8B/70B shapes; 1, 1, 1 for the tiny shape) to mimic the
+  growth of the residual stream with depth.
+* Prompt lengths are either uniform integers or
+  ``clip(rint(exp(ln(median) + sigma * N(0, 1))), lo, hi)``.
+* Draws are fp32 and rounded to the storage format with round-to-nearest-even.
+  The e4m3 weights of the 70B shape use one bf16 scale per output row,
+  ``s = bf16(max|W_row| / 448)``, and codes ``RNE(clamp(W / s, -448, 448))``.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+__all__ = [
+    "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
+    "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
+    "make_step_states", "WEIGHT_NAMES", "BIG_LINEARS",
+]
+
+# Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
+# shape.  Order is the order of their random streams.
+BIG_LINEARS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
+WEIGHT_NAMES = BIG_LINEARS + (
+    "gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1",
+    "head_w2", "head_b2")
+
+
+@dataclasses.dataclass(frozen=True)
+class DraftShape:
+    d: int            # draft hidden size (= target hidden size)
+    n_q: int          # query heads
+    n_kv: int         # key/value heads
+    head_dim: int
+    ffn: int          # SwiGLU inner width
+    head_hidden: int  # width of the length head's hidden layer
+    rope_theta: float
+    rms_eps: float = 1e-5
+
+    def weight_shapes(self) -> Dict[str, Tuple[int, ...]]:
+        d, hd = self.d, self.head_dim
+        return {
+            "w_proj": (d, 3 * d),
+            "w_q": (self.n_q * hd, d),
+            "w_k": (self.n_kv * hd, d),
+            "w_v": (self.n_kv * hd, d),
+            "w_o": (d, self.n_q * hd),
+            "w_gate": (self.ffn, d),
+            "w_up": (self.ffn, d),
+            "w_down": (d, self.ffn),
+            "gamma_attn": (d,),
+            "gamma_mlp": (d,),
+            "gamma_final": (d,),
+            "head_w1": (self.head_hidden, 2 * d),
+            "head_b1": (self.head_hidden,),
+            "head_w2": (self.head_hidden,),
+            "head_b2": (1,),
+        }
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    cfg_id: int
+    name: str
+    shape: DraftShape
+    weight_fmt: str            # "f32" | "bf16" | "e4m3"
+    act_fmt: str               # "f32" | "bf16"
+    n_req: int
+    lengths: Tuple             # ("uniform", lo, hi) | ("lognormal", median, sigma, lo, hi)
+    input_scales: Tuple[float, float, float]
+    steps: int = 0             # decode steps (re-prediction) after the prefill
+    page_size: int = 16
+
+    @property
+    def max_len(self) -> int:
+        return int(self.lengths[-1])
+
+
+SHAPE_TINY = DraftShape(d=256, n_q=4, n_kv=2, head_dim=64, ffn=688,
+                        head_hidden=128, rope_theta=1e4)
+SHAPE_8B = DraftShape(d=4096, n_q=32, n_kv=8, head_dim=128, ffn=14336,
+                      head_hidden=1024, rope_theta=5e5)
+SHAPE_70B = DraftShape(d=8192, n_q=64, n_kv=8, head_dim=128, ffn=28672,
+                       head_hidden=2048, rope_theta=5e5)
+
+WORKLOADS: Dict[int, Workload] = {
+    0: Workload(0, "tiny-fp32", SHAPE_TINY, "f32", "f32", 4,
+                ("uniform", 16, 64), (1.0, 1.0, 1.0), steps=8),
+    1: Workload(1, "8b-bf16-prefill-b32", SHAPE_8B, "bf16", "bf16", 32,
+                ("lognormal", 512, 1.0, 32, 4096), (1.0, 4.0, 16.0)),
+    2: Workload(2, "8b-bf16-prefill-b256", SHAPE_8B, "bf16", "bf16", 256,
+                ("lognormal", 1024, 1.2, 16, 8192), (1.0, 4.0, 16.0)),
+    3: Workload(3, "8b-bf16-step-b512", SHAPE_8B, "bf16", "bf16", 512,
+                ("uniform", 256, 8192), (1.0, 4.0, 16.0), steps=64),
+    4: Workload(4, "70b-e4m3-prefill-b64", SHAPE_70B, "e4m3", "bf16", 64,
+                ("lognormal", 2048, 1.0, 64, 16384), (1.0, 4.0, 16.0)),
+}
+
+
+def workload(cfg_id: int, **overrides) -> Workload:
+    """The named workload, optionally with fields replaced (e.g. a smaller
+    request count or a reduced shape for parity tests)."""
+    w = WORKLOADS[cfg_id]
+    return dataclasses.replace(w, **overrides) if overrides else w
+
+
+# ---------------------------------------------------------------- encodings
+
+def to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 values -> bf16 bit patterns (uint16), round to nearest even.
+    Inputs are finite by construction."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def _bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def encode_e4m3(w: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-output-row OCP e4m3 encoding of an fp32 ``[out, in]`` matrix.
+
+    Returns ``(codes uint8 [out, in], scale_bits uint16 [out])``.  The scale
+    is the bf16 rounding of ``max|row| / 448``; codes are the round-to-nearest
+    -even e4m3 values of ``row / scale`` clamped to the finite range."""
+    import torch  # the encoder uses torch's float8_e4m3fn conversion (RNE)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=1)
+    amax = np.where(amax > 0, amax, np.float32(1.0))
+    s_bits = to_bf16_bits(amax / np.float32(448.0))
+    s = _bf16_bits_to_f32(s_bits)
+    q = np.clip(w / s[:, None], -448.0, 448.0).astype(np.float32)
+    codes = torch.from_numpy(q).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return codes.copy(), s_bits
+
+
+# ---------------------------------------------------------------- draws
+
+def _rng(seed: int, cfg_id: int, stream: int, index: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([seed, cfg_id, stream, index]))
+
+
+def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
+    """All weights of the draft layer and the length head, in storage format.
+
+    Returns a dict ``name -> array``.  For ``f32`` arrays are float32; for
+    ``bf16`` they are uint16 bit patterns; for ``e4m3`` the eight big linears
+    are ``(codes uint8, scale_bits uint16)`` tuples and the rest bf16 bits.
+    ``out['_fmt']`` records the format of each entry."""
+    shapes = wl.shape.weight_shapes()
+    out: Dict[str, object] = {}
+    fmt: Dict[str, str] = {}
+    for stream, name in enumerate(WEIGHT_NAMES):
+        rng = _rng(seed, wl.cfg_id, stream)
+        shp = shapes[name]
+        x = rng.standard_normal(shp, dtype=np.float32)
+        if name.startswith("gamma"):
+            x = np.float32(1.0) + np.float32(0.02) * x
+        else:
+            x = np.float32(0.02) * x
+        if wl.weight_fmt == "f32":
+            out[name], fmt[name] = x, "f32"
+        elif wl.weight_fmt == "e4m3" and name in BIG_LINEARS:
+            out[name], fmt[name] = encode_e4m3(x), "e4m3"
+        else:
+            out[name], fmt[name] = to_bf16_bits(x), "bf16"
+        del x
+    out["_fmt"] = fmt
+    return out
+
+
+def make_lengths(wl: Workload, seed: int = 0, n_req: Optional[int] = None) -> np.ndarray:
+    """Prompt lengths (int32 [n_req]) per the workload's length law."""
+    n = wl.n_req if n_req is None else n_req
+    rng = _rng(seed, wl.cfg_id, 50)
+    law = wl.lengths
+    if law[0] == "uniform":
+        lo, hi = int(law[1]), int(law[2])
+        v = rng.integers(lo, hi + 1, size=n)
+    elif law[0] == "lognormal":
+        med, sigma, lo, hi = float(law[1]), float(law[2]), int(law[3]), int(law[4])
+        z = rng.standard_normal(n)
+        v = np.clip(np.rint(np.exp(np.log(med) + sigma * z)), lo, hi)
+    else:
+        raise ValueError(f"unknown length law {law[0]!r}")
+    return v.astype(np.int32)
+
+
+def _states(rng: np.random.Generator, rows: int, d: int, scale: float, fmt: str) -> np.ndarray:
+    x = rng.standard_normal((rows, d), dtype=np.float32)
+    if scale != 1.0:
+        x *= np.float32(scale)
+    return x if fmt == "f32" else to_bf16_bits(x)
+
+
+def make_prompt_states(wl: Workload, lengths, seed: int = 0,
+                       requests: Optional[List[int]] = None) -> List[np.ndarray]:
+    """Target hidden states (low, mid, high) for the prompts, packed in
+    request order: three arrays ``[sum(lengths), d]``.
+
+    Request ``i`` always draws from its own generator, so any subset of the
+    requests (``requests=[...]`` indexes into ``lengths``) reproduces exactly
+    the rows the full batch holds for them."""
+    lengths = np.asarray(lengths)
+    idx = range(len(lengths)) if requests is None else requests
+    d = wl.shape.d
+    out = []
+    for depth in range(3):
+        parts = [_states(_rng(seed, wl.cfg_id, 100 + depth, int(i)), int(lengths[i]), d,
+                         wl.input_scales[depth], wl.act_fmt) for i in idx]
+        out.append(np.concatenate(parts, axis=0) if parts else
+                   np.zeros((0, d), np.float32 if wl.act_fmt == "f32" else np.uint16))
+    return out
+
+
+def make_step_states(wl: Workload, n_req: int, step: int, seed: int = 0,
+                     requests: Optional[List[int]] = None) -> List[np.ndarray]:
+    """States of the token generated at decode step ``step`` (1-based), one
+    row per request: three arrays ``[n_req or len(requests), d]``.  Row ``i``
+    of the full batch is drawn by its own generator, so subsets reproduce it."""
+    idx = range(n_req) if requests is None else requests
+    d = wl.shape.d
+    out = []
+    for depth in range(3):
+        rows = [_states(_rng(seed, wl.cfg_id, 200 + depth, step * 1_000_003 + int(i)), 1, d,
+                        wl.input_scales[depth], wl.act_fmt) for i in idx]
+        out.append(np.concatenate(rows, axis=0) if rows else
+                   np.zeros((0, d), np.float32 if wl.act_fmt == "f32" else np.uint16))
+    return out
