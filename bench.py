@@ -1,0 +1,199 @@
+"""Throughput of the OUTLETS length-prediction hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: a static prediction for
+every request of the batch (outlets_predict_prefill: fused projection, draft
+layer, pooling, length head, paged KV write), one dynamic re-prediction per
+request (outlets_predict_step: one new token per request through the same
+layer against the paged KV cache), and the release of the requests' slots.
+
+Default workload: the 8B-shaped bf16 draft layer (d 4096, 32 q / 8 KV heads,
+head_dim 128, SwiGLU 14336, head 8192 -> 1024 -> 1) over 32 requests with
+lognormal(median 512, sigma 1.0) prompt lengths clipped to [32, 4096],
+synthetic seeded inputs resident in HBM before timing.
+
+Prints one JSON line (rank 0).  ``--gpus`` above 1 is refused: this build
+runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "predicted requests/sec + draft tokens/sec at 8B shape; MFMA util / HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def gemm_flops(shape, T: int):
+    """Algorithmic FLOPs per launch of each GEMM group for T tokens."""
+    d, hd = shape.d, shape.head_dim
+    qkv = (shape.n_q + 2 * shape.n_kv) * hd
+    return {
+        "FUSE_GEMM": 2.0 * T * d * 3 * d,
+        "QKV_GEMM": 2.0 * T * qkv * d,
+        "O_GEMM": 2.0 * T * d * shape.n_q * hd,
+        "GATE_UP_GEMM": 2.0 * T * 2 * shape.ffn * d,
+        "DOWN_GEMM": 2.0 * T * d * shape.ffn,
+    }
+
+
+def cpu_baseline(wl, W, lens, budget_s: float = 12.0):
+    """The fp64 oracle on a bounded sample of the same batch: requests in
+    batch order, static prediction + one step each, until ``budget_s`` of
+    work; scaled to requests/s of the batch's mean request length."""
+    import numpy as np
+    from oracle import oracle_from_workload, states_to_f64
+    from synth import make_prompt_states, make_step_states
+
+    orc = oracle_from_workload(wl, W)
+    t_total, tok, done = 0.0, 0, []
+    for i in range(len(lens)):
+        st = states_to_f64(make_prompt_states(wl, lens, requests=[i]), wl.act_fmt)
+        sp = states_to_f64(make_step_states(wl, len(lens), 1, requests=[i]), wl.act_fmt)
+        t0 = time.perf_counter()
+        _, _, s = orc.prefill([int(lens[i])], *st)
+        orc.step(s, *sp)
+        t_total += time.perf_counter() - t0
+        tok += int(lens[i]) + 1
+        done.append(i)
+        if t_total >= budget_s:
+            break
+    tok_per_s = tok / t_total
+    mean_tokens = (float(np.sum(lens)) + len(lens)) / len(lens)
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads") or 0) for p in threadpool_info()) or None
+    except Exception:
+        pass
+    return {
+        "value": tok_per_s / mean_tokens,
+        "unit": "requests/s",
+        "cores": threads or os.cpu_count(),
+        "kind": "oracle",
+        "sample": f"requests {done[0]}..{done[-1]} of the batch ({len(done)} requests, {tok} tokens, "
+                  f"prefill + 1 step each, fp64 numpy, {t_total:.1f} s); rate scaled by the batch's "
+                  f"mean of {mean_tokens:.0f} tokens per request",
+        "draft_tokens_per_s": tok_per_s,
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    a = ap.parse_args(argv)
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the path shards over "
+              "requests and this build measures one GPU's share", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
+    from synth import make_lengths, make_prompt_states, make_step_states, make_weights, workload
+
+    wl = workload(1)
+    print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
+    W = make_weights(wl, a.seed)
+    lens = make_lengths(wl, a.seed)
+    T, B = int(lens.sum()), len(lens)
+    H = [to_device(x) for x in make_prompt_states(wl, lens, a.seed)]
+    S = [to_device(x) for x in make_step_states(wl, B, 1, a.seed)]
+    pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B,
+                            max_seq_len=int(lens.max()) + 16, num_pages=B * ((int(lens.max()) + 16 + 15) // 16),
+                            max_batch_tokens=T, max_batch_requests=B)
+    slots = list(range(B))
+    z = torch.empty(B, dtype=torch.float32, device="cuda")
+    z1 = torch.empty(B, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def one_step():
+        pred.prefill(slots, lens, *H, z_out=z, stream=stream)
+        pred.step(slots, *S, z_out=z1, stream=stream)
+        pred.release(slots)
+
+    print(f"[bench] warmup {a.warmup} steps (T={T} tokens, B={B})", file=sys.stderr, flush=True)
+    for _ in range(a.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    pred.profile(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(a.steps):
+        one_step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    prof_pre = pred.profile_read("prefill")
+    prof_step = pred.profile_read("step")
+    pred.profile(False)
+    print(f"[bench] timed {a.steps} steps: {gpu_ms:.2f} ms (events), {wall * 1e3:.2f} ms (wall)",
+          file=sys.stderr, flush=True)
+    ms_per_step = max(gpu_ms, wall * 1e3) / a.steps
+    req_s = B / (ms_per_step / 1e3)
+    tok_s = (T + B) / (ms_per_step / 1e3)
+
+    flops = gemm_flops(wl.shape, T)
+    kernels = {}
+    for name, (ms, n) in prof_pre.items():
+        if n:
+            kernels[name] = {"avg_ms": ms / n, "launches": n}
+            if name in flops:
+                kernels[name]["tflops"] = flops[name] / (ms / n * 1e-3) / 1e12
+    dom = "GATE_UP_GEMM"
+    dom_ms = prof_pre[dom][0] / max(1, prof_pre[dom][1])
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    step_kernels = {name: {"avg_ms": ms / n, "launches": n} for name, (ms, n) in prof_step.items() if n}
+
+    out = {
+        "metric": METRIC,
+        "value": req_s,
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; lognormal prompt lengths; N(0,1) x (1,4,16) target states; N(0,0.02) weights)",
+        "config": {"workload": "8B-shaped bf16 draft layer + length head: 32 requests, lognormal(512, 1.0) "
+                               "prompts clipped to [32, 4096], static prediction + 1 dynamic step per request",
+                   "requests": B, "prompt_tokens": T, "d": wl.shape.d, "heads": [wl.shape.n_q, wl.shape.n_kv],
+                   "head_dim": wl.shape.head_dim, "ffn": wl.shape.ffn, "head_hidden": wl.shape.head_hidden,
+                   "page_size": 16},
+        "draft_tokens_per_s": tok_s,
+        "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
+                     "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flops_per_launch": flops[dom], "avg_ms": dom_ms},
+        "kernels_prefill": kernels,
+        "kernels_step": step_kernels,
+    }
+    if not a.no_cpu_baseline:
+        print("[bench] timing the fp64 oracle on a sample (cpu_baseline)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, W, lens, a.cpu_budget)
+    pred.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

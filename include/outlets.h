@@ -1,0 +1,308 @@
+/*
+ * outlets.h -- C ABI of the MI355X (gfx950) OUTLETS length-prediction path.
+ *
+ * OUTLETS ("Output-Length Prediction from Speculative Decoding Backbones")
+ * predicts the remaining output length of LLM requests from an EAGLE-3-style
+ * speculative draft backbone:
+ *
+ *   f_ctx   = W_proj Concat(h_low, h_mid, h_high)              (Eq. 1)
+ *   h_draft = one Llama-style draft decoder layer over f_ctx    (Section 4.1)
+ *   z_hat   = MLP_len(pooled h_draft) ~ log(1 + remaining len)  (Section 4.2)
+ *
+ * Static prediction runs once after the prompt (Section 3.2, t = 0:
+ * outlets_predict_prefill); dynamic prediction re-predicts after every
+ * generated token (Section 3.2, t >= 1: outlets_predict_step) using a paged
+ * draft KV cache the library owns.
+ *
+ * Layer details the paper leaves open, fixed here and in the fp64 oracle:
+ *   - pre-norm layer, residual stream starting at f_ctx, RMSNorm eps from the
+ *     config, bias-free linears, SwiGLU MLP, final RMSNorm -> h_draft;
+ *   - rotate-half RoPE: channel pair (c, c + hd/2) rotated by
+ *     p * theta^(-2c/hd), no frequency rescaling;
+ *   - plain grouped-query attention (query head h reads KV head
+ *     h / (n_q / n_kv)), causal within a request; no attention gate;
+ *   - head input p = [mean of h_draft over the request's tokens so far ;
+ *     h_draft of the newest token], then Linear(2d, H1) + ReLU +
+ *     Linear(H1, 1), both with biases.
+ *
+ * All functions are thread-compatible (one context per thread at a time) and
+ * return an int status: OUTLETS_OK (0) or a negative OUTLETS_ERR_* code.
+ * No C++ exception crosses this boundary.  outlets_last_error() gives a
+ * message for the calling thread's last failure.
+ *
+ * Memory ownership: the caller owns every buffer passed in (weights,
+ * activations, outputs); weights registered by outlets_create must stay
+ * valid and unchanged until outlets_destroy.  The library owns the KV page
+ * pool, per-slot state (cached length, page list, running pool sum) and its
+ * workspace.  Host arrays are read before a call returns.  Device work is
+ * queued on the given HIP stream (NULL = the default stream); outputs are
+ * valid once the caller synchronises that stream.  All calls on one
+ * context must be ordered on one stream (or externally synchronised).
+ */
+#ifndef OUTLETS_H
+#define OUTLETS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status codes */
+enum {
+    OUTLETS_OK = 0,
+    OUTLETS_ERR_INVALID_ARG = -1,   /* bad size, pointer, slot, length */
+    OUTLETS_ERR_SLOT_BUSY = -2,     /* prefill on a slot that is active */
+    OUTLETS_ERR_SLOT_EMPTY = -3,    /* step on a slot that is not active */
+    OUTLETS_ERR_OUT_OF_PAGES = -4,  /* KV page pool exhausted */
+    OUTLETS_ERR_UNSUPPORTED = -5,   /* format/shape the kernels do not handle */
+    OUTLETS_ERR_HIP = -6,           /* HIP runtime error (message has details) */
+    OUTLETS_ERR_NOMEM = -7          /* device or host allocation failed */
+};
+
+/* ------------------------------------------------------------ formats */
+enum {
+    OUTLETS_FMT_F32 = 0,    /* IEEE binary32 */
+    OUTLETS_FMT_BF16 = 1,   /* bfloat16 (upper half of binary32) */
+    OUTLETS_FMT_E4M3 = 2    /* OCP FP8 E4M3 codes + one bf16 scale per output row */
+};
+
+/*
+ * Model and capacity description.
+ *   d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim: draft layer shape;
+ *     n_q_heads * head_dim need not equal d_model; n_q_heads must be a
+ *     multiple of n_kv_heads; head_dim is 64 or 128.
+ *   head_hidden: H1, the length head's hidden width.
+ *   rope_theta, rms_eps: RoPE base and RMSNorm epsilon.
+ *   weight_fmt: F32 (then act_fmt must be F32), BF16 or E4M3 (act BF16).
+ *     With E4M3 only the eight big linears (proj, q, k, v, o, gate, up, down)
+ *     are fp8; gains and the head are bf16.
+ *   act_fmt: format of h_low/h_mid/h_high, of h_draft output and of the KV
+ *     cache: F32 or BF16.
+ *   page_size: tokens per KV page; must be 16.
+ *   max_slots: number of request slots (per-request state entries).
+ *   max_seq_len: longest request (prompt + generated tokens).
+ *   num_pages: KV pages in the pool (each holds page_size tokens of K and V
+ *     for every KV head).
+ *   max_batch_tokens: largest packed token count one prefill call may pass.
+ *   max_batch_requests: largest n_req of one prefill or step call.
+ *   keep_intermediates: nonzero keeps every intermediate activation of the
+ *     last call in its own buffer so outlets_get_buffer can return it (more
+ *     device memory; for testing).
+ */
+typedef struct outlets_config {
+    int32_t d_model;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn_dim;
+    int32_t head_hidden;
+    double rope_theta;
+    float rms_eps;
+    int32_t weight_fmt;
+    int32_t act_fmt;
+    int32_t page_size;
+    int32_t max_slots;
+    int32_t max_seq_len;
+    int32_t num_pages;
+    int32_t max_batch_tokens;
+    int32_t max_batch_requests;
+    int32_t keep_intermediates;
+} outlets_config;
+
+/*
+ * Device pointers to the weights, PyTorch [out, in] row-major layout.
+ *   w_proj [d, 3d]  (columns: h_low, h_mid, h_high; Eq. 1)
+ *   w_q [n_q*hd, d], w_k [n_kv*hd, d], w_v [n_kv*hd, d], w_o [d, n_q*hd]
+ *   w_gate [F, d], w_up [F, d], w_down [d, F]
+ *   s_*: bf16 [out] row scales, required for E4M3 and ignored otherwise
+ *        (the weight value is decode(code) * scale[row]).
+ *   gamma_attn, gamma_mlp, gamma_final [d]: RMSNorm gains
+ *   head_w1 [H1, 2d], head_b1 [H1], head_w2 [H1], head_b2 [1]
+ * Element format: weight_fmt for the big linears; F32 for the rest when
+ * weight_fmt is F32, BF16 otherwise.
+ */
+typedef struct outlets_weights {
+    const void* w_proj;  const void* s_proj;
+    const void* w_q;     const void* s_q;
+    const void* w_k;     const void* s_k;
+    const void* w_v;     const void* s_v;
+    const void* w_o;     const void* s_o;
+    const void* w_gate;  const void* s_gate;
+    const void* w_up;    const void* s_up;
+    const void* w_down;  const void* s_down;
+    const void* gamma_attn;
+    const void* gamma_mlp;
+    const void* gamma_final;
+    const void* head_w1;
+    const void* head_b1;
+    const void* head_w2;
+    const void* head_b2;
+} outlets_weights;
+
+typedef struct outlets_ctx outlets_ctx;
+typedef struct outlets_pager outlets_pager;
+
+/*
+ * Create a context on HIP device `device`: validates the config, records the
+ * weight pointers (not copied), builds the RoPE cos/sin table on the host in
+ * float64 and uploads it as float32, and allocates the KV page pool, the
+ * per-slot state and the workspace.  Synchronous.  On failure *out is NULL.
+ */
+int outlets_create(const outlets_config* cfg, const outlets_weights* weights,
+                   int32_t device, outlets_ctx** out);
+
+/* Free everything the context owns.  Synchronises the device first.  NULL is a no-op. */
+int outlets_destroy(outlets_ctx* ctx);
+
+/*
+ * Static prediction (Section 3.2, t = 0) for n_req new requests.
+ *   slots [n_req] (host): slot id of each request, all inactive and distinct.
+ *   lens [n_req] (host): prompt length n_i >= 1 of each request.
+ *   h_low, h_mid, h_high (device, act_fmt): the target model's hidden states
+ *     at the three selected depths (Section 4.1: layers 2, N/2, N-2), packed
+ *     varlen in `slots` order: request i owns rows [cu_i, cu_{i+1}) with
+ *     cu_0 = 0, cu_{i+1} = cu_i + lens[i]; row r starts at element
+ *     r * row_stride (row_stride >= d_model).  One [T, 3d] tensor may be
+ *     passed as base, base + d, base + 2d with row_stride 3d.
+ *   z_out (device, float32 [n_req]): z_hat_i, the predicted log(1 + L_i).
+ *   hdraft_out (device, act_fmt [T, d] or NULL): h_draft of every token.
+ *   stream: hipStream_t (NULL = default stream).
+ * Prompt tokens take positions 0..n_i-1.  Each slot receives ceil(n_i/16)
+ * pages: lowest free page ids first, requests in argument order.  All checks
+ * and the page allocation happen before any device work; on any error the
+ * state is unchanged.  Check order: n_req range and pointers, then per
+ * request slot range / repetition / length, then busy slots, then page
+ * availability.  n_req == 0 is a no-op.
+ */
+int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
+                            const int32_t* lens, const void* h_low, const void* h_mid,
+                            const void* h_high, int64_t row_stride, float* z_out,
+                            void* hdraft_out, void* stream);
+
+/*
+ * Dynamic prediction (Section 3.2, t >= 1): one generated token per request.
+ *   slots [n_req] (host): active, distinct slots.
+ *   h_low, h_mid, h_high (device, act_fmt [n_req rows], row_stride): states
+ *     of the newly generated token y_t, row i for slots[i].
+ *   z_out (device float32 [n_req]): z_hat_t, the predicted log(1 + r_t).
+ *   hdraft_out (device act_fmt [n_req, d] or NULL).
+ * The token takes position (cached length) and attends over every cached key
+ * plus itself; the running mean in the head input covers prompt and
+ * generated tokens.  A slot takes a new page exactly when its cached length
+ * is a multiple of 16 before the append.  Check order: n_req range and
+ * pointers, slot range / repetition, inactive slots, full slots
+ * (cached length == max_seq_len), page availability; on error the state is
+ * unchanged.
+ */
+int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
+                         const void* h_low, const void* h_mid, const void* h_high,
+                         int64_t row_stride, float* z_out, void* hdraft_out, void* stream);
+
+/* End requests: frees their pages and state.  Inactive slots are a no-op;
+ * an out-of-range or repeated slot fails with no change. */
+int outlets_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);
+
+/* ------------------------------------------------------------ inspection */
+enum {
+    OUTLETS_META_PAGE_TABLE = 0,        /* host table [max_slots, max_pages_per_seq], -1 = none */
+    OUTLETS_META_SEQ_LEN = 1,           /* host cached length per slot [max_slots] */
+    OUTLETS_META_DEV_PAGE_TABLE = 2,    /* the device copy the kernels read */
+    OUTLETS_META_DEV_CU_SEQLENS = 3,    /* last call, device: [n_req + 1] token offsets */
+    OUTLETS_META_DEV_POSITIONS = 4,     /* last call, device: [T] token positions */
+    OUTLETS_META_DEV_LAST_IDX = 5,      /* last call, device: [n_req] row of the newest token */
+    OUTLETS_META_DEV_TOKEN_SLOT = 6     /* last call, device: [T] slot of each token */
+};
+
+/*
+ * Copy integer metadata into host memory `out` (capacity `cap` int32s);
+ * *n_out receives the element count.  Device entries synchronise the device.
+ * Fails with INVALID_ARG if cap is too small.
+ */
+int outlets_get_meta(outlets_ctx* ctx, int32_t what, int32_t* out, int64_t cap, int64_t* n_out);
+
+enum {
+    OUTLETS_BUF_FUSED = 0,      /* f_ctx, float32 [T, d] */
+    OUTLETS_BUF_NORM_ATTN = 1,  /* RMSNorm(f_ctx), act [T, d] */
+    OUTLETS_BUF_Q = 2,          /* queries after RoPE, act [T, n_q*hd] */
+    OUTLETS_BUF_ATTN = 3,       /* attention output, act [T, n_q*hd] */
+    OUTLETS_BUF_X1 = 4,         /* f + attn W_o^T, float32 [T, d] */
+    OUTLETS_BUF_NORM_MLP = 5,   /* RMSNorm(x1), act [T, d] */
+    OUTLETS_BUF_MLP_ACT = 6,    /* silu(gate) * up, act [T, F] */
+    OUTLETS_BUF_X2 = 7,         /* x1 + mlp, float32 [T, d] */
+    OUTLETS_BUF_HDRAFT = 8,     /* h_draft, float32 [T, d] */
+    OUTLETS_BUF_POOLED = 9,     /* head input p, float32 [n_req, 2d] */
+    OUTLETS_BUF_K_POOL = 10,    /* key pages, act [num_pages, n_kv, 16, hd] */
+    OUTLETS_BUF_V_POOL = 11     /* value pages, act [num_pages, n_kv, 16, hd] */
+};
+
+/*
+ * Copy an activation of the last call (rows of that call only) or a KV pool
+ * into caller device memory `dst` (`nbytes` capacity) on `stream`;
+ * *n_bytes receives the size.  Buffers 0..8 need keep_intermediates (except
+ * HDRAFT, POOLED and the pools, always kept).
+ */
+int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbytes,
+                       int64_t* n_bytes, void* stream);
+
+/* ------------------------------------------------------------ per-kernel timing */
+enum {
+    OUTLETS_K_META = 0,         /* page-table scatter + token metadata */
+    OUTLETS_K_FUSE_GEMM = 1,    /* Eq. 1 projection */
+    OUTLETS_K_NORM = 2,         /* the three RMSNorms */
+    OUTLETS_K_QKV_GEMM = 3,
+    OUTLETS_K_ROPE_KV = 4,      /* rotary embedding + paged K/V write */
+    OUTLETS_K_ATTN = 5,
+    OUTLETS_K_O_GEMM = 6,
+    OUTLETS_K_GATE_UP_GEMM = 7, /* gate/up projection with the SwiGLU epilogue */
+    OUTLETS_K_DOWN_GEMM = 8,
+    OUTLETS_K_POOL = 9,
+    OUTLETS_K_HEAD = 10,        /* length head (both layers) */
+    OUTLETS_K_COUNT = 11
+};
+
+/*
+ * enable != 0 starts recording a HIP event pair around every kernel launch
+ * of later calls (on the call's stream) and clears the totals; 0 stops.
+ * Timing adds a little launch overhead; leave it off in production.
+ */
+int outlets_profile_enable(outlets_ctx* ctx, int32_t enable);
+
+/*
+ * Total milliseconds and launch count recorded for kernel group `which`
+ * (OUTLETS_K_*) inside prefill calls (call = 0) or step calls (call = 1)
+ * since profiling was enabled.  Synchronises on the recorded events.
+ */
+int outlets_profile_read(outlets_ctx* ctx, int32_t call, int32_t which, double* total_ms,
+                         int64_t* launches);
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char* outlets_last_error(void);
+
+/* ------------------------------------------------------------ host-only entry points
+ * These run on the CPU and touch no GPU; the context uses the same code. */
+
+/*
+ * Varlen metadata of packed prompts (host arrays): cu_out [n_req + 1]
+ * (exclusive prefix sum, cu_out[0] = 0), pos_out [T] (0..n_i-1 per request)
+ * and last_out [n_req] (cu_{i+1} - 1).  Any output may be NULL.  Lengths
+ * must be >= 1.
+ */
+int outlets_varlen_meta(int32_t n_req, const int32_t* lens, int32_t* cu_out,
+                        int32_t* pos_out, int32_t* last_out);
+
+/* A stand-alone instance of the context's page allocator (host memory only). */
+int outlets_pager_create(int32_t num_pages, int32_t page_size, int32_t max_slots,
+                         int32_t max_seq_len, outlets_pager** out);
+int outlets_pager_destroy(outlets_pager* p);
+int outlets_pager_prefill(outlets_pager* p, int32_t n, const int32_t* slots, const int32_t* lens);
+int outlets_pager_step(outlets_pager* p, int32_t n, const int32_t* slots);
+int outlets_pager_release(outlets_pager* p, int32_t n, const int32_t* slots);
+/* what: OUTLETS_META_PAGE_TABLE or OUTLETS_META_SEQ_LEN. */
+int outlets_pager_read(outlets_pager* p, int32_t what, int32_t* out, int64_t cap, int64_t* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OUTLETS_H */

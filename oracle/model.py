@@ -156,7 +156,7 @@ class OracleModel:
         self.w = weights
 
     # one pass of the draft layer over new tokens at known positions
-    def _layer(self, h_low, h_mid, h_high, positions, k_prev, v_prev, k_pos_prev):
+    def _layer(self, h_low, h_mid, h_high, positions, k_prev, v_prev, k_pos_prev, capture=None):
         s, w = self.s, self.w
         n = h_low.shape[0]
         f = fuse(w["w_proj"], h_low, h_mid, h_high)
@@ -174,22 +174,30 @@ class OracleModel:
         b = rms_norm(x1, w["gamma_mlp"], s.rms_eps)
         x2 = x1 + swiglu_mlp(b, w["w_gate"], w["w_up"], w["w_down"])
         h_draft = rms_norm(x2, w["gamma_final"], s.rms_eps)
+        if capture is not None:
+            capture.update(fused=f, norm_attn=a, q=q.reshape(n, -1), k=k, v=v,
+                           attn=o.reshape(n, -1), x1=x1, norm_mlp=b,
+                           mlp_act=silu(b @ w["w_gate"].T) * (b @ w["w_up"].T), x2=x2,
+                           hdraft=h_draft)
         return h_draft, k_all, v_all
 
     def _head(self, pooled: np.ndarray) -> np.ndarray:
         w = self.w
         return length_head(pooled, w["head_w1"], w["head_b1"], w["head_w2"], w["head_b2"])
 
-    def prefill_one(self, h_low, h_mid, h_high) -> Tuple[float, np.ndarray, RequestState]:
-        """Static prediction (Section 3.2, t = 0) for one prompt of n tokens."""
+    def prefill_one(self, h_low, h_mid, h_high, capture=None) -> Tuple[float, np.ndarray, RequestState]:
+        """Static prediction (Section 3.2, t = 0) for one prompt of n tokens.
+        ``capture`` (a dict) receives the layer's intermediate activations."""
         s = self.s
         n = h_low.shape[0]
         empty = np.zeros((0, s.n_kv, s.head_dim))
         pos = np.arange(n)
         h_draft, k, v = self._layer(h_low, h_mid, h_high, pos, empty, empty,
-                                    np.zeros(0, dtype=np.int64))
+                                    np.zeros(0, dtype=np.int64), capture)
         pool_sum = h_draft.sum(axis=0)
         pooled = np.concatenate([pool_sum / n, h_draft[n - 1]])[None, :]
+        if capture is not None:
+            capture["pooled"] = pooled[0]
         z = float(self._head(pooled)[0])
         return z, h_draft, RequestState(k, v, pool_sum, n)
 

@@ -1,0 +1,234 @@
+"""ctypes binding of ``liboutlets.so`` (the C ABI declared in include/outlets.h).
+
+Argument marshalling only: every step of the path runs in the HIP library.
+Loading fails loudly when the library has not been built; there is no
+fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liboutlets.so")
+
+OUTLETS_OK = 0
+OUTLETS_ERR_INVALID_ARG = -1
+OUTLETS_ERR_SLOT_BUSY = -2
+OUTLETS_ERR_SLOT_EMPTY = -3
+OUTLETS_ERR_OUT_OF_PAGES = -4
+OUTLETS_ERR_UNSUPPORTED = -5
+OUTLETS_ERR_HIP = -6
+OUTLETS_ERR_NOMEM = -7
+
+OUTLETS_FMT_F32 = 0
+OUTLETS_FMT_BF16 = 1
+OUTLETS_FMT_E4M3 = 2
+
+OUTLETS_META_PAGE_TABLE = 0
+OUTLETS_META_SEQ_LEN = 1
+OUTLETS_META_DEV_PAGE_TABLE = 2
+OUTLETS_META_DEV_CU_SEQLENS = 3
+OUTLETS_META_DEV_POSITIONS = 4
+OUTLETS_META_DEV_LAST_IDX = 5
+OUTLETS_META_DEV_TOKEN_SLOT = 6
+
+KERNELS = ["META", "FUSE_GEMM", "NORM", "QKV_GEMM", "ROPE_KV", "ATTN", "O_GEMM", "GATE_UP_GEMM",
+           "DOWN_GEMM", "POOL", "HEAD"]
+
+BUF = {name: i for i, name in enumerate(
+    ["FUSED", "NORM_ATTN", "Q", "ATTN", "X1", "NORM_MLP", "MLP_ACT", "X2", "HDRAFT",
+     "POOLED", "K_POOL", "V_POOL"])}
+
+
+class OutletsError(RuntimeError):
+    def __init__(self, rc: int, fn: str, msg: str):
+        super().__init__(f"{fn} failed with status {rc}: {msg}")
+        self.rc = rc
+
+
+class outlets_config(C.Structure):
+    _fields_ = [
+        ("d_model", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+        ("head_dim", C.c_int32), ("ffn_dim", C.c_int32), ("head_hidden", C.c_int32),
+        ("rope_theta", C.c_double), ("rms_eps", C.c_float), ("weight_fmt", C.c_int32),
+        ("act_fmt", C.c_int32), ("page_size", C.c_int32), ("max_slots", C.c_int32),
+        ("max_seq_len", C.c_int32), ("num_pages", C.c_int32), ("max_batch_tokens", C.c_int32),
+        ("max_batch_requests", C.c_int32), ("keep_intermediates", C.c_int32),
+    ]
+
+
+WEIGHT_FIELDS = [
+    "w_proj", "s_proj", "w_q", "s_q", "w_k", "s_k", "w_v", "s_v", "w_o", "s_o",
+    "w_gate", "s_gate", "w_up", "s_up", "w_down", "s_down", "gamma_attn", "gamma_mlp",
+    "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2",
+]
+
+
+class outlets_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in WEIGHT_FIELDS]
+
+
+_lib: Optional[C.CDLL] = None
+
+_P = C.c_void_p
+_I32P = C.POINTER(C.c_int32)
+_SIGS = {
+    "outlets_create": (C.c_int, [C.POINTER(outlets_config), C.POINTER(outlets_weights), C.c_int32, C.POINTER(_P)]),
+    "outlets_destroy": (C.c_int, [_P]),
+    "outlets_predict_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
+    "outlets_predict_step": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
+    "outlets_release": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_get_meta": (C.c_int, [_P, C.c_int32, _I32P, C.c_int64, C.POINTER(C.c_int64)]),
+    "outlets_get_buffer": (C.c_int, [_P, C.c_int32, _P, C.c_int64, C.POINTER(C.c_int64), _P]),
+    "outlets_last_error": (C.c_char_p, []),
+    "outlets_profile_enable": (C.c_int, [_P, C.c_int32]),
+    "outlets_profile_read": (C.c_int, [_P, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+    "outlets_varlen_meta": (C.c_int, [C.c_int32, _I32P, _I32P, _I32P, _I32P]),
+    "outlets_pager_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(_P)]),
+    "outlets_pager_destroy": (C.c_int, [_P]),
+    "outlets_pager_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P]),
+    "outlets_pager_step": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_pager_release": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_pager_read": (C.c_int, [_P, C.c_int32, _I32P, C.c_int64, C.POINTER(C.c_int64)]),
+}
+
+
+def lib() -> C.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_01068_amd.build` (there is no fallback)")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_names():
+    return list(_SIGS)
+
+
+def last_error() -> str:
+    return lib().outlets_last_error().decode()
+
+
+def check(rc: int, fn: str) -> int:
+    if rc != OUTLETS_OK:
+        raise OutletsError(rc, fn, last_error())
+    return rc
+
+
+def i32_array(values):
+    vals = [int(v) for v in values]
+    return (C.c_int32 * max(1, len(vals)))(*vals)
+
+
+# ------------------------------------------------------------ thin wrappers
+
+def outlets_create(cfg: outlets_config, weights: outlets_weights, device: int = 0) -> C.c_void_p:
+    ctx = C.c_void_p()
+    check(lib().outlets_create(C.byref(cfg), C.byref(weights), device, C.byref(ctx)), "outlets_create")
+    return ctx
+
+
+def outlets_destroy(ctx) -> None:
+    lib().outlets_destroy(ctx)
+
+
+def outlets_predict_prefill(ctx, slots, lens, h_low: int, h_mid: int, h_high: int, row_stride: int,
+                            z_out: int, hdraft_out: Optional[int], stream: Optional[int]) -> int:
+    n = len(slots)
+    return lib().outlets_predict_prefill(ctx, n, i32_array(slots), i32_array(lens), h_low, h_mid, h_high,
+                                         row_stride, z_out, hdraft_out, stream)
+
+
+def outlets_predict_step(ctx, slots, h_low: int, h_mid: int, h_high: int, row_stride: int,
+                         z_out: int, hdraft_out: Optional[int], stream: Optional[int]) -> int:
+    return lib().outlets_predict_step(ctx, len(slots), i32_array(slots), h_low, h_mid, h_high, row_stride,
+                                      z_out, hdraft_out, stream)
+
+
+def outlets_release(ctx, slots) -> int:
+    return lib().outlets_release(ctx, len(slots), i32_array(slots))
+
+
+def outlets_get_meta(ctx, what: int, cap: int):
+    buf = (C.c_int32 * max(1, cap))()
+    n = C.c_int64()
+    check(lib().outlets_get_meta(ctx, what, buf, cap, C.byref(n)), "outlets_get_meta")
+    return list(buf[:n.value])
+
+
+def outlets_get_buffer(ctx, which: int, dst: int, nbytes: int, stream: Optional[int]) -> int:
+    n = C.c_int64()
+    check(lib().outlets_get_buffer(ctx, which, dst, nbytes, C.byref(n), stream), "outlets_get_buffer")
+    return n.value
+
+
+def outlets_buffer_size(ctx, which: int) -> int:
+    n = C.c_int64()
+    lib().outlets_get_buffer(ctx, which, None, 0, C.byref(n), None)
+    return n.value
+
+
+def outlets_profile_enable(ctx, enable: bool) -> None:
+    check(lib().outlets_profile_enable(ctx, int(bool(enable))), "outlets_profile_enable")
+
+
+def outlets_profile_read(ctx, call: int, which: int):
+    ms, n = C.c_double(), C.c_int64()
+    check(lib().outlets_profile_read(ctx, call, which, C.byref(ms), C.byref(n)), "outlets_profile_read")
+    return ms.value, n.value
+
+
+def outlets_varlen_meta(lens):
+    n = len(lens)
+    T = int(sum(int(x) for x in lens))
+    cu, pos, last = (C.c_int32 * (n + 1))(), (C.c_int32 * max(1, T))(), (C.c_int32 * max(1, n))()
+    check(lib().outlets_varlen_meta(n, i32_array(lens), cu, pos, last), "outlets_varlen_meta")
+    return list(cu), list(pos[:T]), list(last[:n])
+
+
+class Pager:
+    """Host-only page allocator of the library (no GPU involved)."""
+
+    def __init__(self, num_pages: int, page_size: int, max_slots: int, max_seq_len: int):
+        self.h = C.c_void_p()
+        check(lib().outlets_pager_create(num_pages, page_size, max_slots, max_seq_len, C.byref(self.h)),
+              "outlets_pager_create")
+        self.max_slots = max_slots
+        self.max_pages = -(-max_seq_len // page_size)
+
+    def prefill(self, slots, lens) -> int:
+        return lib().outlets_pager_prefill(self.h, len(slots), i32_array(slots), i32_array(lens))
+
+    def step(self, slots) -> int:
+        return lib().outlets_pager_step(self.h, len(slots), i32_array(slots))
+
+    def release(self, slots) -> int:
+        return lib().outlets_pager_release(self.h, len(slots), i32_array(slots))
+
+    def read(self, what: int):
+        cap = self.max_slots * self.max_pages
+        buf = (C.c_int32 * cap)()
+        n = C.c_int64()
+        check(lib().outlets_pager_read(self.h, what, buf, cap, C.byref(n)), "outlets_pager_read")
+        return list(buf[:n.value])
+
+    def close(self):
+        if self.h:
+            lib().outlets_pager_destroy(self.h)
+            self.h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

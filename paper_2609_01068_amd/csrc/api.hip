@@ -1,0 +1,729 @@
+// C ABI of the library: context set-up, the two prediction calls, slot
+// release and inspection.  Host work per call is validation, page allocation
+// (Pager), and one pinned host->device copy of the call's request metadata
+// and page-table updates; everything else is kernels queued on the caller's
+// stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "outlets.h"
+#include "pager.hpp"
+
+using namespace outlets;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int rc, const std::string& msg) {
+    g_err = msg;
+    return rc;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(OUTLETS_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                              \
+    do {                                                 \
+        hipError_t e_ = (expr);                          \
+        if (e_ != hipSuccess) return hip_fail(e_, what); \
+    } while (0)
+
+size_t fmt_bytes(int fmt) { return fmt == FMT_F32 ? 4 : (fmt == FMT_BF16 ? 2 : 1); }
+
+constexpr int kHeadSplits = 8;
+
+}  // namespace
+
+struct outlets_ctx {
+    outlets_config cfg{};
+    outlets_weights w{};
+    int device = 0;
+    int act_fmt = 0, w_fmt = 0, small_fmt = 0;  // small_fmt: gains and head
+    int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
+    std::unique_ptr<Pager> pager;
+    int max_pages = 0;
+
+    std::vector<void*> allocs;
+    void* kpool = nullptr;
+    void* vpool = nullptr;
+    int32_t* page_table = nullptr;
+    float* pool_sum = nullptr;
+    float* cos_t = nullptr;
+    float* sin_t = nullptr;
+
+    float* r_f = nullptr;   // residual stream: f_ctx, x1, x2, h_draft (aliases unless kept)
+    float* r_x1 = nullptr;
+    float* r_x2 = nullptr;
+    float* r_h = nullptr;
+    void* a_norm = nullptr;
+    void* b_norm = nullptr;
+    void* qkv = nullptr;
+    void* attn = nullptr;
+    void* mlp = nullptr;
+    float* pooled = nullptr;
+    uint16_t* pooled_bf16 = nullptr;
+    float* head_part = nullptr;
+    int32_t* tok_slot = nullptr;
+    int32_t* tok_pos = nullptr;
+    int32_t* last_idx = nullptr;
+    int32_t* d_meta = nullptr;   // req_off | req_slot | req_start | page updates
+    int64_t meta_cap = 0;        // int32 entries
+
+    int32_t* h_stage[2] = {nullptr, nullptr};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    bool ev_used[2] = {false, false};
+    int stage = 0;
+
+    int32_t last_n = 0, last_T = 0;
+
+    // per-kernel timing (outlets_profile_enable)
+    bool prof_on = false;
+    struct Mark { int phase, which; hipEvent_t a, b; };
+    std::vector<Mark> marks;
+    std::vector<hipEvent_t> spare;
+    int prof_phase = 0;                      // 0: prefill call, 1: step call
+    double prof_ms[2][OUTLETS_K_COUNT] = {};
+    int64_t prof_n[2][OUTLETS_K_COUNT] = {};
+
+    ~outlets_ctx() {
+        (void)hipSetDevice(device);
+        (void)hipDeviceSynchronize();
+        for (void* p : allocs) (void)hipFree(p);
+        for (int i = 0; i < 2; ++i) {
+            if (h_stage[i]) (void)hipHostFree(h_stage[i]);
+            if (ev[i]) (void)hipEventDestroy(ev[i]);
+        }
+        for (auto& m : marks) { (void)hipEventDestroy(m.a); (void)hipEventDestroy(m.b); }
+        for (auto e : spare) (void)hipEventDestroy(e);
+    }
+
+    hipEvent_t take_event() {
+        hipEvent_t e = nullptr;
+        if (!spare.empty()) { e = spare.back(); spare.pop_back(); return e; }
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+
+    int alloc(void** p, size_t bytes) {
+        if (bytes == 0) bytes = 256;
+        hipError_t e = hipMalloc(p, bytes);
+        if (e != hipSuccess) {
+            *p = nullptr;
+            return fail(OUTLETS_ERR_NOMEM, std::string("hipMalloc of ") + std::to_string(bytes) +
+                                               " bytes failed: " + hipGetErrorString(e));
+        }
+        allocs.push_back(*p);
+        return OUTLETS_OK;
+    }
+};
+
+namespace {
+
+// Records an event pair around the launches of one kernel group when
+// profiling is on.
+struct KTimer {
+    outlets_ctx* c;
+    int which;
+    hipStream_t st;
+    hipEvent_t a = nullptr;
+    KTimer(outlets_ctx* c_, int w, hipStream_t s) : c(c_), which(w), st(s) {
+        if (c->prof_on && (a = c->take_event())) (void)hipEventRecord(a, st);
+    }
+    ~KTimer() {
+        if (!a) return;
+        hipEvent_t b = c->take_event();
+        if (!b) { c->spare.push_back(a); return; }
+        (void)hipEventRecord(b, st);
+        c->marks.push_back({c->prof_phase, which, a, b});
+    }
+};
+
+void collect_marks(outlets_ctx* c) {
+    for (auto& m : c->marks) {
+        float ms = 0.f;
+        if (hipEventSynchronize(m.b) == hipSuccess && hipEventElapsedTime(&ms, m.a, m.b) == hipSuccess) {
+            c->prof_ms[m.phase][m.which] += ms;
+            c->prof_n[m.phase][m.which] += 1;
+        }
+        c->spare.push_back(m.a);
+        c->spare.push_back(m.b);
+    }
+    c->marks.clear();
+}
+
+int check_config(const outlets_config& c, const char** why) {
+    auto bad = [&](int rc, const char* msg) { *why = msg; return rc; };
+    if (c.d_model <= 0 || c.n_q_heads <= 0 || c.n_kv_heads <= 0 || c.ffn_dim <= 0 || c.head_hidden <= 0)
+        return bad(OUTLETS_ERR_INVALID_ARG, "dimensions must be positive");
+    if (c.max_slots <= 0 || c.max_seq_len <= 0 || c.num_pages <= 0 || c.max_batch_tokens <= 0 ||
+        c.max_batch_requests <= 0)
+        return bad(OUTLETS_ERR_INVALID_ARG, "capacities must be positive");
+    if (!(c.rms_eps >= 0.f) || !(c.rope_theta > 0.0))
+        return bad(OUTLETS_ERR_INVALID_ARG, "rms_eps must be >= 0 and rope_theta > 0");
+    if (!attn_supported(c.n_q_heads, c.n_kv_heads, c.head_dim))
+        return bad(OUTLETS_ERR_UNSUPPORTED, "attention supports head_dim 64/128 and n_q/n_kv in {1,2,4,8}");
+    if (c.page_size != 16) return bad(OUTLETS_ERR_UNSUPPORTED, "page_size must be 16");
+    if (c.weight_fmt < 0 || c.weight_fmt > 2 || c.act_fmt < 0 || c.act_fmt > 1)
+        return bad(OUTLETS_ERR_UNSUPPORTED, "unknown weight or activation format");
+    if (c.weight_fmt == OUTLETS_FMT_F32 && c.act_fmt != OUTLETS_FMT_F32)
+        return bad(OUTLETS_ERR_UNSUPPORTED, "f32 weights need f32 activations");
+    if (c.weight_fmt != OUTLETS_FMT_F32 && c.act_fmt != OUTLETS_FMT_BF16)
+        return bad(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 weights need bf16 activations");
+    *why = nullptr;
+    return OUTLETS_OK;
+}
+
+GemmA gemm_a(const void* p, int64_t ld, int64_t kseg) {
+    GemmA a{};
+    a.p[0] = p;
+    a.ld = ld;
+    a.kseg = static_cast<int32_t>(kseg);
+    return a;
+}
+
+GemmB gemm_b1(const void* p, const void* scale, int64_t rows, int64_t ld) {
+    GemmB b{};
+    b.p[0] = p;
+    b.scale[0] = static_cast<const uint16_t*>(scale);
+    b.nend[0] = b.nend[1] = b.nend[2] = static_cast<int32_t>(rows);
+    b.ld = ld;
+    return b;
+}
+
+GemmC gemm_c(void* c, int64_t ldc, const float* resid = nullptr, int64_t ldr = 0) {
+    GemmC r{};
+    r.c = c;
+    r.ldc = ldc;
+    r.resid = resid;
+    r.ldr = ldr;
+    return r;
+}
+
+// The per-layer GEMM descriptors; M varies per call.
+struct LayerGemms {
+    GemmA a_fuse, a_qkv, a_o, a_gu, a_down, a_head;
+    GemmB b_fuse, b_qkv, b_o, b_gu, b_down, b_head;
+    int64_t n_gu;
+};
+
+LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, const void* hh,
+                       int64_t row_stride) {
+    LayerGemms g{};
+    const auto& w = c->w;
+    const int64_t d = c->d;
+    g.a_fuse = gemm_a(hl, row_stride, d);
+    g.a_fuse.p[1] = hm;
+    g.a_fuse.p[2] = hh;
+    g.b_fuse = gemm_b1(w.w_proj, w.s_proj, d, 3 * d);
+    g.a_qkv = gemm_a(c->a_norm, d, d);
+    g.b_qkv = gemm_b1(w.w_q, w.s_q, c->qdim, d);
+    g.b_qkv.p[1] = w.w_k;
+    g.b_qkv.p[2] = w.w_v;
+    g.b_qkv.scale[1] = static_cast<const uint16_t*>(w.s_k);
+    g.b_qkv.scale[2] = static_cast<const uint16_t*>(w.s_v);
+    g.b_qkv.nend[0] = static_cast<int32_t>(c->qdim);
+    g.b_qkv.nend[1] = static_cast<int32_t>(c->qdim + c->kvdim);
+    g.b_qkv.nend[2] = static_cast<int32_t>(c->qkv_dim);
+    g.a_o = gemm_a(c->attn, c->qdim, c->qdim);
+    g.b_o = gemm_b1(w.w_o, w.s_o, d, c->qdim);
+    g.a_gu = gemm_a(c->b_norm, d, d);
+    g.b_gu = gemm_b1(w.w_gate, w.s_gate, c->F, d);
+    g.b_gu.p[1] = w.w_up;
+    g.b_gu.scale[1] = static_cast<const uint16_t*>(w.s_up);
+    if (c->w_fmt == FMT_F32) {
+        g.n_gu = c->F;            // dual-row VALU kernel
+    } else {
+        g.b_gu.paired = 1;        // 32-row gate/up interleave
+        g.n_gu = 2 * c->F;
+    }
+    g.a_down = gemm_a(c->mlp, c->F, c->F);
+    g.b_down = gemm_b1(w.w_down, w.s_down, d, c->F);
+    if (c->w_fmt == FMT_F32)
+        g.a_head = gemm_a(c->pooled, 2 * d, 2 * d);
+    else
+        g.a_head = gemm_a(c->pooled_bf16, 2 * d, 2 * d);
+    g.b_head = gemm_b1(w.head_w1, nullptr, c->H1, 2 * d);
+    return g;
+}
+
+int check_gemms(const outlets_ctx* c) {
+    // Dummy 16-byte aligned pointers stand in for the per-call A operands.
+    LayerGemms g = layer_gemms(c, c->a_norm, c->a_norm, c->a_norm, c->d);
+    const char* why = nullptr;
+    const int af = c->act_fmt, wf = c->w_fmt;
+    const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
+    int rc;
+    if ((rc = gemm_check(af, wf, EPI_STORE_F32, 1, c->d, 3 * c->d, g.a_fuse, g.b_fuse, 1, &why)) ||
+        (rc = gemm_check(af, wf, EPI_STORE_ACT, 1, c->qkv_dim, c->d, g.a_qkv, g.b_qkv, 1, &why)) ||
+        (rc = gemm_check(af, wf, EPI_RESID_F32, 1, c->d, c->qdim, g.a_o, g.b_o, 1, &why)) ||
+        (rc = gemm_check(af, wf, EPI_SWIGLU, 1, g.n_gu, c->d, g.a_gu, g.b_gu, 1, &why)) ||
+        (rc = gemm_check(af, wf, EPI_RESID_F32, 1, c->d, c->F, g.a_down, g.b_down, 1, &why)) ||
+        (rc = gemm_check(af, hf, EPI_PARTIAL, 1, c->H1, 2 * c->d, g.a_head, g.b_head, kHeadSplits, &why)))
+        return fail(rc, std::string("unsupported shape: ") + why);
+    return OUTLETS_OK;
+}
+
+// Queue the draft layer + head for `T` tokens of `n` requests whose
+// metadata is already on the device.
+int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const void* hm,
+              const void* hh, int64_t row_stride, float* z_out, void* hdraft_out, hipStream_t st) {
+    const int af = c->act_fmt, wf = c->w_fmt;
+    const int64_t d = c->d;
+    LayerGemms g = layer_gemms(c, hl, hm, hh, row_stride);
+    const int32_t* req_off = c->d_meta;
+    const int32_t* req_slot = c->d_meta + (n + 1);
+    const int32_t* req_start = c->d_meta + (n + 1) + n;
+    const float eps = c->cfg.rms_eps;
+
+    // Eq. 1: f_ctx = W_proj [h_low | h_mid | h_high]
+    { KTimer t(c, OUTLETS_K_FUSE_GEMM, st);
+      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(c->r_f, d), 1, st); }
+    { KTimer t(c, OUTLETS_K_NORM, st);
+      launch_rmsnorm(af, c->small_fmt, T, d, c->r_f, d, c->w.gamma_attn, eps, c->a_norm, d, nullptr, 0, st); }
+    { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
+      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, d, g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st); }
+    { KTimer t(c, OUTLETS_K_ROPE_KV, st);
+      launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
+                     c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
+                     c->cfg.head_dim, st); }
+    { KTimer t(c, OUTLETS_K_ATTN, st);
+      launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
+                        c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
+                        c->cfg.n_kv_heads, c->cfg.head_dim, st); }
+    { KTimer t(c, OUTLETS_K_O_GEMM, st);
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st); }
+    { KTimer t(c, OUTLETS_K_NORM, st);
+      launch_rmsnorm(af, c->small_fmt, T, d, c->r_x1, d, c->w.gamma_mlp, eps, c->b_norm, d, nullptr, 0, st); }
+    { KTimer t(c, OUTLETS_K_GATE_UP_GEMM, st);
+      gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(c->mlp, c->F), 1, st); }
+    { KTimer t(c, OUTLETS_K_DOWN_GEMM, st);
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(c->r_x2, d, c->r_x1, d), 1, st); }
+    { KTimer t(c, OUTLETS_K_NORM, st);
+      launch_rmsnorm(af, c->small_fmt, T, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d, st); }
+    uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
+    { KTimer t(c, OUTLETS_K_POOL, st);
+      if (prefill)
+          launch_pool_prefill(n, d, c->r_h, d, req_off, req_slot, c->pool_sum, c->pooled, pb, st);
+      else
+          launch_pool_step(n, d, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
+    const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
+    GemmC hc = gemm_c(c->head_part, c->H1);
+    hc.split_stride = static_cast<int64_t>(n) * c->H1;
+    { KTimer t(c, OUTLETS_K_HEAD, st);
+      gemm_launch(af, hf, EPI_PARTIAL, n, c->H1, 2 * d, g.a_head, g.b_head, hc, kHeadSplits, st);
+      launch_head_finish(c->small_fmt, n, c->H1, kHeadSplits, c->head_part, c->w.head_b1, c->w.head_w2,
+                         c->w.head_b2, z_out, st); }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return OUTLETS_OK;
+}
+
+// Stage req_off | req_slot | req_start | updates into pinned memory and copy to the device.
+int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const int32_t* slots,
+                const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
+                hipStream_t st) {
+    const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size());
+    if (count > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
+    const int s = c->stage;
+    if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
+    int32_t* h = c->h_stage[s];
+    std::memcpy(h, off.data(), sizeof(int32_t) * (n + 1));
+    std::memcpy(h + n + 1, slots, sizeof(int32_t) * n);
+    std::memcpy(h + 2 * n + 1, start.data(), sizeof(int32_t) * n);
+    if (!updates.empty()) std::memcpy(h + 3 * n + 1, updates.data(), sizeof(int32_t) * updates.size());
+    HIP_TRY(hipMemcpyAsync(c->d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
+    HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
+    c->ev_used[s] = true;
+    c->stage ^= 1;
+    KTimer t(c, OUTLETS_K_META, st);
+    if (!updates.empty())
+        launch_scatter_i32(static_cast<int>(updates.size() / 2), c->d_meta + 3 * n + 1, c->page_table, st);
+    launch_build_tokens(n, c->d_meta, c->d_meta + n + 1, c->d_meta + 2 * n + 1, c->tok_slot,
+                        c->tok_pos, c->last_idx, st);
+    return OUTLETS_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_states(const outlets_ctx* c, const void* hl, const void* hm, const void* hh,
+                 int64_t row_stride, const float* z_out) {
+    if (!hl || !hm || !hh || !z_out) return fail(OUTLETS_ERR_INVALID_ARG, "null state or output pointer");
+    if (row_stride < c->d) return fail(OUTLETS_ERR_INVALID_ARG, "row_stride < d_model");
+    if (c->act_fmt == FMT_BF16 && (row_stride % 8 || !aligned16(hl) || !aligned16(hm) || !aligned16(hh)))
+        return fail(OUTLETS_ERR_UNSUPPORTED, "bf16 states need 16-byte aligned rows (row_stride % 8 == 0)");
+    return OUTLETS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* outlets_last_error(void) { return g_err.c_str(); }
+
+int outlets_create(const outlets_config* cfg, const outlets_weights* weights, int32_t device,
+                   outlets_ctx** out) {
+    if (!out) return fail(OUTLETS_ERR_INVALID_ARG, "out is null");
+    *out = nullptr;
+    if (!cfg || !weights) return fail(OUTLETS_ERR_INVALID_ARG, "null config or weights");
+    const char* why = nullptr;
+    int rc = check_config(*cfg, &why);
+    if (rc) return fail(rc, std::string("config: ") + why);
+    const outlets_weights& w = *weights;
+    const void* req[] = {w.w_proj, w.w_q, w.w_k, w.w_v, w.w_o, w.w_gate, w.w_up, w.w_down,
+                         w.gamma_attn, w.gamma_mlp, w.gamma_final, w.head_w1, w.head_b1,
+                         w.head_w2, w.head_b2};
+    for (const void* p : req)
+        if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "a weight pointer is null");
+    if (cfg->weight_fmt == OUTLETS_FMT_E4M3) {
+        const void* sc[] = {w.s_proj, w.s_q, w.s_k, w.s_v, w.s_o, w.s_gate, w.s_up, w.s_down};
+        for (const void* p : sc)
+            if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
+    }
+    HIP_TRY(hipSetDevice(device), "hipSetDevice");
+
+    std::unique_ptr<outlets_ctx> c;
+    try {
+        c.reset(new outlets_ctx());
+        c->pager.reset(new Pager(cfg->num_pages, cfg->page_size, cfg->max_slots, cfg->max_seq_len));
+    } catch (const std::bad_alloc&) {
+        return fail(OUTLETS_ERR_NOMEM, "host allocation failed");
+    }
+    c->cfg = *cfg;
+    c->w = w;
+    c->device = device;
+    c->act_fmt = cfg->act_fmt;
+    c->w_fmt = cfg->weight_fmt;
+    c->small_fmt = (cfg->weight_fmt == OUTLETS_FMT_F32) ? FMT_F32 : FMT_BF16;
+    c->d = cfg->d_model;
+    c->qdim = static_cast<int64_t>(cfg->n_q_heads) * cfg->head_dim;
+    c->kvdim = static_cast<int64_t>(cfg->n_kv_heads) * cfg->head_dim;
+    c->qkv_dim = c->qdim + 2 * c->kvdim;
+    c->F = cfg->ffn_dim;
+    c->H1 = cfg->head_hidden;
+    c->max_pages = c->pager->max_pages_per_seq();
+
+    const size_t ab = fmt_bytes(c->act_fmt);
+    const int64_t Tm = cfg->max_batch_tokens, Bm = std::max(cfg->max_batch_requests, 1);
+    const int64_t hd = cfg->head_dim;
+    const size_t pool_elems = static_cast<size_t>(cfg->num_pages) * cfg->n_kv_heads * 16 * hd;
+    void* p = nullptr;
+#define ALLOC(dst, bytes)                                              \
+    do {                                                               \
+        if ((rc = c->alloc(&p, (bytes))) != OUTLETS_OK) return rc;     \
+        dst = decltype(dst)(p);                                        \
+    } while (0)
+    ALLOC(c->kpool, pool_elems * ab);
+    ALLOC(c->vpool, pool_elems * ab);
+    ALLOC(c->page_table, sizeof(int32_t) * c->pager->table().size());
+    ALLOC(c->pool_sum, sizeof(float) * cfg->max_slots * c->d);
+    ALLOC(c->cos_t, sizeof(float) * cfg->max_seq_len * (hd / 2));
+    ALLOC(c->sin_t, sizeof(float) * cfg->max_seq_len * (hd / 2));
+    const bool keep = cfg->keep_intermediates != 0;
+    ALLOC(c->r_f, sizeof(float) * Tm * c->d);
+    if (keep) {
+        ALLOC(c->r_x1, sizeof(float) * Tm * c->d);
+        ALLOC(c->r_x2, sizeof(float) * Tm * c->d);
+        ALLOC(c->r_h, sizeof(float) * Tm * c->d);
+    } else {
+        c->r_x1 = c->r_x2 = c->r_h = c->r_f;
+    }
+    ALLOC(c->a_norm, ab * Tm * c->d);
+    if (keep) ALLOC(c->b_norm, ab * Tm * c->d);
+    else c->b_norm = c->a_norm;
+    ALLOC(c->qkv, ab * Tm * c->qkv_dim);
+    ALLOC(c->attn, ab * Tm * c->qdim);
+    ALLOC(c->mlp, ab * Tm * c->F);
+    ALLOC(c->pooled, sizeof(float) * Bm * 2 * c->d);
+    ALLOC(c->pooled_bf16, sizeof(uint16_t) * Bm * 2 * c->d);
+    ALLOC(c->head_part, sizeof(float) * kHeadSplits * Bm * c->H1);
+    ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
+    ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
+    ALLOC(c->last_idx, sizeof(int32_t) * Bm);
+    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm);
+    ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
+#undef ALLOC
+    for (int i = 0; i < 2; ++i) {
+        HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->meta_cap, 0),
+                "hipHostMalloc");
+        HIP_TRY(hipEventCreateWithFlags(&c->ev[i], hipEventDisableTiming), "hipEventCreate");
+    }
+    if ((rc = check_gemms(c.get())) != OUTLETS_OK) return rc;
+
+    // RoPE tables: angle p * theta^(-2c/hd) evaluated in float64, stored float32.
+    {
+        const int64_t half = hd / 2;
+        std::vector<float> cs(static_cast<size_t>(cfg->max_seq_len) * half), sn(cs.size());
+        for (int64_t pos = 0; pos < cfg->max_seq_len; ++pos)
+            for (int64_t ch = 0; ch < half; ++ch) {
+                const double ang = static_cast<double>(pos) *
+                                   std::pow(cfg->rope_theta, -2.0 * static_cast<double>(ch) / static_cast<double>(hd));
+                cs[pos * half + ch] = static_cast<float>(std::cos(ang));
+                sn[pos * half + ch] = static_cast<float>(std::sin(ang));
+            }
+        HIP_TRY(hipMemcpy(c->cos_t, cs.data(), sizeof(float) * cs.size(), hipMemcpyHostToDevice), "hipMemcpy");
+        HIP_TRY(hipMemcpy(c->sin_t, sn.data(), sizeof(float) * sn.size(), hipMemcpyHostToDevice), "hipMemcpy");
+    }
+    HIP_TRY(hipMemset(c->page_table, 0xFF, sizeof(int32_t) * c->pager->table().size()), "hipMemset");
+    HIP_TRY(hipMemset(c->pool_sum, 0, sizeof(float) * cfg->max_slots * c->d), "hipMemset");
+    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    *out = c.release();
+    return OUTLETS_OK;
+}
+
+int outlets_destroy(outlets_ctx* ctx) {
+    delete ctx;
+    return OUTLETS_OK;
+}
+
+int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
+                            const int32_t* lens, const void* h_low, const void* h_mid,
+                            const void* h_high, int64_t row_stride, float* z_out,
+                            void* hdraft_out, void* stream) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (n_req < 0 || n_req > ctx->cfg.max_batch_requests)
+        return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
+    if (n_req == 0) return OUTLETS_OK;
+    if (!slots || !lens) return fail(OUTLETS_ERR_INVALID_ARG, "null slots or lens");
+    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, z_out);
+    if (rc) return rc;
+    if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
+        return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    std::vector<int32_t> updates;
+    const char* why = "";
+    ctx->prof_phase = 0;
+    rc = ctx->pager->prefill(n_req, slots, lens, &updates, &why);
+    if (rc) return fail(rc, why);
+    std::vector<int32_t> off(n_req + 1), start(n_req, 0);
+    int64_t T = 0;
+    off[0] = 0;
+    for (int i = 0; i < n_req; ++i) {
+        T += lens[i];
+        off[i + 1] = static_cast<int32_t>(std::min<int64_t>(T, INT32_MAX));
+    }
+    if (T > ctx->cfg.max_batch_tokens) {
+        ctx->pager->release(n_req, slots, &why);   // undo: same free set as before
+        return fail(OUTLETS_ERR_INVALID_ARG, "total prompt tokens exceed max_batch_tokens");
+    }
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, st);
+    if (rc == OUTLETS_OK)
+        rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, z_out,
+                       hdraft_out, st);
+    if (rc) {
+        std::string msg = g_err;
+        ctx->pager->release(n_req, slots, &why);
+        return fail(rc, msg);
+    }
+    ctx->last_n = n_req;
+    ctx->last_T = static_cast<int32_t>(T);
+    return OUTLETS_OK;
+}
+
+int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h_low,
+                         const void* h_mid, const void* h_high, int64_t row_stride, float* z_out,
+                         void* hdraft_out, void* stream) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (n_req < 0 || n_req > ctx->cfg.max_batch_requests || n_req > ctx->cfg.max_batch_tokens)
+        return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
+    if (n_req == 0) return OUTLETS_OK;
+    if (!slots) return fail(OUTLETS_ERR_INVALID_ARG, "null slots");
+    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, z_out);
+    if (rc) return rc;
+    if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
+        return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    std::vector<int32_t> updates;
+    const char* why = "";
+    ctx->prof_phase = 1;
+    rc = ctx->pager->step(n_req, slots, &updates, &why);
+    if (rc) return fail(rc, why);
+    std::vector<int32_t> off(n_req + 1), start(n_req);
+    for (int i = 0; i <= n_req; ++i) off[i] = i;
+    for (int i = 0; i < n_req; ++i) start[i] = ctx->pager->seq_len(slots[i]) - 1;
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, st);
+    if (rc == OUTLETS_OK)
+        rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, z_out, hdraft_out, st);
+    if (rc) return rc;   // device work may be partly queued; the slot lengths advanced
+    ctx->last_n = n_req;
+    ctx->last_T = n_req;
+    return OUTLETS_OK;
+}
+
+int outlets_release(outlets_ctx* ctx, int32_t n, const int32_t* slots) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (n < 0 || (n > 0 && !slots)) return fail(OUTLETS_ERR_INVALID_ARG, "bad slot list");
+    const char* why = "";
+    int rc = ctx->pager->release(n, slots, &why);
+    return rc ? fail(rc, why) : OUTLETS_OK;
+}
+
+int outlets_get_meta(outlets_ctx* ctx, int32_t what, int32_t* out, int64_t cap, int64_t* n_out) {
+    if (!ctx || !out || !n_out) return fail(OUTLETS_ERR_INVALID_ARG, "null argument");
+    const int64_t n = ctx->last_n, T = ctx->last_T;
+    int64_t count = 0;
+    const void* dev = nullptr;
+    switch (what) {
+        case OUTLETS_META_PAGE_TABLE: count = static_cast<int64_t>(ctx->pager->table().size()); break;
+        case OUTLETS_META_SEQ_LEN: count = ctx->pager->max_slots(); break;
+        case OUTLETS_META_DEV_PAGE_TABLE: count = static_cast<int64_t>(ctx->pager->table().size()); dev = ctx->page_table; break;
+        case OUTLETS_META_DEV_CU_SEQLENS: count = n + 1; dev = ctx->d_meta; break;
+        case OUTLETS_META_DEV_POSITIONS: count = T; dev = ctx->tok_pos; break;
+        case OUTLETS_META_DEV_LAST_IDX: count = n; dev = ctx->last_idx; break;
+        case OUTLETS_META_DEV_TOKEN_SLOT: count = T; dev = ctx->tok_slot; break;
+        default: return fail(OUTLETS_ERR_INVALID_ARG, "unknown metadata id");
+    }
+    *n_out = count;
+    if (cap < count) return fail(OUTLETS_ERR_INVALID_ARG, "output capacity too small");
+    if (!dev) {
+        const auto& v = (what == OUTLETS_META_PAGE_TABLE) ? ctx->pager->table() : ctx->pager->seq_lens();
+        std::memcpy(out, v.data(), sizeof(int32_t) * count);
+        return OUTLETS_OK;
+    }
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
+    if (count) HIP_TRY(hipMemcpy(out, dev, sizeof(int32_t) * count, hipMemcpyDeviceToHost), "hipMemcpy");
+    return OUTLETS_OK;
+}
+
+int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbytes, int64_t* n_bytes,
+                       void* stream) {
+    if (!ctx || !n_bytes) return fail(OUTLETS_ERR_INVALID_ARG, "null argument");
+    const int64_t T = ctx->last_T, n = ctx->last_n, d = ctx->d;
+    const int64_t ab = static_cast<int64_t>(fmt_bytes(ctx->act_fmt));
+    const bool keep = ctx->cfg.keep_intermediates != 0;
+    const void* src = nullptr;
+    int64_t size = 0;
+    bool needs_keep = true;
+    switch (which) {
+        case OUTLETS_BUF_FUSED: src = ctx->r_f; size = 4 * T * d; break;
+        case OUTLETS_BUF_NORM_ATTN: src = ctx->a_norm; size = ab * T * d; break;
+        case OUTLETS_BUF_Q: src = nullptr; size = ab * T * ctx->qdim; break;
+        case OUTLETS_BUF_ATTN: src = ctx->attn; size = ab * T * ctx->qdim; break;
+        case OUTLETS_BUF_X1: src = ctx->r_x1; size = 4 * T * d; break;
+        case OUTLETS_BUF_NORM_MLP: src = ctx->b_norm; size = ab * T * d; break;
+        case OUTLETS_BUF_MLP_ACT: src = ctx->mlp; size = ab * T * ctx->F; break;
+        case OUTLETS_BUF_X2: src = ctx->r_x2; size = 4 * T * d; break;
+        case OUTLETS_BUF_HDRAFT: src = ctx->r_h; size = 4 * T * d; needs_keep = false; break;
+        case OUTLETS_BUF_POOLED: src = ctx->pooled; size = 4 * n * 2 * d; needs_keep = false; break;
+        case OUTLETS_BUF_K_POOL:
+        case OUTLETS_BUF_V_POOL:
+            src = which == OUTLETS_BUF_K_POOL ? ctx->kpool : ctx->vpool;
+            size = ab * static_cast<int64_t>(ctx->cfg.num_pages) * ctx->cfg.n_kv_heads * 16 * ctx->cfg.head_dim;
+            needs_keep = false;
+            break;
+        default: return fail(OUTLETS_ERR_INVALID_ARG, "unknown buffer id");
+    }
+    *n_bytes = size;
+    if (needs_keep && !keep) return fail(OUTLETS_ERR_INVALID_ARG, "buffer needs keep_intermediates");
+    if (!dst || nbytes < size) return fail(OUTLETS_ERR_INVALID_ARG, "destination too small");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (which == OUTLETS_BUF_Q) {
+        // queries live in the first n_q*hd columns of the fused qkv rows
+        HIP_TRY(hipMemcpy2DAsync(dst, ab * ctx->qdim, ctx->qkv, ab * ctx->qkv_dim, ab * ctx->qdim, T,
+                                 hipMemcpyDeviceToDevice, st), "hipMemcpy2DAsync");
+    } else if (size) {
+        HIP_TRY(hipMemcpyAsync(dst, src, size, hipMemcpyDeviceToDevice, st), "hipMemcpyAsync");
+    }
+    return OUTLETS_OK;
+}
+
+int outlets_profile_enable(outlets_ctx* ctx, int32_t enable) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    (void)hipSetDevice(ctx->device);
+    collect_marks(ctx);
+    for (int p = 0; p < 2; ++p)
+        for (int i = 0; i < OUTLETS_K_COUNT; ++i) { ctx->prof_ms[p][i] = 0.0; ctx->prof_n[p][i] = 0; }
+    ctx->prof_on = enable != 0;
+    return OUTLETS_OK;
+}
+
+int outlets_profile_read(outlets_ctx* ctx, int32_t call, int32_t which, double* total_ms,
+                         int64_t* launches) {
+    if (!ctx || !total_ms || !launches || which < 0 || which >= OUTLETS_K_COUNT || call < 0 || call > 1)
+        return fail(OUTLETS_ERR_INVALID_ARG, "bad argument");
+    (void)hipSetDevice(ctx->device);
+    collect_marks(ctx);
+    *total_ms = ctx->prof_ms[call][which];
+    *launches = ctx->prof_n[call][which];
+    return OUTLETS_OK;
+}
+
+int outlets_varlen_meta(int32_t n_req, const int32_t* lens, int32_t* cu_out, int32_t* pos_out,
+                        int32_t* last_out) {
+    if (n_req < 0 || (n_req > 0 && !lens)) return fail(OUTLETS_ERR_INVALID_ARG, "bad lengths");
+    int rc = varlen_meta(n_req, lens, cu_out, pos_out, last_out);
+    return rc ? fail(rc, "lengths must be >= 1 and sum below 2^31") : OUTLETS_OK;
+}
+
+struct outlets_pager {
+    Pager p;
+    outlets_pager(int32_t a, int32_t b, int32_t c, int32_t d) : p(a, b, c, d) {}
+};
+
+int outlets_pager_create(int32_t num_pages, int32_t page_size, int32_t max_slots, int32_t max_seq_len,
+                         outlets_pager** out) {
+    if (!out) return fail(OUTLETS_ERR_INVALID_ARG, "out is null");
+    *out = nullptr;
+    if (num_pages <= 0 || page_size <= 0 || max_slots <= 0 || max_seq_len <= 0)
+        return fail(OUTLETS_ERR_INVALID_ARG, "sizes must be positive");
+    try {
+        *out = new outlets_pager(num_pages, page_size, max_slots, max_seq_len);
+    } catch (const std::bad_alloc&) {
+        return fail(OUTLETS_ERR_NOMEM, "host allocation failed");
+    }
+    return OUTLETS_OK;
+}
+
+int outlets_pager_destroy(outlets_pager* p) {
+    delete p;
+    return OUTLETS_OK;
+}
+
+int outlets_pager_prefill(outlets_pager* p, int32_t n, const int32_t* slots, const int32_t* lens) {
+    if (!p || n < 0 || (n > 0 && (!slots || !lens))) return fail(OUTLETS_ERR_INVALID_ARG, "bad argument");
+    const char* why = "";
+    int rc = p->p.prefill(n, slots, lens, nullptr, &why);
+    return rc ? fail(rc, why) : OUTLETS_OK;
+}
+
+int outlets_pager_step(outlets_pager* p, int32_t n, const int32_t* slots) {
+    if (!p || n < 0 || (n > 0 && !slots)) return fail(OUTLETS_ERR_INVALID_ARG, "bad argument");
+    const char* why = "";
+    int rc = p->p.step(n, slots, nullptr, &why);
+    return rc ? fail(rc, why) : OUTLETS_OK;
+}
+
+int outlets_pager_release(outlets_pager* p, int32_t n, const int32_t* slots) {
+    if (!p || n < 0 || (n > 0 && !slots)) return fail(OUTLETS_ERR_INVALID_ARG, "bad argument");
+    const char* why = "";
+    int rc = p->p.release(n, slots, &why);
+    return rc ? fail(rc, why) : OUTLETS_OK;
+}
+
+int outlets_pager_read(outlets_pager* p, int32_t what, int32_t* out, int64_t cap, int64_t* n_out) {
+    if (!p || !out || !n_out) return fail(OUTLETS_ERR_INVALID_ARG, "null argument");
+    const std::vector<int32_t>* v;
+    if (what == OUTLETS_META_PAGE_TABLE) v = &p->p.table();
+    else if (what == OUTLETS_META_SEQ_LEN) v = &p->p.seq_lens();
+    else return fail(OUTLETS_ERR_INVALID_ARG, "unknown metadata id");
+    *n_out = static_cast<int64_t>(v->size());
+    if (cap < *n_out) return fail(OUTLETS_ERR_INVALID_ARG, "output capacity too small");
+    std::memcpy(out, v->data(), sizeof(int32_t) * v->size());
+    return OUTLETS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// Launch interface of the gfx950 kernels (library-internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace outlets {
+
+// ---------------------------------------------------------------- GEMM
+// C[M, N] = A[M, K] . B[N, K]^T, fp32 accumulation.
+//
+// A: activations; the K axis may come from up to three pointers, each
+//    supplying `kseg` consecutive columns (the fused projection reads
+//    h_low | h_mid | h_high this way without materialising the concat).
+// B: weights, [out, in] row-major.  Rows come from up to three pointers
+//    (`nend[s]` = exclusive end of block s in logical rows: Wq | Wk | Wv), or,
+//    with `paired`, logical rows alternate 32 rows of p[0] and 32 rows of
+//    p[1] (gate | up) so one output tile holds matching gate/up columns.
+//    E4M3 weights carry one bf16 scale per physical row.
+struct GemmA {
+    const void* p[3];
+    int64_t ld;      // elements between rows
+    int32_t kseg;    // columns per pointer (K when one pointer)
+};
+
+struct GemmB {
+    const void* p[3];
+    const uint16_t* scale[3];
+    int32_t nend[3];
+    int32_t paired;
+    int64_t ld;
+};
+
+enum Epilogue : int {
+    EPI_STORE_F32 = 0,  // C (f32) = acc
+    EPI_STORE_ACT = 1,  // C (act format) = acc
+    EPI_RESID_F32 = 2,  // C (f32) = resid + acc   (C may alias resid)
+    EPI_SWIGLU = 3,     // C (act) [M, N/2] = silu(gate) * up   (requires paired B)
+    EPI_PARTIAL = 4     // C (f32) + split * split_stride = acc over the split's K range
+};
+
+struct GemmC {
+    void* c;
+    int64_t ldc;
+    const float* resid;
+    int64_t ldr;
+    int64_t split_stride;
+};
+
+enum Fmt : int { FMT_F32 = 0, FMT_BF16 = 1, FMT_E4M3 = 2 };
+
+// Checks the shape against what the selected kernel handles; returns 0 or an
+// OUTLETS_ERR_* code (and a reason).  act_fmt is the format of A and of act
+// outputs; w_fmt of B.
+int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
+               const GemmB& b, int splits, const char** why);
+void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
+                 const GemmB& b, const GemmC& c, int splits, hipStream_t st);
+
+// ---------------------------------------------------------------- elementwise / rows
+// Per-call token metadata from per-request arrays:
+//   req[0..n]      : token offsets (cu), req_off
+//   req_slot[n], req_start[n] (first position of the call's tokens)
+// writes tok_slot[T], tok_pos[T], last_idx[n].
+void launch_build_tokens(int n_req, const int32_t* req_off, const int32_t* req_slot,
+                         const int32_t* req_start, int32_t* tok_slot, int32_t* tok_pos,
+                         int32_t* last_idx, hipStream_t st);
+void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStream_t st);
+
+// y = x / sqrt(mean(x^2) + eps) * gamma per row; x fp32; y in act format
+// (either output may be null; y2 is an fp32 copy and may alias x).
+void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x, int64_t ldx,
+                    const void* gamma, float eps, void* y, int64_t ldy, float* y2,
+                    int64_t ldy2, hipStream_t st);
+
+// RoPE on q (in place) and k; k, v scattered into the page pools.
+void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t* tok_slot,
+                    const int32_t* tok_pos, const int32_t* page_table, int max_pages,
+                    void* kpool, void* vpool, const float* cos_t, const float* sin_t,
+                    int n_q, int n_kv, int hd, hipStream_t st);
+
+bool attn_supported(int n_q, int n_kv, int hd);
+
+// Attention of each token's queries over its slot's cached keys 0..pos.
+void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* out,
+                       int64_t ldo, const int32_t* tok_slot, const int32_t* tok_pos,
+                       const int32_t* page_table, int max_pages, const void* kpool,
+                       const void* vpool, int n_q, int n_kv, int hd, hipStream_t st);
+
+// Prefill pooling: pool_sum[slot] = sum of the request's h rows; pooled[i] =
+// [sum / n ; h[last]] (fp32, plus a bf16 copy when pooled_bf16 != null).
+void launch_pool_prefill(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_off,
+                         const int32_t* req_slot, float* pool_sum, float* pooled,
+                         uint16_t* pooled_bf16, hipStream_t st);
+// Step pooling: pool_sum[slot] += h[i]; pooled[i] = [pool_sum / (start + 1) ; h[i]].
+void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_slot,
+                      const int32_t* req_start, float* pool_sum, float* pooled,
+                      uint16_t* pooled_bf16, hipStream_t st);
+
+// z[i] = w2 . relu(sum_s partial[s][i] + b1) + b2
+void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
+                        const void* b1, const void* w2, const void* b2, float* z, hipStream_t st);
+
+void launch_copy_rows_act(int act_fmt, int rows, int d, const float* src, int64_t lds,
+                          void* dst, int64_t ldd, hipStream_t st);
+
+}  // namespace outlets

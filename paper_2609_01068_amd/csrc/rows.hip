@@ -1,0 +1,242 @@
+// Row-wise kernels of the draft layer and the length head (HBM-bound):
+// per-call token metadata, RMSNorm, rotary embedding + paged KV write,
+// segmented mean/last pooling and the head's ReLU + final dot product.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace outlets {
+
+namespace {
+
+__global__ void build_tokens_kernel(const int32_t* req_off, const int32_t* req_slot,
+                                    const int32_t* req_start, int32_t* tok_slot,
+                                    int32_t* tok_pos, int32_t* last_idx) {
+    const int i = blockIdx.x;
+    const int b = req_off[i], e = req_off[i + 1];
+    const int slot = req_slot[i], start = req_start[i];
+    for (int t = b + threadIdx.x; t < e; t += blockDim.x) {
+        tok_slot[t] = slot;
+        tok_pos[t] = start + (t - b);
+    }
+    if (threadIdx.x == 0) last_idx[i] = e - 1;
+}
+
+__global__ void scatter_kernel(int n, const int32_t* pairs, int32_t* dst) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) dst[pairs[2 * i]] = pairs[2 * i + 1];
+}
+
+// One 256-thread block per row.
+template <typename TY, typename TG>
+__global__ void __launch_bounds__(256)
+rmsnorm_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
+               int64_t ldy, float* y2, int64_t ldy2) {
+    __shared__ float red[4];
+    const int64_t row = blockIdx.x;
+    const float* xr = x + row * ldx;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < d; c += 256) {
+        float v = xr[c];
+        ss = fmaf(v, v, ss);
+    }
+    ss = block_sum<256>(ss, red);
+    const float inv = 1.0f / sqrtf(ss / d + eps);
+    for (int c = threadIdx.x; c < d; c += 256) {
+        float v = xr[c] * inv * load_act<TG>(gamma + c);
+        if (y) store_act<TY>(y + row * ldy + c, v);
+        if (y2) y2[row * ldy2 + c] = v;
+    }
+}
+
+// One block per token; thread work items are rotation pairs of the q and k
+// heads and value elements.
+template <typename T>
+__global__ void __launch_bounds__(256)
+rope_kv_kernel(T* qkv, int64_t ld, const int32_t* tok_slot, const int32_t* tok_pos,
+               const int32_t* page_table, int max_pages, T* kpool, T* vpool,
+               const float* cos_t, const float* sin_t, int n_q, int n_kv, int hd) {
+    const int64_t t = blockIdx.x;
+    const int pos = tok_pos[t], slot = tok_slot[t];
+    const int half = hd / 2;
+    const int page = page_table[(int64_t)slot * max_pages + pos / 16];
+    const int off = pos % 16;
+    T* row = qkv + t * ld;
+    const float* cr = cos_t + (int64_t)pos * half;
+    const float* sr = sin_t + (int64_t)pos * half;
+    const int n_rot = (n_q + n_kv) * half;
+    for (int w = threadIdx.x; w < n_rot; w += 256) {
+        const int h = w / half, c = w % half;
+        T* base = row + h * hd;
+        const float x1 = load_act<T>(base + c), x2 = load_act<T>(base + c + half);
+        const float cs = cr[c], sn = sr[c];
+        const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
+        if (h < n_q) {
+            store_act<T>(base + c, y1);
+            store_act<T>(base + c + half, y2);
+        } else {
+            const int g = h - n_q;
+            T* dst = kpool + (((int64_t)page * n_kv + g) * 16 + off) * hd;
+            store_act<T>(dst + c, y1);
+            store_act<T>(dst + c + half, y2);
+        }
+    }
+    const T* vrow = row + (n_q + n_kv) * hd;
+    for (int w = threadIdx.x; w < n_kv * hd; w += 256) {
+        const int g = w / hd, c = w % hd;
+        vpool[(((int64_t)page * n_kv + g) * 16 + off) * hd + c] = vrow[w];
+    }
+}
+
+// grid (n_req, ceil(d / 256)): each thread sums one column of a request in
+// row order (deterministic, independent of the batch).
+__global__ void __launch_bounds__(256)
+pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
+                    const int32_t* req_slot, float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
+    const int i = blockIdx.x;
+    const int c = blockIdx.y * 256 + threadIdx.x;
+    if (c >= d) return;
+    const int b = req_off[i], e = req_off[i + 1];
+    float s = 0.f;
+    for (int r = b; r < e; ++r) s += h[(int64_t)r * ldh + c];
+    pool_sum[(int64_t)req_slot[i] * d + c] = s;
+    const float mean = s / static_cast<float>(e - b);
+    const float last = h[(int64_t)(e - 1) * ldh + c];
+    pooled[(int64_t)i * 2 * d + c] = mean;
+    pooled[(int64_t)i * 2 * d + d + c] = last;
+    if (pooled_bf16) {
+        pooled_bf16[(int64_t)i * 2 * d + c] = f32_to_bf16(mean);
+        pooled_bf16[(int64_t)i * 2 * d + d + c] = f32_to_bf16(last);
+    }
+}
+
+__global__ void __launch_bounds__(256)
+pool_step_kernel(int d, const float* h, int64_t ldh, const int32_t* req_slot,
+                 const int32_t* req_start, float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
+    const int i = blockIdx.x;
+    const int c = blockIdx.y * 256 + threadIdx.x;
+    if (c >= d) return;
+    const float x = h[(int64_t)i * ldh + c];
+    float* ps = pool_sum + (int64_t)req_slot[i] * d + c;
+    const float s = *ps + x;
+    *ps = s;
+    const float mean = s / static_cast<float>(req_start[i] + 1);
+    pooled[(int64_t)i * 2 * d + c] = mean;
+    pooled[(int64_t)i * 2 * d + d + c] = x;
+    if (pooled_bf16) {
+        pooled_bf16[(int64_t)i * 2 * d + c] = f32_to_bf16(mean);
+        pooled_bf16[(int64_t)i * 2 * d + d + c] = f32_to_bf16(x);
+    }
+}
+
+template <typename TW>
+__global__ void __launch_bounds__(256)
+head_finish_kernel(int h1, int splits, int n_req, const float* partial, const TW* b1,
+                   const TW* w2, const TW* b2, float* z) {
+    __shared__ float red[4];
+    const int i = blockIdx.x;
+    float acc = 0.f;
+    for (int j = threadIdx.x; j < h1; j += 256) {
+        float v = load_act<TW>(b1 + j);
+        for (int s = 0; s < splits; ++s) v += partial[((int64_t)s * n_req + i) * h1 + j];
+        acc = fmaf(fmaxf(v, 0.f), load_act<TW>(w2 + j), acc);
+    }
+    acc = block_sum<256>(acc, red);
+    if (threadIdx.x == 0) z[i] = acc + load_act<TW>(b2);
+}
+
+template <typename T>
+__global__ void copy_rows_kernel(int d, const float* src, int64_t lds, T* dst, int64_t ldd) {
+    const int64_t r = blockIdx.x;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) store_act<T>(dst + r * ldd + c, src[r * lds + c]);
+}
+
+}  // namespace
+
+void launch_build_tokens(int n_req, const int32_t* req_off, const int32_t* req_slot,
+                         const int32_t* req_start, int32_t* tok_slot, int32_t* tok_pos,
+                         int32_t* last_idx, hipStream_t st) {
+    if (n_req <= 0) return;
+    hipLaunchKernelGGL(build_tokens_kernel, dim3(n_req), dim3(256), 0, st, req_off, req_slot,
+                       req_start, tok_slot, tok_pos, last_idx);
+}
+
+void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStream_t st) {
+    if (n_pairs <= 0) return;
+    hipLaunchKernelGGL(scatter_kernel, dim3((n_pairs + 255) / 256), dim3(256), 0, st, n_pairs,
+                       pairs, dst);
+}
+
+void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x, int64_t ldx,
+                    const void* gamma, float eps, void* y, int64_t ldy, float* y2,
+                    int64_t ldy2, hipStream_t st) {
+    if (rows <= 0) return;
+    if (act_fmt == FMT_F32) {
+        hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(rows), dim3(256), 0, st, d, x, ldx,
+                           static_cast<const float*>(gamma), eps, static_cast<float*>(y), ldy, y2, ldy2);
+    } else if (gamma_fmt == FMT_F32) {
+        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, float>), dim3(rows), dim3(256), 0, st, d, x, ldx,
+                           static_cast<const float*>(gamma), eps, static_cast<bf16_t*>(y), ldy, y2, ldy2);
+    } else {
+        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(rows), dim3(256), 0, st, d, x, ldx,
+                           static_cast<const bf16_t*>(gamma), eps, static_cast<bf16_t*>(y), ldy, y2, ldy2);
+    }
+}
+
+void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t* tok_slot,
+                    const int32_t* tok_pos, const int32_t* page_table, int max_pages,
+                    void* kpool, void* vpool, const float* cos_t, const float* sin_t,
+                    int n_q, int n_kv, int hd, hipStream_t st) {
+    if (ntok <= 0) return;
+    if (act_fmt == FMT_F32)
+        hipLaunchKernelGGL((rope_kv_kernel<float>), dim3(ntok), dim3(256), 0, st,
+                           static_cast<float*>(qkv), ld, tok_slot, tok_pos, page_table, max_pages,
+                           static_cast<float*>(kpool), static_cast<float*>(vpool), cos_t, sin_t,
+                           n_q, n_kv, hd);
+    else
+        hipLaunchKernelGGL((rope_kv_kernel<bf16_t>), dim3(ntok), dim3(256), 0, st,
+                           static_cast<bf16_t*>(qkv), ld, tok_slot, tok_pos, page_table, max_pages,
+                           static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool), cos_t, sin_t,
+                           n_q, n_kv, hd);
+}
+
+void launch_pool_prefill(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_off,
+                         const int32_t* req_slot, float* pool_sum, float* pooled,
+                         uint16_t* pooled_bf16, hipStream_t st) {
+    if (n_req <= 0) return;
+    hipLaunchKernelGGL(pool_prefill_kernel, dim3(n_req, (d + 255) / 256), dim3(256), 0, st, d, h,
+                       ldh, req_off, req_slot, pool_sum, pooled, pooled_bf16);
+}
+
+void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_slot,
+                      const int32_t* req_start, float* pool_sum, float* pooled,
+                      uint16_t* pooled_bf16, hipStream_t st) {
+    if (n_req <= 0) return;
+    hipLaunchKernelGGL(pool_step_kernel, dim3(n_req, (d + 255) / 256), dim3(256), 0, st, d, h, ldh,
+                       req_slot, req_start, pool_sum, pooled, pooled_bf16);
+}
+
+void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
+                        const void* b1, const void* w2, const void* b2, float* z, hipStream_t st) {
+    if (n_req <= 0) return;
+    if (w_fmt == FMT_F32)
+        hipLaunchKernelGGL((head_finish_kernel<float>), dim3(n_req), dim3(256), 0, st, h1, splits,
+                           n_req, partial, static_cast<const float*>(b1),
+                           static_cast<const float*>(w2), static_cast<const float*>(b2), z);
+    else
+        hipLaunchKernelGGL((head_finish_kernel<bf16_t>), dim3(n_req), dim3(256), 0, st, h1, splits,
+                           n_req, partial, static_cast<const bf16_t*>(b1),
+                           static_cast<const bf16_t*>(w2), static_cast<const bf16_t*>(b2), z);
+}
+
+void launch_copy_rows_act(int act_fmt, int rows, int d, const float* src, int64_t lds, void* dst,
+                          int64_t ldd, hipStream_t st) {
+    if (rows <= 0) return;
+    if (act_fmt == FMT_F32)
+        hipLaunchKernelGGL((copy_rows_kernel<float>), dim3(rows), dim3(256), 0, st, d, src, lds,
+                           static_cast<float*>(dst), ldd);
+    else
+        hipLaunchKernelGGL((copy_rows_kernel<bf16_t>), dim3(rows), dim3(256), 0, st, d, src, lds,
+                           static_cast<bf16_t*>(dst), ldd);
+}
+
+}  // namespace outlets

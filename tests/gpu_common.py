@@ -1,0 +1,105 @@
+"""Helpers shared by the GPU parity tests: build the HIP predictor and the
+fp64 oracle from the same seeded synthetic inputs, and compare them."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+from synth import (DraftShape, make_lengths, make_prompt_states, make_step_states,
+                   make_weights, workload)
+from oracle import oracle_from_workload, states_to_f64
+
+# Tolerances: draft states as a relative Frobenius error per request, the
+# predicted log-length as |dz| <= tol * max(|z_ref|, rms(z_ref)).
+TOL_HDRAFT = {"f32": 1e-4, "bf16": 2e-2, "e4m3": 6e-2}
+TOL_Z = {"f32": 1e-4, "bf16": 1e-2, "e4m3": 1e-2}
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2609_01068_amd import binding
+    binding.lib()          # raises if the library is missing: no fallback
+
+
+def rel_fro(got: np.ndarray, ref: np.ndarray) -> float:
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
+
+
+def z_errors(z_got, z_ref):
+    z_got, z_ref = np.asarray(z_got, np.float64), np.asarray(z_ref, np.float64)
+    floor = max(float(np.sqrt(np.mean(z_ref ** 2))), 1e-30)
+    return np.abs(z_got - z_ref) / np.maximum(np.abs(z_ref), floor)
+
+
+def tensor_to_f64(t) -> np.ndarray:
+    import torch
+    return t.detach().to(torch.float64).cpu().numpy()
+
+
+@dataclasses.dataclass
+class Case:
+    wl: object
+    weights: dict
+    lens: np.ndarray
+    states: list            # stored (low, mid, high) packed
+    fmt: str
+
+
+def make_case(cfg_id: int, lens=None, seed: int = 0, **overrides) -> Case:
+    wl = workload(cfg_id, **overrides)
+    W = make_weights(wl, seed)
+    if lens is None:
+        lens = make_lengths(wl, seed)
+    lens = np.asarray(lens, dtype=np.int32)
+    st = make_prompt_states(wl, lens, seed)
+    return Case(wl, W, lens, st, wl.weight_fmt)
+
+
+def make_predictor(case: Case, *, max_slots=None, num_pages=None, max_seq_len=None,
+                   max_batch_tokens=None, max_batch_requests=None, keep=False):
+    from paper_2609_01068_amd.predictor import OutletsPredictor
+    wl, lens = case.wl, case.lens
+    T = int(lens.sum())
+    n = len(lens)
+    max_seq = max_seq_len or int(lens.max()) + 64
+    slots_n = max_slots or max(n, 1)
+    pages = num_pages or (slots_n * (-(-max_seq // 16)))
+    return OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, case.weights,
+                            max_slots=slots_n, max_seq_len=max_seq, num_pages=pages,
+                            max_batch_tokens=max_batch_tokens or max(T, 1),
+                            max_batch_requests=max_batch_requests or max(n, 1),
+                            keep_intermediates=keep)
+
+
+def device_states(case: Case, arrays=None):
+    from paper_2609_01068_amd.predictor import to_device
+    arrays = case.states if arrays is None else arrays
+    return [to_device(a) for a in arrays]
+
+
+def oracle_for(case: Case):
+    return oracle_from_workload(case.wl, case.weights)
+
+
+def oracle_states(case: Case, arrays=None):
+    return states_to_f64(case.states if arrays is None else arrays, case.wl.act_fmt)
+
+
+def step_inputs(case: Case, step: int, requests=None):
+    return make_step_states(case.wl, len(case.lens), step, requests=requests)
+
+
+def reduced_shape(d=512, n_q=8, n_kv=2, hd=128, ffn=1024, head_hidden=256, theta=5e5):
+    return DraftShape(d=d, n_q=n_q, n_kv=n_kv, head_dim=hd, ffn=ffn, head_hidden=head_hidden,
+                      rope_theta=theta)

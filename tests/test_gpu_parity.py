@@ -1,0 +1,258 @@
+"""GPU parity of the HIP path against the fp64 oracle (MI355X, through the C ABI).
+
+Every case prints its name before touching the GPU.  Tolerances: draft
+states as relative Frobenius error per request (1e-4 fp32, 2e-2 bf16, 6e-2
+e4m3 weights); predicted log-length |dz| <= 1e-2 * max(|z|, rms(z)) (1e-4 for
+fp32); integer metadata bit-exact.
+"""
+import numpy as np
+import pytest
+
+from oracle import meta
+from gpu_common import (TOL_HDRAFT, TOL_Z, device_states, make_case, make_predictor, oracle_for,
+                        oracle_states, reduced_shape, rel_fro, require_gpu, say, step_inputs,
+                        tensor_to_f64, z_errors)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _split(arr, lens):
+    off = np.concatenate([[0], np.cumsum(lens)])
+    return [arr[off[i]:off[i + 1]] for i in range(len(lens))]
+
+
+def _check_meta(pred, lens, slots, alloc):
+    from paper_2609_01068_amd import binding as B
+    assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_CU_SEQLENS), meta.cu_seqlens(lens))
+    assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_POSITIONS), meta.positions(lens))
+    assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_LAST_IDX), meta.last_idx(lens))
+    assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_TOKEN_SLOT), np.repeat(slots, lens))
+    table = alloc.table().reshape(-1)
+    assert np.array_equal(pred.meta(B.OUTLETS_META_PAGE_TABLE), table)
+    dev = pred.meta(B.OUTLETS_META_DEV_PAGE_TABLE)
+    used = table >= 0
+    assert np.array_equal(dev[used], table[used])
+
+
+def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
+    fmt = case.fmt
+    lens = case.lens
+    n = len(lens)
+    slots = list(range(n))
+    pred = make_predictor(case, keep=keep, max_seq_len=int(lens.max()) + steps + 16)
+    H = device_states(case)
+    z, hd = pred.prefill(slots, lens, *H, want_hdraft=True)
+    z = tensor_to_f64(z)
+    hd = tensor_to_f64(hd)
+    orc = oracle_for(case)
+    O = oracle_states(case)
+    off = np.concatenate([[0], np.cumsum(lens)])
+    states, z_ref = [], []
+    caps = []
+    for i in range(n):
+        cap = {}
+        zi, hi, st = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O), capture=cap)
+        z_ref.append(zi)
+        states.append(st)
+        caps.append(cap)
+        err = rel_fro(hd[off[i]:off[i + 1]], hi)
+        assert err <= TOL_HDRAFT[fmt], (i, err)
+    ez = z_errors(z, z_ref)
+    say(f"  prefill z max rel err {ez.max():.3e}; z_ref rms {np.sqrt(np.mean(np.square(z_ref))):.3e}")
+    assert ez.max() <= TOL_Z[fmt], ez
+    if keep and check_intermediates:
+        import torch
+        names = [("FUSED", "fused", torch.float32), ("X1", "x1", torch.float32),
+                 ("X2", "x2", torch.float32), ("HDRAFT", "hdraft", torch.float32)]
+        act = pred.act_dtype
+        names += [("NORM_ATTN", "norm_attn", act), ("Q", "q", act), ("ATTN", "attn", act),
+                  ("NORM_MLP", "norm_mlp", act), ("MLP_ACT", "mlp_act", act)]
+        for buf, key, dt in names:
+            g = tensor_to_f64(pred.buffer(buf, dt))
+            g = g.reshape(int(lens.sum()), -1)
+            worst = max(rel_fro(g[off[i]:off[i + 1]], caps[i][key]) for i in range(n))
+            say(f"  {buf:9s} worst rel err {worst:.3e}")
+            assert worst <= TOL_HDRAFT[fmt], (buf, worst)
+        pooled = tensor_to_f64(pred.buffer("POOLED", torch.float32)).reshape(n, -1)
+        for i in range(n):
+            assert rel_fro(pooled[i], caps[i]["pooled"]) <= TOL_HDRAFT[fmt]
+    alloc = meta.PageAllocator(pred.cfg.num_pages, 16, pred.cfg.max_slots, pred.cfg.max_seq_len)
+    assert alloc.prefill(slots, lens) == meta.OK
+    _check_meta(pred, lens, np.array(slots), alloc)
+
+    for t in range(1, steps + 1):
+        S = step_inputs(case, t)
+        zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True)
+        zs, hs = tensor_to_f64(zs), tensor_to_f64(hs)
+        zr, hr = orc.step(states, *oracle_states(case, S))
+        for i in range(n):
+            assert rel_fro(hs[i], hr[i]) <= TOL_HDRAFT[fmt], (t, i)
+        ez = z_errors(zs, zr)
+        assert ez.max() <= TOL_Z[fmt], (t, ez)
+        assert alloc.step(slots) == meta.OK
+        from paper_2609_01068_amd import binding as B
+        assert np.array_equal(pred.meta(B.OUTLETS_META_PAGE_TABLE), alloc.table().reshape(-1))
+        assert np.array_equal(pred.meta(B.OUTLETS_META_SEQ_LEN), alloc.seq_lens())
+        assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_POSITIONS), np.asarray(lens) + t - 1)
+    say(f"  {steps} decode steps match")
+    pred.close()
+
+
+def test_tiny_fp32_prefill_intermediates_and_steps():
+    say("case: tiny fp32 shape (d=256), 4 requests U[16,64], 8 steps")
+    _run_prefill_case(make_case(0), keep=True, steps=8)
+
+
+def test_bf16_reduced_shape_ragged_tiles_and_steps():
+    say("case: bf16 d=512 8q/2kv hd128 F1024, lens [1,17,100,300,33], 3 steps")
+    case = make_case(1, lens=[1, 17, 100, 300, 33], shape=reduced_shape(), n_req=5)
+    _run_prefill_case(case, keep=True, steps=3)
+
+
+def test_e4m3_reduced_shape_gqa8_and_steps():
+    say("case: e4m3 weights d=512 8q/1kv hd128 F1024, lens [5,64,257,16], 2 steps")
+    case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=8, n_kv=1), n_req=4)
+    _run_prefill_case(case, keep=True, steps=2)
+
+
+def test_bf16_head_dim_64_shape():
+    say("case: bf16 d=256 4q/2kv hd64 F512, lens [3,40,90]")
+    case = make_case(1, lens=[3, 40, 90], shape=reduced_shape(d=256, n_q=4, n_kv=2, hd=64,
+                                                             ffn=512, head_hidden=256), n_req=3)
+    _run_prefill_case(case, keep=True, steps=1)
+
+
+def test_config1_full_shape_sampled_requests():
+    """8B shape, the 32-request lognormal batch; the oracle recomputes a sample."""
+    case = make_case(1)
+    lens = case.lens
+    say(f"case: config-1 8B bf16, B={len(lens)}, T={int(lens.sum())}, sampled oracle")
+    pred = make_predictor(case)
+    H = device_states(case)
+    z, hd = pred.prefill(list(range(len(lens))), lens, *H, want_hdraft=True)
+    z = tensor_to_f64(z)
+    assert np.all(np.isfinite(z))
+    order = np.argsort(lens)
+    sample = [int(order[0]), int(order[1]), int(order[len(order) // 3])]
+    orc = oracle_for(case)
+    off = np.concatenate([[0], np.cumsum(lens)])
+    from synth import make_prompt_states
+    sub = make_prompt_states(case.wl, lens, requests=sample)
+    O = oracle_states(case, sub)
+    z_ref = []
+    o_off = 0
+    hd64 = None
+    for i in sample:
+        n = int(lens[i])
+        zi, hi, _ = orc.prefill_one(*(x[o_off:o_off + n] for x in O))
+        o_off += n
+        z_ref.append(zi)
+        hd64 = tensor_to_f64(hd[off[i]:off[i + 1]])
+        err = rel_fro(hd64, hi)
+        say(f"  request {i} (n={n}) h_draft rel err {err:.3e}")
+        assert err <= TOL_HDRAFT["bf16"]
+    # z tolerance floors at the batch rms of the GPU's z over all requests
+    floor = float(np.sqrt(np.mean(z ** 2)))
+    dz = np.abs(z[sample] - np.array(z_ref)) / np.maximum(np.abs(z_ref), floor)
+    say(f"  sampled z rel err {dz.max():.3e}")
+    assert dz.max() <= TOL_Z["bf16"]
+    pred.close()
+
+
+def test_packing_and_permutation_invariance():
+    say("case: bf16 reduced shape, packed batch vs one-by-one vs permuted")
+    case = make_case(1, lens=[7, 130, 1, 64], shape=reduced_shape(), n_req=4)
+    lens = case.lens
+    pred = make_predictor(case, max_slots=16)
+    H = device_states(case)
+    z, hd = pred.prefill([0, 1, 2, 3], lens, *H, want_hdraft=True)
+    z, hd = tensor_to_f64(z), tensor_to_f64(hd)
+    pred.release([0, 1, 2, 3])
+    off = np.concatenate([[0], np.cumsum(lens)])
+    for i in range(4):
+        Hi = [x[off[i]:off[i + 1]].contiguous() for x in H]
+        zi, hi = pred.prefill([4 + i], [lens[i]], *Hi, want_hdraft=True)
+        assert tensor_to_f64(zi)[0] == z[i]
+        assert np.array_equal(tensor_to_f64(hi), hd[off[i]:off[i + 1]])
+    pred.release([4, 5, 6, 7])
+    perm = [2, 0, 3, 1]
+    import torch
+    Hp = [torch.cat([x[off[i]:off[i + 1]] for i in perm]) for x in H]
+    zp, _ = pred.prefill([8, 9, 10, 11], lens[perm], *Hp, want_hdraft=True)
+    assert np.array_equal(tensor_to_f64(zp), z[perm])
+    pred.close()
+
+
+def test_incremental_steps_equal_prefill_recompute():
+    say("case: bf16 reduced shape, prefill n then 18 steps vs prefill of n + t")
+    import torch
+    case = make_case(1, lens=[30, 15], shape=reduced_shape(), n_req=2)
+    pred = make_predictor(case, max_slots=8, max_seq_len=128, max_batch_tokens=256)
+    lens = case.lens
+    H = device_states(case)
+    pred.prefill([0, 1], lens, *H)
+    rows = [[x[:30] for x in H], [x[30:45] for x in H]]
+    for t in range(1, 19):
+        S = device_states(case, step_inputs(case, t))
+        zs, hs = pred.step([0, 1], *S, want_hdraft=True)
+        for i in range(2):
+            rows[i] = [torch.cat([rows[i][j], S[j][i:i + 1]]) for j in range(3)]
+        if t in (1, 2, 17, 18):
+            for i in range(2):
+                n = int(lens[i]) + t
+                zf, hf = pred.prefill([4 + i], [n], *[r.contiguous() for r in rows[i]], want_hdraft=True)
+                pred.release([4 + i])
+                a, b = tensor_to_f64(hs[i]), tensor_to_f64(hf[-1])
+                assert rel_fro(a, b) <= 1e-2, (t, i)
+                assert abs(float(zs[i]) - float(zf[0])) <= 1e-2 * max(abs(float(zf[0])), 0.05)
+    pred.close()
+
+
+def test_constant_token_prompt_at_long_length():
+    say("case: 8B bf16 shape, constant-token prompts n=1 and n=4096")
+    import torch
+    case = make_case(1, lens=[1, 4096], n_req=2)
+    pred = make_predictor(case, max_slots=4)
+    row = [x[:1] for x in device_states(case)]
+    z1, h1 = pred.prefill([0], [1], *row, want_hdraft=True)
+    long = [r.expand(4096, -1).contiguous() for r in row]
+    z2, h2 = pred.prefill([1], [4096], *long, want_hdraft=True)
+    h1, h2 = tensor_to_f64(h1), tensor_to_f64(h2)
+    spread = np.abs(h2 - h2[0:1]).max() / np.abs(h2[0]).max()
+    say(f"  row spread {spread:.3e}, |z1 - z2| = {abs(float(z1[0]) - float(z2[0])):.3e}")
+    assert spread <= 2e-2
+    assert rel_fro(h2[-1], h1[0]) <= 2e-2
+    assert abs(float(z1[0]) - float(z2[0])) <= 1e-2 * max(abs(float(z1[0])), 0.05)
+    pred.close()
+
+
+def test_error_paths_leave_state_unchanged():
+    say("case: error codes on a live context")
+    from paper_2609_01068_amd import binding as B
+    case = make_case(0, lens=[20, 20])
+    pred = make_predictor(case, max_slots=3, num_pages=4, max_seq_len=64)
+    H = device_states(case)
+    z, _ = pred.prefill([0, 1], [20, 20], *H)   # 2 pages each: pool full
+    table = pred.meta(B.OUTLETS_META_PAGE_TABLE)
+    codes = []
+    for call in (lambda: pred.prefill([0], [5], *[x[:5] for x in H]),
+                 lambda: pred.prefill([2], [5], *[x[:5] for x in H]),
+                 lambda: pred.prefill([2, 2], [1, 1], *[x[:2] for x in H]),
+                 lambda: pred.prefill([2], [0], *[x[:1] for x in H]),
+                 lambda: pred.step([2], *[x[:1] for x in H])):
+        with pytest.raises(B.OutletsError) as e:
+            call()
+        codes.append(e.value.rc)
+    assert codes == [B.OUTLETS_ERR_SLOT_BUSY, B.OUTLETS_ERR_OUT_OF_PAGES,
+                     B.OUTLETS_ERR_INVALID_ARG, B.OUTLETS_ERR_INVALID_ARG, B.OUTLETS_ERR_SLOT_EMPTY]
+    assert np.array_equal(pred.meta(B.OUTLETS_META_PAGE_TABLE), table)
+    z0, _ = pred.prefill([], [], *H)            # n_req == 0 is a no-op
+    pred.release([1])
+    z2, _ = pred.prefill([2], [20], *[x[20:40] for x in H])
+    assert abs(float(z2[0]) - float(z[1])) <= 1e-5 * max(abs(float(z[1])), 1e-3)
+    pred.close()
