@@ -76,7 +76,10 @@ enum {
  *   rope_theta, rms_eps: RoPE base and RMSNorm epsilon.
  *   weight_fmt: F32 (then act_fmt must be F32), BF16 or E4M3 (act BF16).
  *     With E4M3 only the eight big linears (proj, q, k, v, o, gate, up, down)
- *     are fp8; gains and the head are bf16.
+ *     are fp8; gains and the head are bf16.  BF16/E4M3 shapes need d_model,
+ *     n_q_heads*head_dim, n_kv_heads*head_dim and head_hidden to be
+ *     multiples of 256 and ffn_dim a multiple of 128 (the MFMA tiles);
+ *     outlets_create returns UNSUPPORTED otherwise.
  *   act_fmt: format of h_low/h_mid/h_high, of h_draft output and of the KV
  *     cache: F32 or BF16.
  *   page_size: tokens per KV page; must be 16.

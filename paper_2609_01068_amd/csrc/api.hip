@@ -5,6 +5,7 @@
 // stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <memory>
@@ -75,8 +76,10 @@ struct outlets_ctx {
     int32_t* tok_slot = nullptr;
     int32_t* tok_pos = nullptr;
     int32_t* last_idx = nullptr;
-    int32_t* d_meta = nullptr;   // req_off | req_slot | req_start | page updates
+    int32_t* d_meta = nullptr;   // req_off | req_slot | req_start | page updates | work list
     int64_t meta_cap = 0;        // int32 entries
+    int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
+    int32_t n_work = 0;
 
     int32_t* h_stage[2] = {nullptr, nullptr};
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -296,9 +299,14 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
                      c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
                      c->cfg.head_dim, st); }
     { KTimer t(c, OUTLETS_K_ATTN, st);
-      launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
-                        c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
-                        c->cfg.n_kv_heads, c->cfg.head_dim, st); }
+      if (prefill && c->n_work > 0)
+          launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->qkv, c->qkv_dim, c->attn, c->qdim,
+                              req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
+                              c->cfg.n_q_heads, c->cfg.n_kv_heads, st);
+      else
+          launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
+                            c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
+                            c->cfg.n_kv_heads, c->cfg.head_dim, st); }
     { KTimer t(c, OUTLETS_K_O_GEMM, st);
       gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st); }
     { KTimer t(c, OUTLETS_K_NORM, st);
@@ -316,10 +324,12 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
       else
           launch_pool_step(n, d, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
+    // bf16 heads read the hi/lo split of the pooled vector: 2n rows
+    const int head_rows = (wf == FMT_F32) ? n : 2 * n;
     GemmC hc = gemm_c(c->head_part, c->H1);
-    hc.split_stride = static_cast<int64_t>(n) * c->H1;
+    hc.split_stride = static_cast<int64_t>(head_rows) * c->H1;
     { KTimer t(c, OUTLETS_K_HEAD, st);
-      gemm_launch(af, hf, EPI_PARTIAL, n, c->H1, 2 * d, g.a_head, g.b_head, hc, kHeadSplits, st);
+      gemm_launch(af, hf, EPI_PARTIAL, head_rows, c->H1, 2 * d, g.a_head, g.b_head, hc, kHeadSplits, st);
       launch_head_finish(c->small_fmt, n, c->H1, kHeadSplits, c->head_part, c->w.head_b1, c->w.head_w2,
                          c->w.head_b2, z_out, st); }
     hipError_t e = hipGetLastError();
@@ -330,8 +340,9 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
 // Stage req_off | req_slot | req_start | updates into pinned memory and copy to the device.
 int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const int32_t* slots,
                 const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
-                hipStream_t st) {
-    const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size());
+                const std::vector<int32_t>& work, hipStream_t st) {
+    const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size()) +
+                          static_cast<int64_t>(work.size());
     if (count > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
@@ -340,6 +351,9 @@ int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const in
     std::memcpy(h + n + 1, slots, sizeof(int32_t) * n);
     std::memcpy(h + 2 * n + 1, start.data(), sizeof(int32_t) * n);
     if (!updates.empty()) std::memcpy(h + 3 * n + 1, updates.data(), sizeof(int32_t) * updates.size());
+    c->work_off = 3 * n + 1 + static_cast<int64_t>(updates.size());
+    c->n_work = static_cast<int32_t>(work.size() / 2);
+    if (!work.empty()) std::memcpy(h + c->work_off, work.data(), sizeof(int32_t) * work.size());
     HIP_TRY(hipMemcpyAsync(c->d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
@@ -350,6 +364,23 @@ int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const in
     launch_build_tokens(n, c->d_meta, c->d_meta + n + 1, c->d_meta + 2 * n + 1, c->tok_slot,
                         c->tok_pos, c->last_idx, st);
     return OUTLETS_OK;
+}
+
+// Prefill attention work items (request, 32-query tile), longest first:
+// a tile's cost is the number of 64-key tiles it visits.
+std::vector<int32_t> attention_work(int n, const int32_t* lens) {
+    std::vector<std::pair<int32_t, int32_t>> items;
+    for (int i = 0; i < n; ++i)
+        for (int t = 0; t * 32 < lens[i]; ++t) items.emplace_back(i, t);
+    auto cost = [&](const std::pair<int32_t, int32_t>& it) {
+        return std::min(it.second * 32 + 31, lens[it.first] - 1) / 64;
+    };
+    std::stable_sort(items.begin(), items.end(),
+                     [&](const auto& a, const auto& b) { return cost(a) > cost(b); });
+    std::vector<int32_t> out;
+    out.reserve(2 * items.size());
+    for (auto& it : items) { out.push_back(it.first); out.push_back(it.second); }
+    return out;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -443,12 +474,12 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->attn, ab * Tm * c->qdim);
     ALLOC(c->mlp, ab * Tm * c->F);
     ALLOC(c->pooled, sizeof(float) * Bm * 2 * c->d);
-    ALLOC(c->pooled_bf16, sizeof(uint16_t) * Bm * 2 * c->d);
-    ALLOC(c->head_part, sizeof(float) * kHeadSplits * Bm * c->H1);
+    ALLOC(c->pooled_bf16, sizeof(uint16_t) * 2 * Bm * 2 * c->d);
+    ALLOC(c->head_part, sizeof(float) * kHeadSplits * 2 * Bm * c->H1);
     ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->last_idx, sizeof(int32_t) * Bm);
-    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm);
+    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * (Tm / 32 + Bm);
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
@@ -516,7 +547,10 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
         ctx->pager->release(n_req, slots, &why);   // undo: same free set as before
         return fail(OUTLETS_ERR_INVALID_ARG, "total prompt tokens exceed max_batch_tokens");
     }
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, st);
+    std::vector<int32_t> work;
+    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim))
+        work = attention_work(n_req, lens);
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, work, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, z_out,
                        hdraft_out, st);
@@ -553,7 +587,7 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     std::vector<int32_t> off(n_req + 1), start(n_req);
     for (int i = 0; i <= n_req; ++i) off[i] = i;
     for (int i = 0; i < n_req; ++i) start[i] = ctx->pager->seq_len(slots[i]) - 1;
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, st);
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, std::vector<int32_t>(), st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, z_out, hdraft_out, st);
     if (rc) return rc;   // device work may be partly queued; the slot lengths advanced

@@ -10,7 +10,10 @@
 //
 // Score phase: lane = key (0..15) + 16 * part; each lane dots hd/4 channels
 // and two xor-shuffles complete the dot product.  Value phase: each lane owns
-// hd/64 output channels and reads them for all 16 keys of the page.
+// hd/64 output channels and reads them for all 16 keys of the page (value
+// pages are stored [hd][16 tokens]).
+//
+// Prefill (bf16, hd 128): a flash-attention kernel on MFMA, see below.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "outlets.h"
@@ -65,7 +68,7 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
         for (int k = 0; k < 16; ++k)
 #pragma unroll
             for (int d = 0; d < DV; ++d)
-                vv[k][d] = (pi * 16 + k < nkeys) ? load_act<T>(vb + k * HD + lane * DV + d) : 0.f;
+                vv[k][d] = (pi * 16 + k < nkeys) ? load_act<T>(vb + (lane * DV + d) * 16 + k) : 0.f;
         const bool valid = pi * 16 + key < nkeys;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
@@ -122,6 +125,166 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
     }
 }
 
+// ---------------------------------------------------------------- prefill, MFMA
+// One workgroup per (request, tile of 32 queries, KV head); wave w computes
+// query head g * G + w, so the G heads of a group share each K/V tile staged
+// in LDS.  Keys are visited in tiles of 64 (4 pages), up to the tile's last
+// query position (causal tile skipping).
+//
+// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
+// a lane then holds one query (column) and 16 keys per 32x32 block, so the
+// online softmax max/sum need one cross-half shuffle and the rescaling of the
+// output is lane-local.  The output is also kept transposed, O^T = V^T P^T,
+// which takes P straight from the score registers as the B operand.  For the
+// 8 key values a lane half supplies to one MFMA to be contiguous keys, A row
+// rho of the score MFMA reads key pi(rho), pi swapping bits 2 and 3 of rho:
+// with the 32x32 output layout (row = 8 (r / 4) + 4 half + r % 4 for
+// accumulator element r) element r then holds key 16 (r / 8) + 8 half + r % 8.
+// Values are staged as V^T [hd][64 keys], which the transposed value pages
+// make a plain 16-byte copy.
+__device__ __forceinline__ uint4 zero_tail_bf16x8(uint4 v, int valid) {
+    // keep the first `valid` (0..8) bf16 elements of v
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        if (e >= valid) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+template <int G>
+__global__ void __launch_bounds__(G * 64)
+attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
+                  const int32_t* req_off, const int32_t* req_slot, const int32_t* page_table,
+                  int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale) {
+    constexpr int HD = 128, NT = G * 64, BKV = 64, NS = HD / 16, NB = HD / 32;
+    __shared__ uint4 ks[BKV * 16];   // [key][16 chunks of 8 channels], chunk ^ (key % 16)
+    __shared__ uint4 vs[HD * 8];     // [channel][8 chunks of 8 keys], chunk ^ ((channel / 2) % 8)
+
+    const int r = work[2 * blockIdx.x], qt = work[2 * blockIdx.x + 1];
+    const int g = blockIdx.y;
+    const int tok0 = req_off[r], n = req_off[r + 1] - tok0, slot = req_slot[r];
+    const int qs = qt * 32;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int l32 = lane & 31, hf = lane >> 5;
+    const int h = g * G + w;
+    const int tp = min(qs + l32, n - 1);   // this lane's query position (tail lanes repeat the last)
+    const int32_t* prow = page_table + (int64_t)slot * max_pages;
+
+    bf16x8 qf[NS];
+    {
+        const bf16_t* qrow = qkv + (int64_t)(tok0 + tp) * ldq + h * HD + hf * 8;
+#pragma unroll
+        for (int s2 = 0; s2 < NS; ++s2)
+            qf[s2] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * s2));
+    }
+    f32x16 o[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[b][e] = 0.f;
+    float m = -INFINITY, lsum = 0.f;
+    const int maxpos = min(qs + 31, n - 1);
+    const int ntiles = maxpos / BKV + 1;
+    const int arow_key = (l32 & 19) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
+
+    for (int kt = 0; kt < ntiles; ++kt) {
+        const int k0 = kt * BKV;
+        __syncthreads();   // the previous tile's LDS reads are done
+        for (int c = tid; c < BKV * 16; c += NT) {
+            const int key = c >> 4, ch = c & 15, kpos = k0 + key;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (kpos < n) {
+                const int64_t page = prow[kpos >> 4];
+                v = *reinterpret_cast<const uint4*>(kpool + ((page * n_kv + g) * 16 + (kpos & 15)) * HD + ch * 8);
+            }
+            ks[key * 16 + (ch ^ (key & 15))] = v;
+        }
+        for (int c = tid; c < HD * 8; c += NT) {
+            const int ch = c >> 3, vc = c & 7, kp0 = k0 + vc * 8;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (kp0 < n) {
+                const int64_t page = prow[kp0 >> 4];
+                v = *reinterpret_cast<const uint4*>(vpool + ((page * n_kv + g) * HD + ch) * 16 + (kp0 & 15));
+                if (kp0 + 8 > n) v = zero_tail_bf16x8(v, n - kp0);   // keys past the prompt
+            }
+            vs[ch * 8 + (vc ^ ((ch >> 1) & 7))] = v;
+        }
+        __syncthreads();
+
+        f32x16 sacc[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
+            const int key = 32 * kb + arow_key;
+#pragma unroll
+            for (int s2 = 0; s2 < NS; ++s2) {
+                const int ch = 2 * s2 + hf;
+                const bf16x8 a = __builtin_bit_cast(bf16x8, ks[key * 16 + (ch ^ (key & 15))]);
+                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s2], sacc[kb], 0, 0, 0);
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int kpos = k0 + 32 * kb + 16 * (e >> 3) + 8 * hf + (e & 7);
+                const float v = (kpos <= tp) ? sacc[kb][e] * qscale : -INFINITY;
+                sacc[kb][e] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mn = fmaxf(m, mx);          // finite: key 0 <= every query position
+        const float corr = exp2f(m - mn);
+        float ps = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const float p = exp2f(sacc[kb][e] - mn);
+                sacc[kb][e] = p;
+                ps += p;
+            }
+        ps += __shfl_xor(ps, 32, 64);
+        lsum = lsum * corr + ps;
+        m = mn;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[b][e] *= corr;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                bf16x8 pb;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(sacc[kb][8 * u + e]);
+                const int ch = 4 * kb + 2 * u + hf;
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    const int row = 32 * b + l32;
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, vs[row * 8 + (ch ^ ((row >> 1) & 7))]);
+                    o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[b], 0, 0, 0);
+                }
+            }
+    }
+    if (qs + l32 < n) {
+        bf16_t* orow = out + (int64_t)(tok0 + qs + l32) * ldo + h * HD;
+        const float inv = 1.0f / lsum;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int c0 = 32 * b + 8 * j + 4 * hf;
+                uint2 pk;
+                pk.x = f32_to_bf16(o[b][4 * j + 0] * inv) | (uint32_t(f32_to_bf16(o[b][4 * j + 1] * inv)) << 16);
+                pk.y = f32_to_bf16(o[b][4 * j + 2] * inv) | (uint32_t(f32_to_bf16(o[b][4 * j + 3] * inv)) << 16);
+                *reinterpret_cast<uint2*>(orow + c0) = pk;
+            }
+    }
+}
+
 template <typename T, int HD>
 bool launch_hd(int G, int ntok, const void* q, int64_t ldq, void* out, int64_t ldo,
                const int32_t* tok_slot, const int32_t* tok_pos, const int32_t* page_table,
@@ -146,6 +309,36 @@ bool launch_hd(int G, int ntok, const void* q, int64_t ldq, void* out, int64_t l
 }
 
 }  // namespace
+
+bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd) {
+    const int G = n_q / n_kv;
+    return act_fmt == FMT_BF16 && hd == 128 && (G == 1 || G == 2 || G == 4 || G == 8);
+}
+
+void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64_t ldq, void* out,
+                         int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
+                         const int32_t* page_table, int max_pages, const void* kpool,
+                         const void* vpool, int n_q, int n_kv, hipStream_t st) {
+    if (n_work <= 0) return;
+    const int G = n_q / n_kv;
+    const float qscale = 1.4426950408889634f / sqrtf(128.0f);
+    dim3 grid(n_work, n_kv);
+#define OUTLETS_PF_G(GG)                                                                        \
+    case GG:                                                                                    \
+        hipLaunchKernelGGL((attn_prefill_mfma<GG>), grid, dim3(GG * 64), 0, st,                 \
+                           static_cast<const bf16_t*>(qkv), ldq, static_cast<bf16_t*>(out), ldo, \
+                           work, req_off, req_slot, page_table, max_pages,                      \
+                           static_cast<const bf16_t*>(kpool), static_cast<const bf16_t*>(vpool), \
+                           n_kv, qscale);                                                       \
+        break;
+    switch (G) {
+        OUTLETS_PF_G(1)
+        OUTLETS_PF_G(2)
+        OUTLETS_PF_G(4)
+        OUTLETS_PF_G(8)
+    }
+#undef OUTLETS_PF_G
+}
 
 bool attn_supported(int n_q, int n_kv, int hd) {
     if (n_kv <= 0 || n_q % n_kv) return false;

@@ -80,6 +80,14 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
                     int n_q, int n_kv, int hd, hipStream_t st);
 
 bool attn_supported(int n_q, int n_kv, int hd);
+bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd);
+
+// Causal prefill attention on MFMA (bf16, hd 128).  work[2 * i], work[2 * i + 1]
+// = (request, 32-query tile) of workgroup row i; req_off = token offsets.
+void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64_t ldq, void* out,
+                         int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
+                         const int32_t* page_table, int max_pages, const void* kpool,
+                         const void* vpool, int n_q, int n_kv, hipStream_t st);
 
 // Attention of each token's queries over its slot's cached keys 0..pos.
 void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* out,
@@ -88,7 +96,8 @@ void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* 
                        const void* vpool, int n_q, int n_kv, int hd, hipStream_t st);
 
 // Prefill pooling: pool_sum[slot] = sum of the request's h rows; pooled[i] =
-// [sum / n ; h[last]] (fp32, plus a bf16 copy when pooled_bf16 != null).
+// [sum / n ; h[last]] (fp32; with pooled_bf16 != null also a bf16 hi/lo
+// split: hi in rows [0, n), lo in rows [n, 2n)).
 void launch_pool_prefill(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_off,
                          const int32_t* req_slot, float* pool_sum, float* pooled,
                          uint16_t* pooled_bf16, hipStream_t st);
@@ -97,7 +106,8 @@ void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32
                       const int32_t* req_start, float* pool_sum, float* pooled,
                       uint16_t* pooled_bf16, hipStream_t st);
 
-// z[i] = w2 . relu(sum_s partial[s][i] + b1) + b2
+// z[i] = w2 . relu(sum_s partial[s][i] + b1) + b2 (bf16 heads also add the
+// lo-split rows partial[s][n + i])
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
                         const void* b1, const void* w2, const void* b2, float* z, hipStream_t st);
 

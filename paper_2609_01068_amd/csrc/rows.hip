@@ -80,11 +80,22 @@ rope_kv_kernel(T* qkv, int64_t ld, const int32_t* tok_slot, const int32_t* tok_p
             store_act<T>(dst + c + half, y2);
         }
     }
+    // value pages are stored transposed, [n_kv][hd][16 tokens], so that a
+    // channel's 16 values of a page are contiguous
     const T* vrow = row + (n_q + n_kv) * hd;
     for (int w = threadIdx.x; w < n_kv * hd; w += 256) {
         const int g = w / hd, c = w % hd;
-        vpool[(((int64_t)page * n_kv + g) * 16 + off) * hd + c] = vrow[w];
+        vpool[(((int64_t)page * n_kv + g) * hd + c) * 16 + off] = vrow[w];
     }
+}
+
+// The head's MFMA GEMM reads bf16: an fp32 value v is passed as two rows,
+// hi = bf16(v) in row i and lo = bf16(v - hi) in row n + i (n = requests),
+// whose products the head sums, so the head input keeps ~16 mantissa bits.
+__device__ __forceinline__ void split_bf16(float v, uint16_t* hi_row, int64_t lo_offset) {
+    const bf16_t hi = f32_to_bf16(v);
+    hi_row[0] = hi;
+    hi_row[lo_offset] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
 // grid (n_req, ceil(d / 256)): each thread sums one column of a request in
@@ -104,8 +115,8 @@ pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
     pooled[(int64_t)i * 2 * d + c] = mean;
     pooled[(int64_t)i * 2 * d + d + c] = last;
     if (pooled_bf16) {
-        pooled_bf16[(int64_t)i * 2 * d + c] = f32_to_bf16(mean);
-        pooled_bf16[(int64_t)i * 2 * d + d + c] = f32_to_bf16(last);
+        split_bf16(mean, pooled_bf16 + (int64_t)i * 2 * d + c, (int64_t)gridDim.x * 2 * d);
+        split_bf16(last, pooled_bf16 + (int64_t)i * 2 * d + d + c, (int64_t)gridDim.x * 2 * d);
     }
 }
 
@@ -123,21 +134,24 @@ pool_step_kernel(int d, const float* h, int64_t ldh, const int32_t* req_slot,
     pooled[(int64_t)i * 2 * d + c] = mean;
     pooled[(int64_t)i * 2 * d + d + c] = x;
     if (pooled_bf16) {
-        pooled_bf16[(int64_t)i * 2 * d + c] = f32_to_bf16(mean);
-        pooled_bf16[(int64_t)i * 2 * d + d + c] = f32_to_bf16(x);
+        split_bf16(mean, pooled_bf16 + (int64_t)i * 2 * d + c, (int64_t)gridDim.x * 2 * d);
+        split_bf16(x, pooled_bf16 + (int64_t)i * 2 * d + d + c, (int64_t)gridDim.x * 2 * d);
     }
 }
 
 template <typename TW>
 __global__ void __launch_bounds__(256)
-head_finish_kernel(int h1, int splits, int n_req, const float* partial, const TW* b1,
+head_finish_kernel(int h1, int splits, int n_req, int rows, const float* partial, const TW* b1,
                    const TW* w2, const TW* b2, float* z) {
     __shared__ float red[4];
     const int i = blockIdx.x;
     float acc = 0.f;
     for (int j = threadIdx.x; j < h1; j += 256) {
         float v = load_act<TW>(b1 + j);
-        for (int s = 0; s < splits; ++s) v += partial[((int64_t)s * n_req + i) * h1 + j];
+        for (int s = 0; s < splits; ++s) {
+            v += partial[((int64_t)s * rows + i) * h1 + j];
+            if (rows > n_req) v += partial[((int64_t)s * rows + n_req + i) * h1 + j];
+        }
         acc = fmaf(fmaxf(v, 0.f), load_act<TW>(w2 + j), acc);
     }
     acc = block_sum<256>(acc, red);
@@ -220,11 +234,11 @@ void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* p
     if (n_req <= 0) return;
     if (w_fmt == FMT_F32)
         hipLaunchKernelGGL((head_finish_kernel<float>), dim3(n_req), dim3(256), 0, st, h1, splits,
-                           n_req, partial, static_cast<const float*>(b1),
+                           n_req, n_req, partial, static_cast<const float*>(b1),
                            static_cast<const float*>(w2), static_cast<const float*>(b2), z);
     else
         hipLaunchKernelGGL((head_finish_kernel<bf16_t>), dim3(n_req), dim3(256), 0, st, h1, splits,
-                           n_req, partial, static_cast<const bf16_t*>(b1),
+                           n_req, 2 * n_req, partial, static_cast<const bf16_t*>(b1),
                            static_cast<const bf16_t*>(w2), static_cast<const bf16_t*>(b2), z);
 }
 

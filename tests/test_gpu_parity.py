@@ -115,14 +115,14 @@ def test_bf16_reduced_shape_ragged_tiles_and_steps():
 
 
 def test_e4m3_reduced_shape_gqa8_and_steps():
-    say("case: e4m3 weights d=512 8q/1kv hd128 F1024, lens [5,64,257,16], 2 steps")
-    case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=8, n_kv=1), n_req=4)
+    say("case: e4m3 weights d=512 16q/2kv hd128 F1024, lens [5,64,257,16], 2 steps")
+    case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=16, n_kv=2), n_req=4)
     _run_prefill_case(case, keep=True, steps=2)
 
 
 def test_bf16_head_dim_64_shape():
-    say("case: bf16 d=256 4q/2kv hd64 F512, lens [3,40,90]")
-    case = make_case(1, lens=[3, 40, 90], shape=reduced_shape(d=256, n_q=4, n_kv=2, hd=64,
+    say("case: bf16 d=256 4q/4kv hd64 F512, lens [3,40,90]")
+    case = make_case(1, lens=[3, 40, 90], shape=reduced_shape(d=256, n_q=4, n_kv=4, hd=64,
                                                              ffn=512, head_hidden=256), n_req=3)
     _run_prefill_case(case, keep=True, steps=1)
 
