@@ -2,13 +2,14 @@
 //
 // bf16 / e4m3-weight path: 256x256x64 workgroup tiles, 4 waves (2 x 2), each
 // wave owning a 128x128 sub-tile built from v_mfma_f32_32x32x16_bf16 (its 256
-// accumulators fit the accumulation registers at one wave per SIMD).  Tiles
-// are staged through LDS, double buffered with a register prefetch of the
-// next K slice, so each iteration needs a single barrier.  LDS rows are 64
-// bf16 (128 B) with 16-byte chunks XOR-swizzled by (row / 2) % 8, which makes
-// the 16-lane phases of ds_read_b128 fragment loads conflict free.  e4m3
-// weights are widened to bf16 (exact) on their way into LDS and the per-row
-// scale is applied in the epilogue.
+// accumulators fit the accumulation registers at one wave per SIMD).  K
+// slices move global -> LDS by DMA (global_load_lds_dwordx4), so no registers
+// stage them; two LDS stages let the copy of slice k+1 run under the MFMAs of
+// slice k, with one wait + barrier per slice.  16-byte LDS chunks are
+// XOR-swizzled per row (the swizzle is applied to the DMA source addresses,
+// since each lane's LDS slot is fixed), making fragment reads conflict free.
+// e4m3 weights stay as codes in LDS, are widened to bf16 (exact) when a
+// fragment is read, and the per-row scale is applied in the epilogue.
 //
 // fp32 path (tiny shape): a plain LDS-tiled VALU kernel with full bounds
 // handling; it exists for the fp32 configuration, not for speed.
@@ -55,16 +56,43 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int mt, int nt, int& tm
     tn = in / gsize;
 }
 
+// LDS DMA: each lane of the wave copies 16 bytes from its own global address
+// to lds_base + 16 * lane (global_load_lds_dwordx4).
+__device__ __forceinline__ void dma16(const void* g, char* lds_base) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// 16 OCP e4m3 codes -> two groups of 8 bf16 (exact).
+__device__ __forceinline__ void e4m3x16_to_bf16(uint4 c, bf16x8& lo, bf16x8& hi) {
+    uint32_t w[8];
+    e4m3x4_to_bf16x4(c.x, w[0], w[1]);
+    e4m3x4_to_bf16x4(c.y, w[2], w[3]);
+    e4m3x4_to_bf16x4(c.z, w[4], w[5]);
+    e4m3x4_to_bf16x4(c.w, w[6], w[7]);
+    lo = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+    hi = __builtin_bit_cast(bf16x8, make_uint4(w[4], w[5], w[6], w[7]));
+}
+
+// K-slice layout inside one BK = 64 step: MFMA step kk = 2a + t takes, in lane
+// half hf, the 8 k-values 32a + 16hf + 8t + (0..7).  A and B use the same
+// assignment, so every product pairs equal k.
+//
+// LDS per stage: A [256 rows][8 chunks of 16 B] (chunk c of row r at
+// c ^ ((r / 2) % 8)), then B the same for bf16, or [256 rows][4 chunks of 16
+// e4m3 codes] (chunk c of row r at c ^ ((r / 4) % 4)) for e4m3.  Both make
+// the 16-lane phases of ds_read_b128 conflict free.
 template <int EPI, bool E4M3, typename OutT>
 __global__ void __launch_bounds__(256)
 gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split) {
-    constexpr int BM = 256, BN = 256, NT = 256;
+    constexpr int BM = 256, BN = 256, NT = 256, NW = NT / 64;
     constexpr int WN = 2;
     constexpr int TM = 128, TN = 128, FM = TM / 32, FN = TN / 32;
-    constexpr int RPP = NT / 8;             // tile rows covered per load pass
-    constexpr int CA = BM / RPP;            // 16-byte A chunks per thread
-    constexpr int CB = BN / RPP;
-    __shared__ uint4 lds[2][(BM + BN) * (BK / 8)];
+    constexpr int A_BYTES = BM * BK * 2;
+    constexpr int B_BYTES = E4M3 ? BN * BK : BN * BK * 2;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
 
     const int mt = (M + BM - 1) / BM, nt = N / BN;
     int tm, tn;
@@ -76,62 +104,51 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
-    const int chunk = tid & 7, r0 = tid >> 3;
 
-    // A: thread rows r0 + RPP * i, clamped to the last valid row
-    const bf16_t* a_base = static_cast<const bf16_t*>(A.p[0]) + (int64_t)min(m0 + r0, M - 1) * A.ld + chunk * 8;
-    const int a_room = M - 1 - (m0 + r0);   // rows available below r0 (may be < 0 on the last tile)
+    // ---- DMA source addresses.  Wave w fills A rows [64w, 64w + 64) with 8
+    // copies of 8 rows each; lane -> (row 8j + lane / 8, slot lane % 8).
+    constexpr int AROWS = BM / NW;                 // 64
     const int64_t seg1 = (const bf16_t*)A.p[1] - (const bf16_t*)A.p[0];
     const int64_t seg2 = (const bf16_t*)A.p[2] - (const bf16_t*)A.p[0];
-    // B: thread rows r0 + RPP * i.  Rows of one 256-row tile stay in one block
-    // (block ends are multiples of 256); in paired mode consecutive 32-row
-    // passes alternate gate/up, so chunk i reads bsrc[i & 1] + (i >> 1) * bstep.
-    const char* bsrc[2];
-    int64_t bstep;
-    {
-        const int esz = E4M3 ? 1 : 2;
-        int s, r;
-        b_row(B, n0 + r0, s, r);
-        bsrc[0] = static_cast<const char*>(B.p[s]) + ((int64_t)r * B.ld + chunk * 8) * esz;
-        if (B.paired) {
-            int s1, r1;
-            b_row(B, n0 + r0 + RPP, s1, r1);
-            bsrc[1] = static_cast<const char*>(B.p[s1]) + ((int64_t)r1 * B.ld + chunk * 8) * esz;
-            bstep = (int64_t)RPP * B.ld * esz;
+    const bf16_t* a_row[AROWS / 8];
+#pragma unroll
+    for (int j = 0; j < AROWS / 8; ++j) {
+        const int row = wave * AROWS + j * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        a_row[j] = static_cast<const bf16_t*>(A.p[0]) + (int64_t)min(m0 + row, M - 1) * A.ld + c * 8;
+    }
+    // B: bf16 like A; e4m3 rows are 64 bytes, one copy covers 16 rows.
+    constexpr int BCOPIES = E4M3 ? (BN / NW) / 16 : (BN / NW) / 8;
+    const char* b_row_p[BCOPIES];
+#pragma unroll
+    for (int j = 0; j < BCOPIES; ++j) {
+        int row, off;
+        if (E4M3) {
+            row = wave * (BN / NW) + j * 16 + (lane >> 2);
+            off = ((lane & 3) ^ ((row >> 2) & 3)) * 16;
         } else {
-            bsrc[1] = bsrc[0] + (int64_t)RPP * B.ld * esz;
-            bstep = (int64_t)2 * RPP * B.ld * esz;
+            row = wave * (BN / NW) + j * 8 + (lane >> 3);
+            off = ((lane & 7) ^ ((row >> 1) & 7)) * 16;
         }
+        int s, r;
+        b_row(B, n0 + row, s, r);
+        b_row_p[j] = static_cast<const char*>(B.p[s]) + (int64_t)r * B.ld * (E4M3 ? 1 : 2) + off;
     }
 
-    uint4 ra[CA], rb[CB];
-    auto gload = [&](int k0) {
+    auto issue = [&](int k0, int stage) {
+        char* base = lds + stage * STAGE;
         const int s = k0 / A.kseg;
         const int64_t aoff = (s == 0 ? 0 : (s == 1 ? seg1 : seg2)) + (k0 - s * A.kseg);
 #pragma unroll
-        for (int i = 0; i < CA; ++i) {
-            const int dr = max(0, min(RPP * i, a_room));
-            ra[i] = *reinterpret_cast<const uint4*>(a_base + aoff + (int64_t)dr * A.ld);
+        for (int j = 0; j < AROWS / 8; ++j)
+            dma16(a_row[j] + aoff, base + (wave * AROWS + j * 8) * 128);
+#pragma unroll
+        for (int j = 0; j < BCOPIES; ++j) {
+            if (E4M3)
+                dma16(b_row_p[j] + k0, base + A_BYTES + (wave * (BN / NW) + j * 16) * 64);
+            else
+                dma16(b_row_p[j] + (int64_t)k0 * 2, base + A_BYTES + (wave * (BN / NW) + j * 8) * 128);
         }
-#pragma unroll
-        for (int i = 0; i < CB; ++i) {
-            const char* src = bsrc[i & 1] + (i >> 1) * bstep;
-            if (E4M3) {
-                uint2 c8 = *reinterpret_cast<const uint2*>(src + k0);
-                uint32_t x0, x1, x2, x3;
-                e4m3x4_to_bf16x4(c8.x, x0, x1);
-                e4m3x4_to_bf16x4(c8.y, x2, x3);
-                rb[i] = make_uint4(x0, x1, x2, x3);
-            } else {
-                rb[i] = *reinterpret_cast<const uint4*>(src + (int64_t)k0 * 2);
-            }
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < CA; ++i) lds[buf][swz(r0 + RPP * i, chunk)] = ra[i];
-#pragma unroll
-        for (int i = 0; i < CB; ++i) lds[buf][BM * 8 + swz(r0 + RPP * i, chunk)] = rb[i];
     };
 
     f32x16 acc[FM][FN];
@@ -142,38 +159,57 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    if (nk > 0) {
-        gload(kb);
-        lstore(0);
-    }
-    __syncthreads();
     const int half = lane >> 5, l32 = lane & 31;
+    // fragment loaders for MFMA step kk of the stage at `base`
+    auto load_a = [&](const char* base, int kk, bf16x8* af) {
+        const int c = 4 * (kk >> 1) + 2 * half + (kk & 1);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int row = wm * TM + i * 32 + l32;
+            af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + row * 128 + ((c ^ ((row >> 1) & 7)) << 4)));
+        }
+    };
+    auto load_b = [&](const char* base, int kk, bf16x8* bfr) {
+        const char* bb = base + A_BYTES;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int row = wn * TN + j * 32 + l32;
+            if (E4M3) {
+                const int c = 2 * (kk >> 1) + half;
+                const uint4 codes = *reinterpret_cast<const uint4*>(bb + row * 64 + ((c ^ ((row >> 2) & 3)) << 4));
+                bf16x8 lo, hi;
+                e4m3x16_to_bf16(codes, lo, hi);
+                bfr[j] = (kk & 1) ? hi : lo;
+            } else {
+                const int c = 4 * (kk >> 1) + 2 * half + (kk & 1);
+                bfr[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(bb + row * 128 + ((c ^ ((row >> 1) & 7)) << 4)));
+            }
+        }
+    };
+
+    if (nk > 0) issue(kb, 0);
+    wait_dma();
+    __syncthreads();
     for (int it = 0; it < nk; ++it) {
-        const int buf = it & 1;
-        if (it + 1 < nk) gload(kb + (it + 1) * BK);
+        const int stage = it & 1;
+        if (it + 1 < nk) issue(kb + (it + 1) * BK, stage ^ 1);
+        const char* base = lds + stage * STAGE;
+        bf16x8 af[2][FM], bfr[2][FN];
+        load_a(base, 0, af[0]);
+        load_b(base, 0, bfr[0]);
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
-            const int c = kk * 2 + half;
-            bf16x8 af[FM], bfr[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                int row = wm * TM + i * 32 + l32;
-                uint4 v = lds[buf][swz(row, c)];
-                af[i] = __builtin_bit_cast(bf16x8, v);
-            }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                int row = wn * TN + j * 32 + l32;
-                uint4 v = lds[buf][BM * 8 + swz(row, c)];
-                bfr[j] = __builtin_bit_cast(bf16x8, v);
+            if (kk + 1 < BK / 16) {
+                load_a(base, kk + 1, af[(kk + 1) & 1]);
+                load_b(base, kk + 1, bfr[(kk + 1) & 1]);
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk & 1][i], bfr[kk & 1][j], acc[i][j], 0, 0, 0);
         }
-        if (it + 1 < nk) lstore(buf ^ 1);
+        wait_dma();
         __syncthreads();
     }
 
