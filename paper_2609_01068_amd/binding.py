@@ -11,7 +11,8 @@ import os
 from typing import Optional
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "liboutlets.so")
+# OUTLETS_LIB may name another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("OUTLETS_LIB") or os.path.join(PKG, "liboutlets.so")
 
 OUTLETS_OK = 0
 OUTLETS_ERR_INVALID_ARG = -1

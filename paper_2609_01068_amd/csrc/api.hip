@@ -80,6 +80,9 @@ struct outlets_ctx {
     int64_t meta_cap = 0;        // int32 entries
     int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
     int32_t n_work = 0;
+    int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
+    int32_t n_tiles = 0;
+    float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
 
     int32_t* h_stage[2] = {nullptr, nullptr};
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -320,7 +323,8 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
     uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
     { KTimer t(c, OUTLETS_K_POOL, st);
       if (prefill)
-          launch_pool_prefill(n, d, c->r_h, d, req_off, req_slot, c->pool_sum, c->pooled, pb, st);
+          launch_pool_prefill(n, c->n_tiles, d, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
+                              c->pool_part, c->pool_sum, c->pooled, pb, st);
       else
           launch_pool_step(n, d, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
@@ -340,9 +344,10 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
 // Stage req_off | req_slot | req_start | updates into pinned memory and copy to the device.
 int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const int32_t* slots,
                 const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
-                const std::vector<int32_t>& work, hipStream_t st) {
+                const std::vector<int32_t>& work, const std::vector<int32_t>& cu_tiles,
+                hipStream_t st) {
     const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size()) +
-                          static_cast<int64_t>(work.size());
+                          static_cast<int64_t>(work.size()) + static_cast<int64_t>(cu_tiles.size());
     if (count > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
@@ -354,6 +359,9 @@ int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const in
     c->work_off = 3 * n + 1 + static_cast<int64_t>(updates.size());
     c->n_work = static_cast<int32_t>(work.size() / 2);
     if (!work.empty()) std::memcpy(h + c->work_off, work.data(), sizeof(int32_t) * work.size());
+    c->tiles_off = c->work_off + static_cast<int64_t>(work.size());
+    c->n_tiles = cu_tiles.empty() ? 0 : cu_tiles.back();
+    if (!cu_tiles.empty()) std::memcpy(h + c->tiles_off, cu_tiles.data(), sizeof(int32_t) * cu_tiles.size());
     HIP_TRY(hipMemcpyAsync(c->d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
@@ -479,7 +487,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->last_idx, sizeof(int32_t) * Bm);
-    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * (Tm / 32 + Bm);
+    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * (Tm / 32 + Bm) + (Bm + 1);
+    ALLOC(c->pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
@@ -550,7 +559,9 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     std::vector<int32_t> work;
     if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim))
         work = attention_work(n_req, lens);
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, work, st);
+    std::vector<int32_t> cu_tiles(n_req + 1, 0);
+    for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, work, cu_tiles, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, z_out,
                        hdraft_out, st);
@@ -587,7 +598,7 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     std::vector<int32_t> off(n_req + 1), start(n_req);
     for (int i = 0; i <= n_req; ++i) off[i] = i;
     for (int i = 0; i < n_req; ++i) start[i] = ctx->pager->seq_len(slots[i]) - 1;
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, std::vector<int32_t>(), st);
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, std::vector<int32_t>(), std::vector<int32_t>(), st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, z_out, hdraft_out, st);
     if (rc) return rc;   // device work may be partly queued; the slot lengths advanced

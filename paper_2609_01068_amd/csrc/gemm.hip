@@ -1,8 +1,9 @@
 // Dense contractions of the draft layer and the length head on gfx950.
 //
-// bf16 / e4m3-weight path: 256x256x64 workgroup tiles, 4 waves (2 x 2), each
-// wave owning a 128x128 sub-tile built from v_mfma_f32_32x32x16_bf16 (its 256
-// accumulators fit the accumulation registers at one wave per SIMD).  K
+// bf16 / e4m3-weight path: 256x256x64 workgroup tiles, 8 waves (2 x 4), each
+// wave owning a 128x64 sub-tile built from v_mfma_f32_32x32x16_bf16; two waves
+// per SIMD let one issue MFMAs while the other waits on LDS (measured faster
+// than 4 waves of 128x128 at one wave per SIMD).  K
 // slices move global -> LDS by DMA (global_load_lds_dwordx4), so no registers
 // stage them; two LDS stages let the copy of slice k+1 run under the MFMAs of
 // slice k, with one wait + barrier per slice.  16-byte LDS chunks are
@@ -83,12 +84,16 @@ __device__ __forceinline__ void e4m3x16_to_bf16(uint4 c, bf16x8& lo, bf16x8& hi)
 // c ^ ((r / 2) % 8)), then B the same for bf16, or [256 rows][4 chunks of 16
 // e4m3 codes] (chunk c of row r at c ^ ((r / 4) % 4)) for e4m3.  Both make
 // the 16-lane phases of ds_read_b128 conflict free.
-template <int EPI, bool E4M3, typename OutT>
-__global__ void __launch_bounds__(256)
+#ifndef OUTLETS_GEMM_WM
+#define OUTLETS_GEMM_WM 2
+#define OUTLETS_GEMM_WN 4
+#endif
+
+template <int EPI, bool E4M3, typename OutT, int WM, int WN>
+__global__ void __launch_bounds__(WM * WN * 64)
 gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split) {
-    constexpr int BM = 256, BN = 256, NT = 256, NW = NT / 64;
-    constexpr int WN = 2;
-    constexpr int TM = 128, TN = 128, FM = TM / 32, FN = TN / 32;
+    constexpr int BM = 256, BN = 256, NW = WM * WN;
+    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
     constexpr int A_BYTES = BM * BK * 2;
     constexpr int B_BYTES = E4M3 ? BN * BK : BN * BK * 2;
     constexpr int STAGE = A_BYTES + B_BYTES;
@@ -254,6 +259,9 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
                     }
                 }
             }
+            // keep the compiler from hoisting the next fragment's loads and
+            // conversions over this one (it would run out of registers)
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 }
@@ -340,7 +348,8 @@ void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& 
     const int mt = (M + 255) / 256, nt = N / 256;
     const int kps = ((K / BK + splits - 1) / splits) * BK;
     dim3 grid(mt * nt, splits);
-    hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, bf16_t>), grid, dim3(256), 0, st, M, N, K,
+    hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, bf16_t, OUTLETS_GEMM_WM, OUTLETS_GEMM_WN>), grid,
+                       dim3(OUTLETS_GEMM_WM * OUTLETS_GEMM_WN * 64), 0, st, M, N, K,
                        a, b, c, kps);
 }
 

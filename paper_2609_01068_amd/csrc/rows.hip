@@ -98,17 +98,39 @@ __device__ __forceinline__ void split_bf16(float v, uint16_t* hi_row, int64_t lo
     hi_row[lo_offset] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
-// grid (n_req, ceil(d / 256)): each thread sums one column of a request in
-// row order (deterministic, independent of the batch).
+// Prefill pooling in two deterministic stages.  Stage 1, grid (tiles,
+// ceil(d / 256)): tile t (request r's rows [32 k, 32 k + 32), t = cu_tiles[r]
+// + k) sums its rows in order.  Stage 2, grid (n_req, ceil(d / 256)): each
+// request sums its tiles in order.  Tiles are relative to the request start,
+// so the result does not depend on the rest of the batch.
+__global__ void __launch_bounds__(256)
+pool_tiles_kernel(int d, int n_req, const float* h, int64_t ldh, const int32_t* req_off,
+                  const int32_t* cu_tiles, float* part) {
+    const int t = blockIdx.x;
+    const int c = blockIdx.y * 256 + threadIdx.x;
+    if (c >= d) return;
+    int lo = 0, hi = n_req - 1;        // request r with cu_tiles[r] <= t < cu_tiles[r + 1]
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (cu_tiles[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const int b = req_off[lo] + (t - cu_tiles[lo]) * 32;
+    const int e = min(b + 32, req_off[lo + 1]);
+    float s = 0.f;
+    for (int r = b; r < e; ++r) s += h[(int64_t)r * ldh + c];
+    part[(int64_t)t * d + c] = s;
+}
+
 __global__ void __launch_bounds__(256)
 pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
-                    const int32_t* req_slot, float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
+                    const int32_t* req_slot, const int32_t* cu_tiles, const float* part,
+                    float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
     const int i = blockIdx.x;
     const int c = blockIdx.y * 256 + threadIdx.x;
     if (c >= d) return;
     const int b = req_off[i], e = req_off[i + 1];
     float s = 0.f;
-    for (int r = b; r < e; ++r) s += h[(int64_t)r * ldh + c];
+    for (int t = cu_tiles[i]; t < cu_tiles[i + 1]; ++t) s += part[(int64_t)t * d + c];
     pool_sum[(int64_t)req_slot[i] * d + c] = s;
     const float mean = s / static_cast<float>(e - b);
     const float last = h[(int64_t)(e - 1) * ldh + c];
@@ -213,12 +235,15 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
                            n_q, n_kv, hd);
 }
 
-void launch_pool_prefill(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_off,
-                         const int32_t* req_slot, float* pool_sum, float* pooled,
-                         uint16_t* pooled_bf16, hipStream_t st) {
+void launch_pool_prefill(int n_req, int n_tiles, int d, const float* h, int64_t ldh,
+                         const int32_t* req_off, const int32_t* req_slot, const int32_t* cu_tiles,
+                         float* part, float* pool_sum, float* pooled, uint16_t* pooled_bf16,
+                         hipStream_t st) {
     if (n_req <= 0) return;
+    hipLaunchKernelGGL(pool_tiles_kernel, dim3(n_tiles, (d + 255) / 256), dim3(256), 0, st, d, n_req,
+                       h, ldh, req_off, cu_tiles, part);
     hipLaunchKernelGGL(pool_prefill_kernel, dim3(n_req, (d + 255) / 256), dim3(256), 0, st, d, h,
-                       ldh, req_off, req_slot, pool_sum, pooled, pooled_bf16);
+                       ldh, req_off, req_slot, cu_tiles, part, pool_sum, pooled, pooled_bf16);
 }
 
 void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_slot,
