@@ -44,6 +44,25 @@ def gemm_flops(shape, T: int):
     }
 
 
+def recorded_traffic():
+    """HBM bytes per launch of the prefill gate/up GEMM from the committed
+    rocprofv3 counter summary, or None when the GEMM source has changed since
+    the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "gate_up_gemm_8b_prefill_b32.md")
+    src = os.path.join(ROOT, "paper_2609_01068_amd", "csrc", "gemm.hip")
+    try:
+        text = open(path).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    vals = dict(re.findall(r"^(traffic_bytes_per_launch|gemm_source_sha256_16): (\S+)$", text, re.M))
+    if vals.get("gemm_source_sha256_16") != sha or "traffic_bytes_per_launch" not in vals:
+        return None
+    return float(vals["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl, W, lens, budget_s: float = 12.0):
     """The fp64 oracle on a bounded sample of the same batch: requests in
     batch order, static prediction + one step each, until ``budget_s`` of
@@ -93,6 +112,9 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (3 times); used to scale "
+                         "rocprof's FETCH_SIZE / WRITE_SIZE counters to bytes")
     a = ap.parse_args(argv)
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the path shards over "
@@ -101,6 +123,16 @@ def main(argv=None):
 
     import numpy as np
     import torch
+
+    if a.copy_probe:
+        n = 1 << 30
+        x = torch.ones(n, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_per_launch": n, "launches": 3}))
+        return 0
 
     from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
     from synth import make_lengths, make_prompt_states, make_step_states, make_weights, workload
@@ -182,7 +214,7 @@ def main(argv=None):
         "draft_tokens_per_s": tok_s,
         "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(),
                      "flops_per_launch": flops[dom], "avg_ms": dom_ms},
         "kernels_prefill": kernels,
         "kernels_step": step_kernels,
