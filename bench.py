@@ -104,6 +104,149 @@ def cpu_baseline(wl, W, lens, budget_s: float = 12.0):
     }
 
 
+def _emit(out):
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def bench_decode(a):
+    """Dynamic re-prediction at scale: 512 in-flight requests whose paged draft
+    KV caches hold U[256, 8192] prompt tokens (filled by untimed prefill calls),
+    then `steps` decode steps of one new token per request."""
+    import numpy as np
+    import torch
+    from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
+    from synth import device_states, make_lengths, make_weights, workload
+
+    wl = workload(3)
+    steps = a.steps
+    print(f"[bench] generating {wl.name} weights", file=sys.stderr, flush=True)
+    W = make_weights(wl, a.seed)
+    lens = make_lengths(wl, a.seed)
+    B = len(lens)
+    max_seq = int(lens.max()) + steps + a.warmup + 16
+    pages = int(sum((int(n) + steps + a.warmup + 15) // 16 for n in lens)) + B
+    chunk = 48
+    max_chunk_tokens = max(int(lens[i:i + chunk].sum()) for i in range(0, B, chunk))
+    pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B, max_seq_len=max_seq,
+                            num_pages=pages, max_batch_tokens=max_chunk_tokens, max_batch_requests=B)
+    print(f"[bench] filling {B} KV caches ({int(lens.sum())} tokens) with prefill calls", file=sys.stderr, flush=True)
+    for i in range(0, B, chunk):
+        idx = list(range(i, min(B, i + chunk)))
+        H = device_states(wl, int(lens[idx].sum()), a.seed, 300, i)
+        pred.prefill(idx, lens[idx], *H)
+        torch.cuda.synchronize()
+        del H
+        print(f"[bench]   prefilled requests {idx[0]}..{idx[-1]}", file=sys.stderr, flush=True)
+    n_in = a.warmup + steps
+    S = [device_states(wl, B, a.seed, 400, t) for t in range(n_in)]
+    slots = list(range(B))
+    z = torch.empty(B, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for t in range(a.warmup):
+        pred.step(slots, *S[t], z_out=z, stream=stream)
+    torch.cuda.synchronize()
+    cached0 = int(lens.sum()) + B * a.warmup
+    pred.profile(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for t in range(a.warmup, n_in):
+        pred.step(slots, *S[t], z_out=z, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    prof = pred.profile_read("step")
+    pred.profile(False)
+    ms_per_step = max(gpu_ms, wall * 1e3) / steps
+    # keys read per step: every cached token of every request plus the new one
+    keys = sum(cached0 + B * (t + 1) for t in range(steps)) / steps
+    kv_bytes = keys * wl.shape.n_kv * wl.shape.head_dim * 2 * 2
+    attn_ms = prof["ATTN"][0] / max(1, prof["ATTN"][1])
+    achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": B / (ms_per_step / 1e3), "unit": "draft tokens/s (request-steps/s)",
+        "n_gpus": 1, "steps": steps, "warmup": a.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded on device; U[256,8192] cached prompt tokens; fresh N(0,1) x (1,4,16) states per step)",
+        "config": {"workload": "8B-shaped bf16 draft layer + length head, dynamic re-prediction: 512 in-flight "
+                               "requests with paged draft KV caches of U[256, 8192] tokens (page 16), one new "
+                               "token per request per step", "requests": B, "cached_tokens_at_start": cached0},
+        "roofline": {"kernel": "decode attention over the paged KV cache", "bound": "hbm",
+                     "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": None, "bytes_per_launch": kv_bytes, "avg_ms": attn_ms},
+        "kernels_step": {n: {"avg_ms": ms / k, "launches": k} for n, (ms, k) in prof.items() if k},
+    }
+    pred.close()
+    return _emit(out)
+
+
+def bench_prefill(a, cfg_id):
+    """Static prediction of one large batch in a single call (configs 2 and 4)."""
+    import numpy as np
+    import torch
+    from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
+    from synth import device_states, make_lengths, make_weights, workload
+
+    wl = workload(cfg_id)
+    print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
+    W = make_weights(wl, a.seed)
+    lens = make_lengths(wl, a.seed)
+    T, B = int(lens.sum()), len(lens)
+    H = device_states(wl, T, a.seed, 300, 0)
+    pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B,
+                            max_seq_len=int(lens.max()) + 16, num_pages=B * ((int(lens.max()) + 31) // 16),
+                            max_batch_tokens=T, max_batch_requests=B)
+    del W
+    print(f"[bench] {B} requests, {T} tokens; warmup {a.warmup}, timed {a.steps}", file=sys.stderr, flush=True)
+    slots = list(range(B))
+    z = torch.empty(B, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(a.warmup):
+        pred.prefill(slots, lens, *H, z_out=z, stream=stream)
+        pred.release(slots)
+    torch.cuda.synchronize()
+    pred.profile(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(a.steps):
+        pred.prefill(slots, lens, *H, z_out=z, stream=stream)
+        pred.release(slots)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = pred.profile_read("prefill")
+    pred.profile(False)
+    ms_per_step = max(ev0.elapsed_time(ev1), wall * 1e3) / a.steps
+    flops = gemm_flops(wl.shape, T)
+    kernels = {}
+    for name, (ms, n) in prof.items():
+        if n:
+            kernels[name] = {"avg_ms": ms / n, "launches": n}
+            if name in flops:
+                kernels[name]["tflops"] = flops[name] / (ms / n * 1e-3) / 1e12
+    dom = "GATE_UP_GEMM"
+    dom_ms = prof[dom][0] / max(1, prof[dom][1])
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": B / (ms_per_step / 1e3), "unit": "requests/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if wl.weight_fmt == "bf16" else "bf16 (e4m3 weights)",
+        "data": "synthetic (seeded; lognormal prompt lengths; N(0,1) x (1,4,16) target states drawn on device)",
+        "config": {"workload": wl.name, "requests": B, "prompt_tokens": T, "d": wl.shape.d,
+                   "heads": [wl.shape.n_q, wl.shape.n_kv], "ffn": wl.shape.ffn, "weights": wl.weight_fmt},
+        "draft_tokens_per_s": T / (ms_per_step / 1e3),
+        "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
+                     "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None, "avg_ms": dom_ms},
+        "kernels_prefill": kernels,
+    }
+    pred.close()
+    return _emit(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -112,6 +255,12 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--workload", default="prefill-8b",
+                    choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3"],
+                    help="prefill-8b (default): 32-request 8B prefill + one step; decode-8b: 512 "
+                         "in-flight requests with 256..8192 cached tokens, timed decode steps; "
+                         "prefill-8b-large: 256 requests (~466k tokens) in one call; "
+                         "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 times); used to scale "
                          "rocprof's FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -136,6 +285,11 @@ def main(argv=None):
 
     from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
     from synth import make_lengths, make_prompt_states, make_step_states, make_weights, workload
+
+    if a.workload == "decode-8b":
+        return bench_decode(a)
+    if a.workload != "prefill-8b":
+        return bench_prefill(a, {"prefill-8b-large": 2, "prefill-70b-e4m3": 4}[a.workload])
 
     wl = workload(1)
     print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)

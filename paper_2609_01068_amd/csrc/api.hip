@@ -83,6 +83,9 @@ struct outlets_ctx {
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
     int32_t n_tiles = 0;
     float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
+    float* decode_part = nullptr;  // split-KV decode attention partials
+    float* splitk_ws = nullptr;  // fp32 partial sums of small-M split-K GEMMs
+    size_t splitk_bytes = 0;
 
     int32_t* h_stage[2] = {nullptr, nullptr};
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -292,11 +295,11 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
 
     // Eq. 1: f_ctx = W_proj [h_low | h_mid | h_high]
     { KTimer t(c, OUTLETS_K_FUSE_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(c->r_f, d), 1, st); }
+      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
       launch_rmsnorm(af, c->small_fmt, T, d, c->r_f, d, c->w.gamma_attn, eps, c->a_norm, d, nullptr, 0, st); }
     { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, d, g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st); }
+      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, d, g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_ROPE_KV, st);
       launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
                      c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
@@ -306,18 +309,23 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
           launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->qkv, c->qkv_dim, c->attn, c->qdim,
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, st);
+      else if (!prefill && c->n_work > 0)
+          launch_attn_decode(n, c->n_work, c->d_meta + c->work_off, c->d_meta + c->tiles_off, c->qkv,
+                             c->qkv_dim, c->attn, c->qdim, req_slot, req_start, c->page_table,
+                             c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
+                             c->decode_part, st);
       else
           launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
                             c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
                             c->cfg.n_kv_heads, c->cfg.head_dim, st); }
     { KTimer t(c, OUTLETS_K_O_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st); }
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
       launch_rmsnorm(af, c->small_fmt, T, d, c->r_x1, d, c->w.gamma_mlp, eps, c->b_norm, d, nullptr, 0, st); }
     { KTimer t(c, OUTLETS_K_GATE_UP_GEMM, st);
-      gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(c->mlp, c->F), 1, st); }
+      gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(c->mlp, c->F), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_DOWN_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(c->r_x2, d, c->r_x1, d), 1, st); }
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(c->r_x2, d, c->r_x1, d), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
       launch_rmsnorm(af, c->small_fmt, T, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d, st); }
     uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
@@ -487,8 +495,27 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->last_idx, sizeof(int32_t) * Bm);
-    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * (Tm / 32 + Bm) + (Bm + 1);
+    const int64_t max_chunks = Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages());
+    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
+    if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
+        ALLOC(c->decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * (cfg->head_dim + 2));
     ALLOC(c->pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
+    {
+        // split-K scratch: the largest plan over the layer's GEMMs for M up to 1024
+        const int64_t gemm_nk[5][2] = {{c->d, 3 * c->d}, {c->qkv_dim, c->d}, {c->d, c->qdim},
+                                       {(c->w_fmt == FMT_F32 ? 1 : 2) * c->F, c->d}, {c->d, c->F}};
+        const int epis[5] = {EPI_STORE_F32, EPI_STORE_ACT, EPI_RESID_F32, EPI_SWIGLU, EPI_RESID_F32};
+        size_t need = 0;
+        for (int64_t mt = 1; mt <= 4 && (mt - 1) * 256 < Tm; ++mt) {
+            const int64_t m = std::min<int64_t>(mt * 256, Tm);
+            for (int g = 0; g < 5; ++g) {
+                const int sk = gemm_splitk_plan(c->w_fmt, epis[g], (int)m, (int)gemm_nk[g][0], (int)gemm_nk[g][1]);
+                if (sk > 1) need = std::max(need, (size_t)sk * m * gemm_nk[g][0] * sizeof(float));
+            }
+        }
+        c->splitk_bytes = need;
+        if (need) ALLOC(c->splitk_ws, need);
+    }
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
@@ -598,7 +625,19 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     std::vector<int32_t> off(n_req + 1), start(n_req);
     for (int i = 0; i <= n_req; ++i) off[i] = i;
     for (int i = 0; i < n_req; ++i) start[i] = ctx->pager->seq_len(slots[i]) - 1;
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, std::vector<int32_t>(), std::vector<int32_t>(), st);
+    // split-KV decode work items (request, chunk of pages), requests in order
+    std::vector<int32_t> dwork, cu_chunks;
+    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
+        const int chunk = attn_decode_chunk_pages();
+        cu_chunks.assign(n_req + 1, 0);
+        for (int i = 0; i < n_req; ++i) {
+            const int pages = (start[i] + 1 + 15) / 16;
+            const int nch = (pages + chunk - 1) / chunk;
+            cu_chunks[i + 1] = cu_chunks[i] + nch;
+            for (int c = 0; c < nch; ++c) { dwork.push_back(i); dwork.push_back(c); }
+        }
+    }
+    rc = upload_meta(ctx, n_req, off, slots, start, updates, dwork, cu_chunks, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, z_out, hdraft_out, st);
     if (rc) return rc;   // device work may be partly queued; the slot lengths advanced

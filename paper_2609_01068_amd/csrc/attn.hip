@@ -285,6 +285,149 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
     }
 }
 
+// ---------------------------------------------------------------- decode, MFMA
+// One query token per request (a decode step).  Split-KV: one wave per
+// (request, KV head, chunk of kDecodeChunk pages); each wave keeps an online
+// softmax for the G query heads of its KV head and writes (m, l, o) partials,
+// which attn_decode_combine merges in chunk order (deterministic).
+//
+// Per 16-key page: S = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K rows, lane
+// l -> key l % 16; B = Q^T with the G heads in columns 0..G-1 of 16, the rest
+// zero); the 16x16 output gives lane l the scores of head l % 16 for keys
+// 4 (l / 16) + i, which is exactly the B-operand layout of
+// O^T += V^T P^T with v_mfma_f32_16x16x16bf16_1k (A = V^T rows from the
+// transposed value page).  The softmax is lane-local plus two xor-shuffles.
+// The next page's K/V fragments are loaded before the current page is used.
+constexpr int kDecodeChunk = 32;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+template <int G>
+__global__ void __launch_bounds__(64)
+attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_t* req_slot,
+                 const int32_t* req_start, const int32_t* page_table, int max_pages,
+                 const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale, float* part) {
+    constexpr int HD = 128;
+    static_assert(G <= 16, "query heads per KV head");
+    const int wi = blockIdx.x, g = blockIdx.y;
+    const int r = work[2 * wi], c = work[2 * wi + 1];
+    const int slot = req_slot[r];
+    const int nkeys = req_start[r] + 1;            // cached keys plus the new token's
+    const int npages = (nkeys + 15) / 16;
+    const int p0 = c * kDecodeChunk, p1 = min(npages, p0 + kDecodeChunk);
+    const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
+
+    bf16x8 qb[HD / 32];
+    {
+        const bf16_t* qrow = q + (int64_t)r * ldq + (int64_t)(g * G + min(col, G - 1)) * HD + 8 * grp;
+#pragma unroll
+        for (int b = 0; b < HD / 32; ++b) {
+            uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * b);
+            if (col >= G) v = make_uint4(0u, 0u, 0u, 0u);
+            qb[b] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    float m = -INFINITY, l = 0.f;
+    f32x4 o[HD / 16];
+#pragma unroll
+    for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int32_t* prow = page_table + (int64_t)slot * max_pages;
+    uint4 kc[HD / 32], kn[HD / 32];
+    uint2 vc[HD / 16], vn[HD / 16];
+    auto load_page = [&](int pi, uint4* kf, uint2* vf) {
+        const int64_t page = prow[pi];
+        const bf16_t* kb = kpool + (page * n_kv + g) * 16 * HD + col * HD + 8 * grp;
+        const bf16_t* vb = vpool + (page * n_kv + g) * HD * 16 + col * 16 + 4 * grp;
+#pragma unroll
+        for (int b = 0; b < HD / 32; ++b) kf[b] = *reinterpret_cast<const uint4*>(kb + 32 * b);
+#pragma unroll
+        for (int cb = 0; cb < HD / 16; ++cb) vf[cb] = *reinterpret_cast<const uint2*>(vb + 16 * 16 * cb);
+    };
+    if (p0 < p1) load_page(p0, kc, vc);
+    for (int pi = p0; pi < p1; ++pi) {
+        if (pi + 1 < p1) load_page(pi + 1, kn, vn);
+        f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int b = 0; b < HD / 32; ++b)
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kc[b]), qb[b], sc, 0, 0, 0);
+        // lane: head col, keys 4 grp + i of this page
+        const int k0 = pi * 16 + 4 * grp;
+        float v[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[i] = (k0 + i < nkeys) ? sc[i] * qscale : -INFINITY;
+            mx = fmaxf(mx, v[i]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mn = fmaxf(m, mx);                 // finite: key 16 pi < nkeys
+        const float corr = exp2f(m - mn);
+        float ps = 0.f;
+        s16x4 pb;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float pv = exp2f(v[i] - mn);
+            ps += pv;
+            pb[i] = static_cast<short>(f32_to_bf16(pv));
+        }
+        ps += __shfl_xor(ps, 16, 64);
+        ps += __shfl_xor(ps, 32, 64);
+        l = l * corr + ps;
+        m = mn;
+        // value rows of keys past the end may hold stale data: zero them
+        const bool tail = (pi * 16 + 16 > nkeys);
+#pragma unroll
+        for (int cb = 0; cb < HD / 16; ++cb) {
+            uint2 vv = vc[cb];
+            if (tail) {
+                if (k0 + 0 >= nkeys) vv.x &= 0xFFFF0000u;
+                if (k0 + 1 >= nkeys) vv.x &= 0x0000FFFFu;
+                if (k0 + 2 >= nkeys) vv.y &= 0xFFFF0000u;
+                if (k0 + 3 >= nkeys) vv.y &= 0x0000FFFFu;
+            }
+            o[cb] = o[cb] * corr;
+            o[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, vv), pb, o[cb], 0, 0, 0);
+        }
+        if (pi + 1 < p1) {
+#pragma unroll
+            for (int b = 0; b < HD / 32; ++b) kc[b] = kn[b];
+#pragma unroll
+            for (int cb = 0; cb < HD / 16; ++cb) vc[cb] = vn[cb];
+        }
+    }
+    // partial record: [m, l, o[0..HD)] per (work item, KV head, query head)
+    if (col < G) {
+        float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * (HD + 2);
+        if (grp == 0) { rec[0] = m; rec[1] = l; }
+#pragma unroll
+        for (int cb = 0; cb < HD / 16; ++cb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) rec[2 + 16 * cb + 4 * grp + i] = o[cb][i];
+    }
+}
+
+// grid (n_req, n_q), 128 threads: merge the request's chunk partials in order.
+template <int G>
+__global__ void __launch_bounds__(128)
+attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_t* out, int64_t ldo) {
+    constexpr int HD = 128;
+    const int r = blockIdx.x, h = blockIdx.y, ch = threadIdx.x;
+    const int g = h / G, col = h % G;
+    const int c0 = cu_chunks[r], c1 = cu_chunks[r + 1];
+    float M = -INFINITY;
+    for (int c = c0; c < c1; ++c) M = fmaxf(M, part[(((int64_t)c * n_kv + g) * G + col) * (HD + 2)]);
+    float L = 0.f, O = 0.f;
+    for (int c = c0; c < c1; ++c) {
+        const float* rec = part + (((int64_t)c * n_kv + g) * G + col) * (HD + 2);
+        const float f = exp2f(rec[0] - M);
+        L = fmaf(rec[1], f, L);
+        O = fmaf(rec[2 + ch], f, O);
+    }
+    out[(int64_t)r * ldo + (int64_t)h * HD + ch] = f32_to_bf16(O / L);
+}
+
 template <typename T, int HD>
 bool launch_hd(int G, int ntok, const void* q, int64_t ldq, void* out, int64_t ldo,
                const int32_t* tok_slot, const int32_t* tok_pos, const int32_t* page_table,
@@ -338,6 +481,34 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
         OUTLETS_PF_G(8)
     }
 #undef OUTLETS_PF_G
+}
+
+int attn_decode_chunk_pages() { return kDecodeChunk; }
+
+void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
+                        const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
+                        const int32_t* req_start, const int32_t* page_table, int max_pages,
+                        const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
+                        hipStream_t st) {
+    if (n_req <= 0 || n_work <= 0) return;
+    const int G = n_q / n_kv;
+    const float qscale = 1.4426950408889634f / sqrtf(128.0f);
+#define OUTLETS_DEC_G(GG)                                                                          \
+    case GG:                                                                                       \
+        hipLaunchKernelGGL((attn_decode_mfma<GG>), dim3(n_work, n_kv), dim3(64), 0, st,            \
+                           static_cast<const bf16_t*>(q), ldq, work, req_slot, req_start,          \
+                           page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
+                           static_cast<const bf16_t*>(vpool), n_kv, qscale, part);                 \
+        hipLaunchKernelGGL((attn_decode_combine<GG>), dim3(n_req, n_q), dim3(128), 0, st,          \
+                           cu_chunks, part, n_kv, static_cast<bf16_t*>(out), ldo);                 \
+        break;
+    switch (G) {
+        OUTLETS_DEC_G(1)
+        OUTLETS_DEC_G(2)
+        OUTLETS_DEC_G(4)
+        OUTLETS_DEC_G(8)
+    }
+#undef OUTLETS_DEC_G
 }
 
 bool attn_supported(int n_q, int n_kv, int hd) {

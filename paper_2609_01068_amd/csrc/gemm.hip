@@ -14,6 +14,8 @@
 //
 // fp32 path (tiny shape): a plain LDS-tiled VALU kernel with full bounds
 // handling; it exists for the fp32 configuration, not for speed.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "outlets.h"
@@ -353,6 +355,36 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     }
 }
 
+// ---------------------------------------------------------------- split-K reduce
+// part[s][m][n] (fp32, logical columns) summed over s in order, then the
+// epilogue of the unsplit GEMM.  One thread per output element.
+template <int EPI, typename OutT>
+__global__ void __launch_bounds__(256)
+splitk_reduce(int M, int N, int S, const float* part, GemmC C) {
+    const int nout = (EPI == EPI_SWIGLU) ? N / 2 : N;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)M * nout) return;
+    const int m = static_cast<int>(idx / nout), n = static_cast<int>(idx % nout);
+    const int64_t plane = (int64_t)M * N;
+    if (EPI == EPI_SWIGLU) {
+        // output feature n = gate column (n/32)*64 + n%32, up column +32
+        const int ng = (n >> 5) * 64 + (n & 31);
+        float g = 0.f, u = 0.f;
+        for (int sp = 0; sp < S; ++sp) {
+            g += part[sp * plane + (int64_t)m * N + ng];
+            u += part[sp * plane + (int64_t)m * N + ng + 32];
+        }
+        store_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + n, silu_f(g) * u);
+        return;
+    }
+    float v = 0.f;
+    for (int sp = 0; sp < S; ++sp) v += part[sp * plane + (int64_t)m * N + n];
+    if (EPI == EPI_STORE_F32) static_cast<float*>(C.c)[(int64_t)m * C.ldc + n] = v;
+    else if (EPI == EPI_STORE_ACT) store_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + n, v);
+    else if (EPI == EPI_RESID_F32)
+        static_cast<float*>(C.c)[(int64_t)m * C.ldc + n] = C.resid[(int64_t)m * C.ldr + n] + v;
+}
+
 // ---------------------------------------------------------------- fp32 VALU path
 template <int EPI>
 __global__ void __launch_bounds__(256)
@@ -451,6 +483,15 @@ void launch_f32(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC
 
 }  // namespace
 
+int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
+    if (w_fmt == FMT_F32 || epi == EPI_PARTIAL) return 1;
+    const int tiles = ((M + 255) / 256) * (N / 256);
+    if (tiles >= 192) return 1;
+    int s = (384 + tiles - 1) / tiles;
+    s = std::min(s, std::max(1, (K / BK) / 4));   // keep >= 4 K slices per split
+    return std::min(s, 16);
+}
+
 int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
                const GemmB& b, int splits, const char** why) {
     if (M <= 0 || N <= 0 || K <= 0 || splits <= 0) { *why = "gemm: empty shape"; return OUTLETS_ERR_INVALID_ARG; }
@@ -476,7 +517,28 @@ int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA
 }
 
 void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
-                 const GemmB& b, const GemmC& c, int splits, hipStream_t st) {
+                 const GemmB& b, const GemmC& c, int splits, hipStream_t st, float* ws,
+                 size_t ws_bytes) {
+    // Small M: split K over more workgroups into fp32 partials, then reduce in
+    // a fixed order and apply the epilogue (deterministic).
+    const int sk = (splits == 1) ? gemm_splitk_plan(w_fmt, epi, M, N, K) : 1;
+    if (sk > 1 && ws && (size_t)sk * M * N * sizeof(float) <= ws_bytes) {
+        GemmC pc{};
+        pc.c = ws;
+        pc.ldc = N;
+        pc.split_stride = (int64_t)M * N;
+        gemm_launch(act_fmt, w_fmt, EPI_PARTIAL, M, N, K, a, b, pc, sk, st, nullptr, 0);
+        const int nout = (epi == EPI_SWIGLU) ? N / 2 : N;
+        const int64_t total = (int64_t)M * nout;
+        const dim3 grid((unsigned)((total + 255) / 256));
+        switch (epi) {
+            case EPI_STORE_F32: hipLaunchKernelGGL((splitk_reduce<EPI_STORE_F32, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
+            case EPI_STORE_ACT: hipLaunchKernelGGL((splitk_reduce<EPI_STORE_ACT, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
+            case EPI_RESID_F32: hipLaunchKernelGGL((splitk_reduce<EPI_RESID_F32, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
+            case EPI_SWIGLU: hipLaunchKernelGGL((splitk_reduce<EPI_SWIGLU, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
+        }
+        return;
+    }
     if (w_fmt == FMT_F32) {
         switch (epi) {
             case EPI_STORE_F32: case EPI_STORE_ACT: launch_f32<EPI_STORE_F32>(M, N, K, a, b, c, splits, st); break;

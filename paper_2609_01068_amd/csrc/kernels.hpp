@@ -54,8 +54,13 @@ enum Fmt : int { FMT_F32 = 0, FMT_BF16 = 1, FMT_E4M3 = 2 };
 // outputs; w_fmt of B.
 int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
                const GemmB& b, int splits, const char** why);
+// `ws` (fp32 scratch of ws_bytes, may be null) enables the small-M split-K
+// path (gemm_splitk_plan splits > 1): partial sums, then a fixed-order reduce
+// that applies the epilogue.
 void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
-                 const GemmB& b, const GemmC& c, int splits, hipStream_t st);
+                 const GemmB& b, const GemmC& c, int splits, hipStream_t st,
+                 float* ws = nullptr, size_t ws_bytes = 0);
+int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
 
 // ---------------------------------------------------------------- elementwise / rows
 // Per-call token metadata from per-request arrays:
@@ -88,6 +93,17 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
                          int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
                          const int32_t* page_table, int max_pages, const void* kpool,
                          const void* vpool, int n_q, int n_kv, hipStream_t st);
+
+// Decode attention (bf16, hd 128, one query per request, split over chunks of
+// attn_decode_chunk_pages() pages): work[2 i], work[2 i + 1] = (request, chunk);
+// cu_chunks[n_req + 1] = first work item of each request; part = fp32 scratch
+// [n_work, n_kv, G, 130].  Queries are row r of q for request r.
+int attn_decode_chunk_pages();
+void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
+                        const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
+                        const int32_t* req_start, const int32_t* page_table, int max_pages,
+                        const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
+                        hipStream_t st);
 
 // Attention of each token's queries over its slot's cached keys 0..pos.
 void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* out,

@@ -33,7 +33,7 @@ import numpy as np
 __all__ = [
     "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
     "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
-    "make_step_states", "WEIGHT_NAMES", "BIG_LINEARS",
+    "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS",
 ]
 
 # Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
@@ -245,4 +245,21 @@ def make_step_states(wl: Workload, n_req: int, step: int, seed: int = 0,
                         wl.input_scales[depth], wl.act_fmt) for i in idx]
         out.append(np.concatenate(rows, axis=0) if rows else
                    np.zeros((0, d), np.float32 if wl.act_fmt == "f32" else np.uint16))
+    return out
+
+
+def device_states(wl: Workload, rows: int, seed: int, stream: int, index: int, device="cuda"):
+    """Target states drawn directly on the GPU (torch's seeded normal
+    generator), for benchmark workloads too large to draw on the host in
+    reasonable time: three tensors [rows, d] in the workload's activation
+    format, N(0, 1) times the per-depth scales.  The values differ from
+    make_prompt_states' (another generator); parity tests use the host draws."""
+    import torch
+    g = torch.Generator(device=device)
+    out = []
+    for depth in range(3):
+        g.manual_seed(int(np.random.SeedSequence([seed, wl.cfg_id, stream + depth, index]).generate_state(1)[0]))
+        x = torch.randn((rows, wl.shape.d), generator=g, device=device, dtype=torch.float32)
+        x *= wl.input_scales[depth]
+        out.append(x if wl.act_fmt == "f32" else x.to(torch.bfloat16))
     return out

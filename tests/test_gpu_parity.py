@@ -256,3 +256,15 @@ def test_error_paths_leave_state_unchanged():
     z2, _ = pred.prefill([2], [20], *[x[20:40] for x in H])
     assert abs(float(z2[0]) - float(z[1])) <= 1e-5 * max(abs(float(z[1])), 1e-3)
     pred.close()
+
+
+def test_decode_steps_over_long_caches_merge_chunks():
+    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (several 512-key chunks), 3 steps")
+    case = make_case(1, lens=[1100, 600, 40], shape=reduced_shape(), n_req=3)
+    _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
+
+
+def test_decode_steps_8b_shape():
+    say("case: 8B bf16 shape, caches of 600/40 tokens, 2 steps")
+    case = make_case(1, lens=[600, 40], n_req=2)
+    _run_prefill_case(case, keep=False, steps=2, check_intermediates=False)
