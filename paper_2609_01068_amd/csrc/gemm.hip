@@ -26,10 +26,10 @@ namespace {
 
 // Tile shape of the MFMA GEMM (measured choices; override at build time to tune).
 #ifndef OUTLETS_GEMM_WM
-#define OUTLETS_GEMM_WM 2
+#define OUTLETS_GEMM_WM 4
 #endif
 #ifndef OUTLETS_GEMM_WN
-#define OUTLETS_GEMM_WN 4
+#define OUTLETS_GEMM_WN 2
 #endif
 #ifndef OUTLETS_GEMM_BK
 #define OUTLETS_GEMM_BK 64
