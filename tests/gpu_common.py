@@ -103,3 +103,33 @@ def step_inputs(case: Case, step: int, requests=None):
 def reduced_shape(d=512, n_q=8, n_kv=2, hd=128, ffn=1024, head_hidden=256, theta=5e5):
     return DraftShape(d=d, n_q=n_q, n_kv=n_kv, head_dim=hd, ffn=ffn, head_hidden=head_hidden,
                       rope_theta=theta)
+
+
+def mixed_prompt_states(wl, lens, sample, seed=0):
+    """Packed prompt states for a full-size batch: requests in `sample` get the
+    host draws the oracle can reproduce, the others on-device draws (their
+    results are not checked; they load the call at its full size)."""
+    import torch
+    from paper_2609_01068_amd.predictor import to_device
+    from synth import device_states, make_prompt_states
+    parts = [[], [], []]
+    for i, n in enumerate(lens):
+        if i in sample:
+            H = [to_device(x) for x in make_prompt_states(wl, lens, seed, requests=[i])]
+        else:
+            H = device_states(wl, int(n), seed, 300, i)
+        for j in range(3):
+            parts[j].append(H[j])
+    return [torch.cat(p) for p in parts]
+
+
+def mixed_step_states(wl, n_req, step, sample, seed=0):
+    import torch
+    from paper_2609_01068_amd.predictor import to_device
+    from synth import device_states, make_step_states
+    H = device_states(wl, n_req, seed, 400, step)
+    for i in sample:
+        S = make_step_states(wl, n_req, step, seed, requests=[i])
+        for j in range(3):
+            H[j][i:i + 1] = to_device(S[j])
+    return H
