@@ -44,21 +44,21 @@ def gemm_flops(shape, T: int):
     }
 
 
-def recorded_traffic():
-    """HBM bytes per launch of the prefill gate/up GEMM from the committed
-    rocprofv3 counter summary, or None when the GEMM source has changed since
+def recorded_traffic(profile="gate_up_gemm_8b_prefill_b32.md", source="gemm.hip", key="gemm"):
+    """HBM bytes per launch of a dominant kernel from its committed rocprofv3
+    counter summary, or None when the kernel's source file has changed since
     the counters were taken."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "gate_up_gemm_8b_prefill_b32.md")
-    src = os.path.join(ROOT, "paper_2609_01068_amd", "csrc", "gemm.hip")
+    path = os.path.join(ROOT, "profiles", profile)
+    src = os.path.join(ROOT, "paper_2609_01068_amd", "csrc", source)
     try:
         text = open(path).read()
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     except OSError:
         return None
-    vals = dict(re.findall(r"^(traffic_bytes_per_launch|gemm_source_sha256_16): (\S+)$", text, re.M))
-    if vals.get("gemm_source_sha256_16") != sha or "traffic_bytes_per_launch" not in vals:
+    vals = dict(re.findall(r"^(\w+): (\S+)$", text, re.M))
+    if vals.get(f"{key}_source_sha256_16") != sha or "traffic_bytes_per_launch" not in vals:
         return None
     return float(vals["traffic_bytes_per_launch"])
 
@@ -175,7 +175,8 @@ def bench_decode(a):
                                "token per request per step", "requests": B, "cached_tokens_at_start": cached0},
         "roofline": {"kernel": "decode attention over the paged KV cache", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                     "traffic": None, "bytes_per_launch": kv_bytes, "avg_ms": attn_ms},
+                     "traffic": recorded_traffic("decode_attention_8b_b512.md", "attn.hip", "attn"),
+                     "bytes_per_launch": kv_bytes, "avg_ms": attn_ms},
         "kernels_step": {n: {"avg_ms": ms / k, "launches": k} for n, (ms, k) in prof.items() if k},
     }
     pred.close()
