@@ -298,7 +298,13 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
 // O^T += V^T P^T with v_mfma_f32_16x16x16bf16_1k (A = V^T rows from the
 // transposed value page).  The softmax is lane-local plus two xor-shuffles.
 // The next page's K/V fragments are loaded before the current page is used.
-constexpr int kDecodeChunk = 32;
+#ifndef OUTLETS_DECODE_CHUNK
+#define OUTLETS_DECODE_CHUNK 64
+#endif
+#ifndef OUTLETS_DECODE_PPI
+#define OUTLETS_DECODE_PPI 2
+#endif
+constexpr int kDecodeChunk = OUTLETS_DECODE_CHUNK;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -332,11 +338,18 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
 #pragma unroll
     for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // the chunk's page ids, one per lane, fetched up front so the K/V loads of
+    // a page never wait on its page-table entry
     const int32_t* prow = page_table + (int64_t)slot * max_pages;
-    uint4 kc[HD / 32], kn[HD / 32];
-    uint2 vc[HD / 16], vn[HD / 16];
+    static_assert(kDecodeChunk <= 64, "one page id per lane");
+    const int my_page = (p0 + lane < p1) ? prow[p0 + lane] : 0;
+    // PPI pages per iteration: their K/V fragments for the next iteration are
+    // loaded before this iteration's pages are used (2 * PPI pages in flight)
+    constexpr int PPI = OUTLETS_DECODE_PPI;
+    uint4 kc[PPI][HD / 32], kn[PPI][HD / 32];
+    uint2 vc[PPI][HD / 16], vn[PPI][HD / 16];
     auto load_page = [&](int pi, uint4* kf, uint2* vf) {
-        const int64_t page = prow[pi];
+        const int64_t page = __shfl(my_page, min(pi, p1 - 1) - p0, 64);
         const bf16_t* kb = kpool + (page * n_kv + g) * 16 * HD + col * HD + 8 * grp;
         const bf16_t* vb = vpool + (page * n_kv + g) * HD * 16 + col * 16 + 4 * grp;
 #pragma unroll
@@ -344,13 +357,11 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
 #pragma unroll
         for (int cb = 0; cb < HD / 16; ++cb) vf[cb] = *reinterpret_cast<const uint2*>(vb + 16 * 16 * cb);
     };
-    if (p0 < p1) load_page(p0, kc, vc);
-    for (int pi = p0; pi < p1; ++pi) {
-        if (pi + 1 < p1) load_page(pi + 1, kn, vn);
+    auto one_page = [&](int pi, const uint4* kf, const uint2* vf) {
         f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int b = 0; b < HD / 32; ++b)
-            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kc[b]), qb[b], sc, 0, 0, 0);
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[b]), qb[b], sc, 0, 0, 0);
         // lane: head col, keys 4 grp + i of this page
         const int k0 = pi * 16 + 4 * grp;
         float v[4];
@@ -380,7 +391,7 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
         const bool tail = (pi * 16 + 16 > nkeys);
 #pragma unroll
         for (int cb = 0; cb < HD / 16; ++cb) {
-            uint2 vv = vc[cb];
+            uint2 vv = vf[cb];
             if (tail) {
                 if (k0 + 0 >= nkeys) vv.x &= 0xFFFF0000u;
                 if (k0 + 1 >= nkeys) vv.x &= 0x0000FFFFu;
@@ -390,11 +401,25 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
             o[cb] = o[cb] * corr;
             o[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, vv), pb, o[cb], 0, 0, 0);
         }
-        if (pi + 1 < p1) {
+    };
 #pragma unroll
-            for (int b = 0; b < HD / 32; ++b) kc[b] = kn[b];
+    for (int u = 0; u < PPI; ++u) load_page(p0 + u, kc[u], vc[u]);
+    for (int pi = p0; pi < p1; pi += PPI) {
+        if (pi + PPI < p1) {
 #pragma unroll
-            for (int cb = 0; cb < HD / 16; ++cb) vc[cb] = vn[cb];
+            for (int u = 0; u < PPI; ++u) load_page(pi + PPI + u, kn[u], vn[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < PPI; ++u)
+            if (pi + u < p1) one_page(pi + u, kc[u], vc[u]);
+        if (pi + PPI < p1) {
+#pragma unroll
+            for (int u = 0; u < PPI; ++u) {
+#pragma unroll
+                for (int b = 0; b < HD / 32; ++b) kc[u][b] = kn[u][b];
+#pragma unroll
+                for (int cb = 0; cb < HD / 16; ++cb) vc[u][cb] = vn[u][cb];
+            }
         }
     }
     // partial record: [m, l, o[0..HD)] per (work item, KV head, query head)
