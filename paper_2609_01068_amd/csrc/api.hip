@@ -382,14 +382,14 @@ int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const in
     return OUTLETS_OK;
 }
 
-// Prefill attention work items (request, 32-query tile), longest first:
-// a tile's cost is the number of 64-key tiles it visits.
-std::vector<int32_t> attention_work(int n, const int32_t* lens) {
+// Prefill attention work items (request, tile of qt queries), longest
+// first: a tile's cost is the number of 64-key tiles it visits.
+std::vector<int32_t> attention_work(int n, const int32_t* lens, int qt) {
     std::vector<std::pair<int32_t, int32_t>> items;
     for (int i = 0; i < n; ++i)
-        for (int t = 0; t * 32 < lens[i]; ++t) items.emplace_back(i, t);
+        for (int t = 0; t * qt < lens[i]; ++t) items.emplace_back(i, t);
     auto cost = [&](const std::pair<int32_t, int32_t>& it) {
-        return std::min(it.second * 32 + 31, lens[it.first] - 1) / 64;
+        return std::min(it.second * qt + qt - 1, lens[it.first] - 1) / 64;
     };
     std::stable_sort(items.begin(), items.end(),
                      [&](const auto& a, const auto& b) { return cost(a) > cost(b); });
@@ -541,6 +541,10 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     }
     HIP_TRY(hipMemset(c->page_table, 0xFF, sizeof(int32_t) * c->pager->table().size()), "hipMemset");
     HIP_TRY(hipMemset(c->pool_sum, 0, sizeof(float) * cfg->max_slots * c->d), "hipMemset");
+    // attention kernels may read (and give zero weight to) rows of a page no
+    // token has written yet: start from zeros so those rows are finite
+    HIP_TRY(hipMemset(c->kpool, 0, pool_elems * ab), "hipMemset");
+    HIP_TRY(hipMemset(c->vpool, 0, pool_elems * ab), "hipMemset");
     HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
     *out = c.release();
     return OUTLETS_OK;
@@ -585,7 +589,7 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     }
     std::vector<int32_t> work;
     if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim))
-        work = attention_work(n_req, lens);
+        work = attention_work(n_req, lens, attn_prefill_query_tile(ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads));
     std::vector<int32_t> cu_tiles(n_req + 1, 0);
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
     rc = upload_meta(ctx, n_req, off, slots, start, updates, work, cu_tiles, st);

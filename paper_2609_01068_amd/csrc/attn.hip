@@ -22,6 +22,20 @@ namespace outlets {
 
 namespace {
 
+// 16-byte LDS DMA per lane (lane i writes lds_base + 16 i), its wait, and a
+// workgroup barrier without the release fence (the DMA is ordered by the
+// explicit wait; the empty asm statements keep the compiler from moving
+// memory accesses across the barrier).
+__device__ __forceinline__ void dma_16(const void* g, char* lds_base) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void block_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 template <typename T, int HD, int G>
 __global__ void __launch_bounds__(256)
 attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* tok_slot,
@@ -126,10 +140,17 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
 }
 
 // ---------------------------------------------------------------- prefill, MFMA
-// One workgroup per (request, tile of 32 queries, KV head); wave w computes
-// query head g * G + w, so the G heads of a group share each K/V tile staged
-// in LDS.  Keys are visited in tiles of 64 (4 pages), up to the tile's last
-// query position (causal tile skipping).
+// Query blocks per wave: two where the registers allow (G = 2, 4), one where
+// eight waves share a SIMD pair's register file (G = 8) or a lone wave would
+// spill (G = 1).
+constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? 2 : 1; }
+
+// One workgroup per (request, tile of 32 QB queries, KV head); wave w
+// computes query head g * G + w for the tile's QB blocks of 32 queries, so the
+// G heads of a group share each K/V tile and the blocks share every fragment
+// read from LDS.  Keys are visited in tiles of 64 (4 pages) up to the tile's last query
+// position (causal tile skipping); tiles are copied into two LDS stages by
+// DMA while the previous tile is multiplied.
 //
 // Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 // a lane then holds one query (column) and 16 keys per 32x32 block, so the
@@ -151,135 +172,167 @@ __device__ __forceinline__ uint4 zero_tail_bf16x8(uint4 v, int valid) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <int G>
+template <int G, int QB>
 __global__ void __launch_bounds__(G * 64)
 attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
                   const int32_t* req_off, const int32_t* req_slot, const int32_t* page_table,
                   int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale) {
-    constexpr int HD = 128, NT = G * 64, BKV = 64, NS = HD / 16, NB = HD / 32;
-    __shared__ uint4 ks[BKV * 16];   // [key][16 chunks of 8 channels], chunk ^ (key % 16)
-    __shared__ uint4 vs[HD * 8];     // [channel][8 chunks of 8 keys], chunk ^ ((channel / 2) % 8)
+    constexpr int HD = 128, NW = G, BKV = 64, NS = HD / 16, NB = HD / 32, QT = 32 * QB;
+    constexpr int KB = BKV * HD * 2, STAGE = 2 * KB;    // K [64][128] + V^T [128][64], bf16
+    constexpr int KCP = (KB / 1024) / NW;               // DMA copies per wave for K (and for V)
+    __shared__ __attribute__((aligned(16))) char lds[2 * STAGE];
 
     const int r = work[2 * blockIdx.x], qt = work[2 * blockIdx.x + 1];
     const int g = blockIdx.y;
     const int tok0 = req_off[r], n = req_off[r + 1] - tok0, slot = req_slot[r];
-    const int qs = qt * 32;
+    const int qs = qt * QT;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int l32 = lane & 31, hf = lane >> 5;
     const int h = g * G + w;
-    const int tp = min(qs + l32, n - 1);   // this lane's query position (tail lanes repeat the last)
     const int32_t* prow = page_table + (int64_t)slot * max_pages;
+    const int last_page = (n - 1) >> 4;
 
-    bf16x8 qf[NS];
-    {
-        const bf16_t* qrow = qkv + (int64_t)(tok0 + tp) * ldq + h * HD + hf * 8;
+    // queries of this lane: block qb covers positions qs + 32 qb + l32 (tail lanes repeat the last)
+    int tp[QB];
+    bf16x8 qf[QB][NS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        tp[qb] = min(qs + 32 * qb + l32, n - 1);
+        const bf16_t* qrow = qkv + (int64_t)(tok0 + tp[qb]) * ldq + h * HD + hf * 8;
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2)
-            qf[s2] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * s2));
+            qf[qb][s2] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * s2));
     }
-    f32x16 o[NB];
+    f32x16 o[QB][NB];
+    float m[QB], lsum[QB];
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[b][e] = 0.f;
-    float m = -INFINITY, lsum = 0.f;
-    const int maxpos = min(qs + 31, n - 1);
-    const int ntiles = maxpos / BKV + 1;
-    const int arow_key = (l32 & 19) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
-
-    for (int kt = 0; kt < ntiles; ++kt) {
-        const int k0 = kt * BKV;
-        __syncthreads();   // the previous tile's LDS reads are done
-        for (int c = tid; c < BKV * 16; c += NT) {
-            const int key = c >> 4, ch = c & 15, kpos = k0 + key;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (kpos < n) {
-                const int64_t page = prow[kpos >> 4];
-                v = *reinterpret_cast<const uint4*>(kpool + ((page * n_kv + g) * 16 + (kpos & 15)) * HD + ch * 8);
-            }
-            ks[key * 16 + (ch ^ (key & 15))] = v;
-        }
-        for (int c = tid; c < HD * 8; c += NT) {
-            const int ch = c >> 3, vc = c & 7, kp0 = k0 + vc * 8;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (kp0 < n) {
-                const int64_t page = prow[kp0 >> 4];
-                v = *reinterpret_cast<const uint4*>(vpool + ((page * n_kv + g) * HD + ch) * 16 + (kp0 & 15));
-                if (kp0 + 8 > n) v = zero_tail_bf16x8(v, n - kp0);   // keys past the prompt
-            }
-            vs[ch * 8 + (vc ^ ((ch >> 1) & 7))] = v;
-        }
-        __syncthreads();
-
-        f32x16 sacc[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
-            const int key = 32 * kb + arow_key;
-#pragma unroll
-            for (int s2 = 0; s2 < NS; ++s2) {
-                const int ch = 2 * s2 + hf;
-                const bf16x8 a = __builtin_bit_cast(bf16x8, ks[key * 16 + (ch ^ (key & 15))]);
-                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s2], sacc[kb], 0, 0, 0);
-            }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int kpos = k0 + 32 * kb + 16 * (e >> 3) + 8 * hf + (e & 7);
-                const float v = (kpos <= tp) ? sacc[kb][e] * qscale : -INFINITY;
-                sacc[kb][e] = v;
-                mx = fmaxf(mx, v);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mn = fmaxf(m, mx);          // finite: key 0 <= every query position
-        const float corr = exp2f(m - mn);
-        float ps = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float p = exp2f(sacc[kb][e] - mn);
-                sacc[kb][e] = p;
-                ps += p;
-            }
-        ps += __shfl_xor(ps, 32, 64);
-        lsum = lsum * corr + ps;
-        m = mn;
+    for (int qb = 0; qb < QB; ++qb) {
+        m[qb] = -INFINITY;
+        lsum[qb] = 0.f;
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) o[b][e] *= corr;
+            for (int e = 0; e < 16; ++e) o[qb][b][e] = 0.f;
+    }
+    const int maxpos = min(qs + QT - 1, n - 1);
+    const int ntiles = maxpos / BKV + 1;
+    const int arow_key = (l32 & 19) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
+
+    // DMA of one 64-key tile: K rows (key, 16 chunks of 8 channels, chunk c at
+    // c ^ key%16) and V^T rows (channel, 8 chunks of 8 keys, chunk c at
+    // c ^ (channel/2)%8).  The tile's four page ids are uniform (scalar
+    // loads); pages past the prompt's last one repeat it.  Keys past the
+    // prompt are masked out of the scores and their (finite) rows get weight 0.
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    auto issue = [&](int kt, int stage) {
+        char* base = lds + stage * STAGE;
+        int pg[4];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int j = 0; j < 4; ++j) pg[j] = prow[min(4 * kt + j, last_page)];
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                bf16x8 pb;
+        for (int j = 0; j < KCP; ++j) {
+            const int cp = wu * KCP + j;             // 4 keys per copy, all on page cp / 4
+            const int key = cp * 4 + (lane >> 4);
+            const int c = (lane & 15) ^ (key & 15);
+            const bf16_t* src = kpool + ((int64_t)pg[cp >> 2] * n_kv + g) * (16 * HD);
+            dma_16(src + (key & 15) * HD + c * 8, base + cp * 1024);
+        }
 #pragma unroll
-                for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(sacc[kb][8 * u + e]);
-                const int ch = 4 * kb + 2 * u + hf;
+        for (int j = 0; j < KCP; ++j) {
+            const int cp = wu * KCP + j;             // 8 channels per copy
+            const int ch = cp * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ ((ch >> 1) & 7);
+            const int q2 = c >> 1;
+            const int page = q2 == 0 ? pg[0] : q2 == 1 ? pg[1] : q2 == 2 ? pg[2] : pg[3];
+            const bf16_t* src = vpool + ((int64_t)page * n_kv + g) * (HD * 16);
+            dma_16(src + ch * 16 + (c & 1) * 8, base + KB + cp * 1024);
+        }
+    };
+
+    issue(0, 0);
+    for (int kt = 0; kt < ntiles; ++kt) {
+        wait_vm0();
+        block_barrier();      // tile kt is in LDS; every wave is done with tile kt-1
+        issue(min(kt + 1, ntiles - 1), (kt + 1) & 1);
+        const char* ks = lds + (kt & 1) * STAGE;
+        const char* vs = ks + KB;
+        const int k0 = kt * BKV;
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
-                    const int row = 32 * b + l32;
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, vs[row * 8 + (ch ^ ((row >> 1) & 7))]);
-                    o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[b], 0, 0, 0);
+        for (int qb = 0; qb < QB; ++qb) {
+            f32x16 sacc[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
+                const int key = 32 * kb + arow_key;
+#pragma unroll
+                for (int s2 = 0; s2 < NS; ++s2) {
+                    const int ch = 2 * s2 + hf;
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(ks + key * 256 + ((ch ^ (key & 15)) << 4)));
+                    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qb][s2], sacc[kb], 0, 0, 0);
                 }
             }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int kpos = k0 + 32 * kb + 16 * (e >> 3) + 8 * hf + (e & 7);
+                    const float v = (kpos <= tp[qb]) ? sacc[kb][e] * qscale : -INFINITY;
+                    sacc[kb][e] = v;
+                    mx = fmaxf(mx, v);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float mn = fmaxf(m[qb], mx);      // finite: key 0 <= every query position
+            const float corr = exp2f(m[qb] - mn);
+            float ps = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const float p = exp2f(sacc[kb][e] - mn);
+                    sacc[kb][e] = p;
+                    ps += p;
+                }
+            ps += __shfl_xor(ps, 32, 64);
+            lsum[qb] = lsum[qb] * corr + ps;
+            m[qb] = mn;
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) o[qb][b][e] *= corr;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    bf16x8 pb;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(sacc[kb][8 * u + e]);
+                    const int ch = 4 * kb + 2 * u + hf;
+#pragma unroll
+                    for (int b = 0; b < NB; ++b) {
+                        const int row = 32 * b + l32;
+                        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vs + row * 128 + ((ch ^ ((row >> 1) & 7)) << 4)));
+                        o[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[qb][b], 0, 0, 0);
+                    }
+                }
+        }
     }
-    if (qs + l32 < n) {
-        bf16_t* orow = out + (int64_t)(tok0 + qs + l32) * ldo + h * HD;
-        const float inv = 1.0f / lsum;
+    wait_vm0();   // the last (duplicate) tile copy must land before the workgroup ends
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int q = qs + 32 * qb + l32;
+        if (q >= n) continue;
+        bf16_t* orow = out + (int64_t)(tok0 + q) * ldo + h * HD;
+        const float inv = 1.0f / lsum[qb];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int c0 = 32 * b + 8 * j + 4 * hf;
                 uint2 pk;
-                pk.x = f32_to_bf16(o[b][4 * j + 0] * inv) | (uint32_t(f32_to_bf16(o[b][4 * j + 1] * inv)) << 16);
-                pk.y = f32_to_bf16(o[b][4 * j + 2] * inv) | (uint32_t(f32_to_bf16(o[b][4 * j + 3] * inv)) << 16);
+                pk.x = f32_to_bf16(o[qb][b][4 * j + 0] * inv) | (uint32_t(f32_to_bf16(o[qb][b][4 * j + 1] * inv)) << 16);
+                pk.y = f32_to_bf16(o[qb][b][4 * j + 2] * inv) | (uint32_t(f32_to_bf16(o[qb][b][4 * j + 3] * inv)) << 16);
                 *reinterpret_cast<uint2*>(orow + c0) = pk;
             }
     }
@@ -478,6 +531,8 @@ bool launch_hd(int G, int ntok, const void* q, int64_t ldq, void* out, int64_t l
 
 }  // namespace
 
+int attn_prefill_query_tile(int n_q, int n_kv) { return 32 * prefill_blocks(n_q / n_kv); }
+
 bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd) {
     const int G = n_q / n_kv;
     return act_fmt == FMT_BF16 && hd == 128 && (G == 1 || G == 2 || G == 4 || G == 8);
@@ -493,7 +548,7 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
     dim3 grid(n_work, n_kv);
 #define OUTLETS_PF_G(GG)                                                                        \
     case GG:                                                                                    \
-        hipLaunchKernelGGL((attn_prefill_mfma<GG>), grid, dim3(GG * 64), 0, st,                 \
+        hipLaunchKernelGGL((attn_prefill_mfma<GG, prefill_blocks(GG)>), grid, dim3(GG * 64), 0, st, \
                            static_cast<const bf16_t*>(qkv), ldq, static_cast<bf16_t*>(out), ldo, \
                            work, req_off, req_slot, page_table, max_pages,                      \
                            static_cast<const bf16_t*>(kpool), static_cast<const bf16_t*>(vpool), \

@@ -86,6 +86,8 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
 
 bool attn_supported(int n_q, int n_kv, int hd);
 bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd);
+// Queries per prefill attention work item (a multiple of 32).
+int attn_prefill_query_tile(int n_q, int n_kv);
 
 // Causal prefill attention on MFMA (bf16, hd 128).  work[2 * i], work[2 * i + 1]
 // = (request, 32-query tile) of workgroup row i; req_off = token offsets.
