@@ -46,9 +46,6 @@ namespace {
 #ifndef OUTLETS_GEMM_GM
 #define OUTLETS_GEMM_GM 8     // row tiles walked per column step within an XCD
 #endif
-#ifndef OUTLETS_GEMM_NT
-#define OUTLETS_GEMM_NT 0     // non-temporal output stores
-#endif
 constexpr int BK = OUTLETS_GEMM_BK;
 
 __device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
@@ -82,24 +79,6 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int mt, int nt, int& tm
     const int in = pid % (GM * nt);
     tm = first + in % gsize;
     tn = in / gsize;
-}
-
-// Output stores (optionally non-temporal, so the output stream does not
-// evict operand lines from L2).
-__device__ __forceinline__ void out_f32(float* p, float v) {
-#if OUTLETS_GEMM_NT
-    __builtin_nontemporal_store(v, p);
-#else
-    *p = v;
-#endif
-}
-template <typename T> __device__ __forceinline__ void out_act(T* p, float v) {
-#if OUTLETS_GEMM_NT
-    if constexpr (sizeof(T) == 4) __builtin_nontemporal_store(v, reinterpret_cast<float*>(p));
-    else __builtin_nontemporal_store(f32_to_bf16(v), reinterpret_cast<bf16_t*>(p));
-#else
-    store_act<T>(p, v);
-#endif
 }
 
 // LDS DMA through a raw buffer descriptor: each lane copies 16 bytes from
@@ -312,7 +291,26 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     wait_dma<0>();   // no LDS copy may outlive the workgroup
 
     // epilogue: lane holds column l32 of each 32x32 block, rows
-    // 8*(r/4) + 4*half + r%4 for accumulator element r
+    // 8*(r/4) + 4*half + r%4 for accumulator element r.  Outputs (and the
+    // residual) go through descriptors based at the tile's first row whose
+    // size ends at row M: stores to rows past M are dropped by the range
+    // check, so there are no per-element branches, and the offsets are 32-bit.
+    constexpr bool F32OUT = EPI == EPI_STORE_F32 || EPI == EPI_RESID_F32 || EPI == EPI_PARTIAL;
+    constexpr int OSZ = F32OUT ? 4 : static_cast<int>(sizeof(OutT));
+    const int rows_valid = min(BM, M - m0);
+    const int ldc = static_cast<int>(C.ldc), ldr = static_cast<int>(C.ldr);   // tile offsets fit 32 bits
+    char* cbase = static_cast<char*>(C.c) +
+                  ((EPI == EPI_PARTIAL ? (int64_t)blockIdx.y * C.split_stride : 0) + (int64_t)m0 * C.ldc) * OSZ;
+    const __amdgpu_buffer_rsrc_t rc = buf_rsrc(cbase, (int64_t)rows_valid * C.ldc * OSZ);
+    const __amdgpu_buffer_rsrc_t rr =
+        EPI == EPI_RESID_F32 ? buf_rsrc(C.resid + (int64_t)m0 * C.ldr, (int64_t)rows_valid * C.ldr * 4) : rc;
+    auto put = [&](uint32_t off, float v) {
+        if constexpr (OSZ == 4) {
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rc, off, 0, 0);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), rc, off, 0, 0);
+        }
+    };
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int n = n0 + wn * TN + j * 32 + l32;
@@ -322,38 +320,46 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             b_row(B, n, s, r);
             sc = bf16_to_f32(B.scale[s][r]);
         }
+        // the residual may alias the output (in-place update): load the
+        // column's FM blocks first so the loads overlap
+        float rv[EPI == EPI_RESID_F32 ? FM : 1][16];
+        if (EPI == EPI_RESID_F32) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = wm * TM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+                    rv[i][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                        rr, static_cast<uint32_t>((row * ldr + n) * 4), 0, 0));
+                }
+        }
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * TM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (m >= M) continue;
-                float v = acc[i][j][r] * sc;
-                if (EPI == EPI_STORE_F32) {
-                    out_f32(static_cast<float*>(C.c) + (int64_t)m * C.ldc + n, v);
-                } else if (EPI == EPI_STORE_ACT) {
-                    out_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + n, v);
+                const int row = wm * TM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+                const float v = acc[i][j][r] * sc;
+                if (EPI == EPI_STORE_F32 || EPI == EPI_STORE_ACT || EPI == EPI_PARTIAL) {
+                    put(static_cast<uint32_t>((row * ldc + n) * OSZ), v);
                 } else if (EPI == EPI_RESID_F32) {
-                    out_f32(static_cast<float*>(C.c) + (int64_t)m * C.ldc + n, C.resid[(int64_t)m * C.ldr + n] + v);
-                } else if (EPI == EPI_PARTIAL) {
-                    static_cast<float*>(C.c)[blockIdx.y * C.split_stride + (int64_t)m * C.ldc + n] = v;
+                    put(static_cast<uint32_t>((row * ldc + n) * OSZ), rv[i][r] + v);
                 } else if (EPI == EPI_SWIGLU) {
                     if ((j & 1) == 0) {
                         // partner fragment j + 1 holds the matching up column
                         float sc_u = 1.f;
                         if (E4M3) {
-                            int s, rr;
-                            b_row(B, n + 32, s, rr);
-                            sc_u = bf16_to_f32(B.scale[s][rr]);
+                            int s, rr2;
+                            b_row(B, n + 32, s, rr2);
+                            sc_u = bf16_to_f32(B.scale[s][rr2]);
                         }
                         const float g = v, u = acc[i][j + 1][r] * sc_u;
                         const int f = ((n >> 5) >> 1) * 32 + l32;
-                        out_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + f, silu_f(g) * u);
+                        put(static_cast<uint32_t>((row * ldc + f) * OSZ), silu_f(g) * u);
                     }
                 }
             }
-            // keep the compiler from hoisting the next fragment's loads and
-            // conversions over this one (it would run out of registers)
+            // keep the compiler from hoisting the next fragment's conversions
+            // over this one (it would run out of registers)
             __builtin_amdgcn_sched_barrier(0);
         }
     }
@@ -509,6 +515,7 @@ int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA
     if (K % BK || a.kseg % BK) { *why = "gemm: K must be a multiple of 64"; return OUTLETS_ERR_UNSUPPORTED; }
     if ((K / BK) < splits) { *why = "gemm: more K splits than K tiles"; return OUTLETS_ERR_UNSUPPORTED; }
     if (a.ld % 8 || b.ld % (w_fmt == FMT_E4M3 ? 16 : 8)) { *why = "gemm: row strides must keep 16-byte alignment"; return OUTLETS_ERR_UNSUPPORTED; }
+    if (a.ld > (1 << 22) || b.ld > (1 << 22)) { *why = "gemm: row strides above 4M elements (tile offsets are 32-bit)"; return OUTLETS_ERR_UNSUPPORTED; }
     for (int s = 0; s < 3; ++s) {
         if (a.p[s] && (reinterpret_cast<uintptr_t>(a.p[s]) & 15)) { *why = "gemm: A must be 16-byte aligned"; return OUTLETS_ERR_UNSUPPORTED; }
         if (b.p[s] && (reinterpret_cast<uintptr_t>(b.p[s]) & 15)) { *why = "gemm: B must be 16-byte aligned"; return OUTLETS_ERR_UNSUPPORTED; }
