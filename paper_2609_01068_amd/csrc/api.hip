@@ -513,6 +513,9 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
                 if (sk > 1) need = std::max(need, (size_t)sk * m * gemm_nk[g][0] * sizeof(float));
             }
         }
+        // large GEMMs split their last round of tiles over K: up to one
+        // 256 x 256 fp32 block per CU (256 CUs)
+        if (Tm > 256) need = std::max(need, (size_t)256 * 65536 * sizeof(float));
         c->splitk_bytes = need;
         if (need) ALLOC(c->splitk_ws, need);
     }

@@ -64,21 +64,24 @@ __device__ __forceinline__ void b_row(const GemmB& B, int n, int& s, int& r) {
 
 __device__ __forceinline__ float silu_f(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
-// Map the hardware workgroup id to a tile so that consecutive tiles run on
-// the same XCD (workgroups are dealt round-robin over the 8 XCDs) and walk
-// GM row-tiles before moving along N, so A rows and B columns are reused
-// from that XCD's L2.
-__device__ __forceinline__ void tile_of(int bid, int nb, int mt, int nt, int& tm, int& tn) {
-    const int q = nb / 8, r = nb % 8;
-    const int x = bid % 8, i = bid / 8;
-    const int pid = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+// Tile order: pid walks GM row-tiles before moving along N, so A rows and
+// B columns are reused from L2.
+__host__ __device__ __forceinline__ void tile_coords(int pid, int mt, int nt, int& tm, int& tn) {
     constexpr int GM = OUTLETS_GEMM_GM;
     const int group = pid / (GM * nt);
     const int first = group * GM;
-    const int gsize = min(mt - first, GM);
+    const int gsize = (mt - first < GM) ? mt - first : GM;
     const int in = pid % (GM * nt);
     tm = first + in % gsize;
     tn = in / gsize;
+}
+
+// Workgroups are dealt round-robin over the 8 XCDs: give each XCD a
+// contiguous run of the nb pids so that neighbouring tiles share its L2.
+__device__ __forceinline__ int xcd_pid(int bid, int nb) {
+    const int q = nb / 8, r = nb % 8;
+    const int x = bid % 8, i = bid / 8;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
 // LDS DMA through a raw buffer descriptor: each lane copies 16 bytes from
@@ -142,7 +145,7 @@ __device__ __forceinline__ int swz_chunk(int row, int c) {
 // - 1 is copied while slice k is multiplied.
 template <int EPI, bool E4M3, typename OutT, int WM, int WN, int BK, int STAGES>
 __global__ void __launch_bounds__(WM * WN * 64)
-gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split) {
+gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split, int pid0) {
     constexpr int BM = 256, BN = 256, NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
     constexpr int AROWB = BK * 2;                       // bytes per A row
@@ -157,9 +160,11 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     static_assert(ACP >= 1 && BCP >= 1, "tile too small for the wave count");
     __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGE];
 
+    // this launch covers tiles pid0 .. pid0 + gridDim.x - 1 of the tile order
     const int mt = (M + BM - 1) / BM, nt = N / BN;
+    const int tpid = pid0 + xcd_pid(blockIdx.x, gridDim.x);
     int tm, tn;
-    tile_of(blockIdx.x, mt * nt, mt, nt, tm, tn);
+    tile_coords(tpid, mt, nt, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kb = blockIdx.y * k_per_split;
     const int ke = min(K, kb + k_per_split);
@@ -295,13 +300,21 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     // residual) go through descriptors based at the tile's first row whose
     // size ends at row M: stores to rows past M are dropped by the range
     // check, so there are no per-element branches, and the offsets are 32-bit.
-    constexpr bool F32OUT = EPI == EPI_STORE_F32 || EPI == EPI_RESID_F32 || EPI == EPI_PARTIAL;
+    // EPI_PARTIAL_TILE writes the whole tile to its own 256 x 256 block of
+    // the workspace, (split, tile of this launch) in that order.
+    constexpr bool F32OUT = EPI == EPI_STORE_F32 || EPI == EPI_RESID_F32 || EPI == EPI_PARTIAL ||
+                            EPI == EPI_PARTIAL_TILE;
     constexpr int OSZ = F32OUT ? 4 : static_cast<int>(sizeof(OutT));
-    const int rows_valid = min(BM, M - m0);
-    const int ldc = static_cast<int>(C.ldc), ldr = static_cast<int>(C.ldr);   // tile offsets fit 32 bits
-    char* cbase = static_cast<char*>(C.c) +
+    const int rows_valid = EPI == EPI_PARTIAL_TILE ? BM : min(BM, M - m0);
+    const int ldc = EPI == EPI_PARTIAL_TILE ? BN : static_cast<int>(C.ldc);   // tile offsets fit 32 bits
+    const int ldr = static_cast<int>(C.ldr);
+    const int ncol0 = EPI == EPI_PARTIAL_TILE ? n0 : 0;       // column origin of the output block
+    char* cbase =
+        EPI == EPI_PARTIAL_TILE
+            ? static_cast<char*>(C.c) + ((int64_t)blockIdx.y * gridDim.x + (tpid - pid0)) * (BM * BN * 4)
+            : static_cast<char*>(C.c) +
                   ((EPI == EPI_PARTIAL ? (int64_t)blockIdx.y * C.split_stride : 0) + (int64_t)m0 * C.ldc) * OSZ;
-    const __amdgpu_buffer_rsrc_t rc = buf_rsrc(cbase, (int64_t)rows_valid * C.ldc * OSZ);
+    const __amdgpu_buffer_rsrc_t rc = buf_rsrc(cbase, (int64_t)rows_valid * ldc * OSZ);
     const __amdgpu_buffer_rsrc_t rr =
         EPI == EPI_RESID_F32 ? buf_rsrc(C.resid + (int64_t)m0 * C.ldr, (int64_t)rows_valid * C.ldr * 4) : rc;
     auto put = [&](uint32_t off, float v) {
@@ -339,8 +352,9 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             for (int r = 0; r < 16; ++r) {
                 const int row = wm * TM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
                 const float v = acc[i][j][r] * sc;
-                if (EPI == EPI_STORE_F32 || EPI == EPI_STORE_ACT || EPI == EPI_PARTIAL) {
-                    put(static_cast<uint32_t>((row * ldc + n) * OSZ), v);
+                if (EPI == EPI_STORE_F32 || EPI == EPI_STORE_ACT || EPI == EPI_PARTIAL ||
+                    EPI == EPI_PARTIAL_TILE) {
+                    put(static_cast<uint32_t>((row * ldc + n - ncol0) * OSZ), v);
                 } else if (EPI == EPI_RESID_F32) {
                     put(static_cast<uint32_t>((row * ldc + n) * OSZ), rv[i][r] + v);
                 } else if (EPI == EPI_SWIGLU) {
@@ -362,6 +376,37 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             // over this one (it would run out of registers)
             __builtin_amdgcn_sched_barrier(0);
         }
+    }
+}
+
+// ---------------------------------------------------------------- tail reduce
+// The last tiles of a large GEMM (fewer than the CUs) run as S K-splits into
+// per-tile fp32 blocks ws[s][t][256][256], t = pid - pid0; this sums the S
+// blocks of each element in order and applies the epilogue.  One thread per
+// element of a tile row; SwiGLU threads take gate columns only.
+template <int EPI, typename OutT>
+__global__ void __launch_bounds__(256)
+tile_reduce(int M, int N, int S, int ntail, int pid0, const float* ws, GemmC C) {
+    const int t = blockIdx.x >> 8, rl = blockIdx.x & 255, cl = threadIdx.x;
+    const int mt = (M + 255) / 256, nt = N / 256;
+    int tm, tn;
+    tile_coords(pid0 + t, mt, nt, tm, tn);
+    const int m = tm * 256 + rl, n = tn * 256 + cl;
+    if (m >= M) return;
+    if (EPI == EPI_SWIGLU && ((n >> 5) & 1)) return;
+    const int64_t e = (int64_t)rl * 256 + cl, blk = (int64_t)ntail * 65536;
+    float v = 0.f, u = 0.f;
+    for (int sp = 0; sp < S; ++sp) {
+        v += ws[sp * blk + (int64_t)t * 65536 + e];
+        if (EPI == EPI_SWIGLU) u += ws[sp * blk + (int64_t)t * 65536 + e + 32];
+    }
+    if (EPI == EPI_STORE_F32) static_cast<float*>(C.c)[(int64_t)m * C.ldc + n] = v;
+    else if (EPI == EPI_STORE_ACT) store_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + n, v);
+    else if (EPI == EPI_RESID_F32)
+        static_cast<float*>(C.c)[(int64_t)m * C.ldc + n] = C.resid[(int64_t)m * C.ldr + n] + v;
+    else if (EPI == EPI_SWIGLU) {
+        const int f = ((n >> 5) >> 1) * 32 + (n & 31);
+        store_act<OutT>(static_cast<OutT*>(C.c) + (int64_t)m * C.ldc + f, silu_f(v) * u);
     }
 }
 
@@ -471,16 +516,54 @@ gemm_f32_64x64(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split) 
 }
 
 template <int EPI, bool E4M3>
-void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& b,
-                 const GemmC& c, int splits, hipStream_t st) {
-    (void)act_fmt;
-    const int mt = (M + 255) / 256, nt = N / 256;
+void launch_tiles(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC& c, int splits,
+                  int pid0, int ntiles, hipStream_t st) {
     const int kps = ((K / BK + splits - 1) / splits) * BK;
-    dim3 grid(mt * nt, splits);
     hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, bf16_t, OUTLETS_GEMM_WM, OUTLETS_GEMM_WN,
                                           OUTLETS_GEMM_BK, OUTLETS_GEMM_STAGES>),
-                       grid, dim3(OUTLETS_GEMM_WM * OUTLETS_GEMM_WN * 64), 0, st, M, N, K,
-                       a, b, c, kps);
+                       dim3(ntiles, splits), dim3(OUTLETS_GEMM_WM * OUTLETS_GEMM_WN * 64), 0, st, M, N, K,
+                       a, b, c, kps, pid0);
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cache[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+template <int EPI, bool E4M3>
+void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& b,
+                 const GemmC& c, int splits, hipStream_t st, float* ws, size_t ws_bytes) {
+    (void)act_fmt;
+    const int mt = (M + 255) / 256, nt = N / 256, T = mt * nt;
+    // With one workgroup per CU, T tiles take ceil(T / W) rounds; when the
+    // last round holds only a few tiles, those tiles run instead as S K-splits
+    // (S * tail <= W workgroups of 1/S the work) and are summed by
+    // tile_reduce, so the last round costs about 1/S of a round.
+    const int W = device_cus();
+    const int full = T / W, tail = T % W;
+    int S = 1;
+    if (splits == 1 && EPI != EPI_PARTIAL && full >= 1 && full <= 64 && tail > 0 && ws) {
+        S = std::min({16, W / tail, (K / BK) / 4});
+        if ((size_t)S * tail * 65536 * sizeof(float) > ws_bytes) S = 1;
+    }
+    if (S < 2) {
+        launch_tiles<EPI, E4M3>(M, N, K, a, b, c, splits, 0, T, st);
+        return;
+    }
+    launch_tiles<EPI, E4M3>(M, N, K, a, b, c, 1, 0, T - tail, st);
+    GemmC pc{};
+    pc.c = ws;
+    launch_tiles<EPI_PARTIAL_TILE, E4M3>(M, N, K, a, b, pc, S, T - tail, tail, st);
+    hipLaunchKernelGGL((tile_reduce<EPI, bf16_t>), dim3(tail * 256), dim3(256), 0, st, M, N, S, tail,
+                       T - tail, ws, c);
 }
 
 template <int EPI>
@@ -562,8 +645,8 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
     const bool e4 = (w_fmt == FMT_E4M3);
 #define OUTLETS_GEMM_CASE(E)                                                        \
     case E:                                                                         \
-        if (e4) launch_mfma<E, true>(act_fmt, M, N, K, a, b, c, splits, st);        \
-        else launch_mfma<E, false>(act_fmt, M, N, K, a, b, c, splits, st);          \
+        if (e4) launch_mfma<E, true>(act_fmt, M, N, K, a, b, c, splits, st, ws, ws_bytes); \
+        else launch_mfma<E, false>(act_fmt, M, N, K, a, b, c, splits, st, ws, ws_bytes);  \
         break;
     switch (epi) {
         OUTLETS_GEMM_CASE(EPI_STORE_F32)

@@ -36,7 +36,8 @@ enum Epilogue : int {
     EPI_STORE_ACT = 1,  // C (act format) = acc
     EPI_RESID_F32 = 2,  // C (f32) = resid + acc   (C may alias resid)
     EPI_SWIGLU = 3,     // C (act) [M, N/2] = silu(gate) * up   (requires paired B)
-    EPI_PARTIAL = 4     // C (f32) + split * split_stride = acc over the split's K range
+    EPI_PARTIAL = 4,    // C (f32) + split * split_stride = acc over the split's K range
+    EPI_PARTIAL_TILE = 5  // internal: per-tile fp32 blocks of the K-split tail of a large GEMM
 };
 
 struct GemmC {
