@@ -48,6 +48,55 @@ rmsnorm_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float eps, T
     }
 }
 
+// Vectorised form for d = 1024 V (V = 1..8 groups of 4 floats per thread):
+// the row stays in registers between the sum of squares and the scaling,
+// and every access is a 16-byte (x, y2) or 8-byte (bf16 y, gamma) access
+// with consecutive threads on consecutive addresses.
+template <typename TY, typename TG, int V>
+__global__ void __launch_bounds__(256)
+rmsnorm_vec_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
+                   int64_t ldy, float* y2, int64_t ldy2) {
+    __shared__ float red[4];
+    const int64_t row = blockIdx.x;
+    const int t = threadIdx.x;
+    const float4* xr = reinterpret_cast<const float4*>(x + row * ldx);
+    float4 v[V];
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        v[j] = xr[j * 256 + t];
+        ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
+    }
+    ss = block_sum<256>(ss, red);
+    const float inv = 1.0f / sqrtf(ss / d + eps);
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        const int c = (j * 256 + t) * 4;
+        float g[4];
+        if constexpr (sizeof(TG) == 4) {
+            const float4 gv = *reinterpret_cast<const float4*>(gamma + c);
+            g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
+        } else {
+            const uint2 gv = *reinterpret_cast<const uint2*>(gamma + c);
+            g[0] = __uint_as_float(gv.x << 16); g[1] = __uint_as_float(gv.x & 0xffff0000u);
+            g[2] = __uint_as_float(gv.y << 16); g[3] = __uint_as_float(gv.y & 0xffff0000u);
+        }
+        const float o0 = v[j].x * inv * g[0], o1 = v[j].y * inv * g[1];
+        const float o2 = v[j].z * inv * g[2], o3 = v[j].w * inv * g[3];
+        if (y) {
+            if constexpr (sizeof(TY) == 4) {
+                *reinterpret_cast<float4*>(y + row * ldy + c) = make_float4(o0, o1, o2, o3);
+            } else {
+                uint2 pk;
+                pk.x = f32_to_bf16(o0) | (uint32_t(f32_to_bf16(o1)) << 16);
+                pk.y = f32_to_bf16(o2) | (uint32_t(f32_to_bf16(o3)) << 16);
+                *reinterpret_cast<uint2*>(y + row * ldy + c) = pk;
+            }
+        }
+        if (y2) *reinterpret_cast<float4*>(y2 + row * ldy2 + c) = make_float4(o0, o1, o2, o3);
+    }
+}
+
 // One block per token; thread work items are rotation pairs of the q and k
 // heads and value elements.
 template <typename T>
@@ -84,6 +133,54 @@ rope_kv_kernel(T* qkv, int64_t ld, const int32_t* tok_slot, const int32_t* tok_p
     // channel's 16 values of a page are contiguous
     const T* vrow = row + (n_q + n_kv) * hd;
     for (int w = threadIdx.x; w < n_kv * hd; w += 256) {
+        const int g = w / hd, c = w % hd;
+        vpool[(((int64_t)page * n_kv + g) * hd + c) * 16 + off] = vrow[w];
+    }
+}
+
+// bf16 form: one wave per token, four rotation pairs per lane and step
+// (8-byte loads and stores of the two halves, 16-byte cos/sin loads).
+__global__ void __launch_bounds__(256)
+rope_kv_bf16_kernel(int ntok, bf16_t* qkv, int64_t ld, const int32_t* tok_slot, const int32_t* tok_pos,
+                    const int32_t* page_table, int max_pages, bf16_t* kpool, bf16_t* vpool,
+                    const float* cos_t, const float* sin_t, int n_q, int n_kv, int hd) {
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= ntok) return;
+    const int lane = threadIdx.x & 63;
+    const int pos = tok_pos[t], slot = tok_slot[t];
+    const int half = hd / 2, quads = half / 4;
+    const int page = page_table[(int64_t)slot * max_pages + pos / 16];
+    const int off = pos % 16;
+    bf16_t* row = qkv + t * ld;
+    const float* cr = cos_t + (int64_t)pos * half;
+    const float* sr = sin_t + (int64_t)pos * half;
+    const int n_items = (n_q + n_kv) * quads;
+    for (int w = lane; w < n_items; w += 64) {
+        const int h = w / quads, c = (w % quads) * 4;
+        bf16_t* base = row + h * hd;
+        const uint2 a1 = *reinterpret_cast<const uint2*>(base + c);
+        const uint2 a2 = *reinterpret_cast<const uint2*>(base + c + half);
+        const float4 cs = *reinterpret_cast<const float4*>(cr + c);
+        const float4 sn = *reinterpret_cast<const float4*>(sr + c);
+        const float x1[4] = {__uint_as_float(a1.x << 16), __uint_as_float(a1.x & 0xffff0000u),
+                             __uint_as_float(a1.y << 16), __uint_as_float(a1.y & 0xffff0000u)};
+        const float x2[4] = {__uint_as_float(a2.x << 16), __uint_as_float(a2.x & 0xffff0000u),
+                             __uint_as_float(a2.y << 16), __uint_as_float(a2.y & 0xffff0000u)};
+        const float cv[4] = {cs.x, cs.y, cs.z, cs.w}, sv[4] = {sn.x, sn.y, sn.z, sn.w};
+        uint16_t y1[4], y2[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            y1[e] = f32_to_bf16(x1[e] * cv[e] - x2[e] * sv[e]);
+            y2[e] = f32_to_bf16(x2[e] * cv[e] + x1[e] * sv[e]);
+        }
+        const uint2 o1 = make_uint2(y1[0] | (uint32_t(y1[1]) << 16), y1[2] | (uint32_t(y1[3]) << 16));
+        const uint2 o2 = make_uint2(y2[0] | (uint32_t(y2[1]) << 16), y2[2] | (uint32_t(y2[3]) << 16));
+        bf16_t* dst = h < n_q ? base : kpool + (((int64_t)page * n_kv + (h - n_q)) * 16 + off) * hd;
+        *reinterpret_cast<uint2*>(dst + c) = o1;
+        *reinterpret_cast<uint2*>(dst + c + half) = o2;
+    }
+    const bf16_t* vrow = row + (n_q + n_kv) * hd;
+    for (int w = lane; w < n_kv * hd; w += 64) {
         const int g = w / hd, c = w % hd;
         vpool[(((int64_t)page * n_kv + g) * hd + c) * 16 + off] = vrow[w];
     }
@@ -206,6 +303,33 @@ void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x,
                     const void* gamma, float eps, void* y, int64_t ldy, float* y2,
                     int64_t ldy2, hipStream_t st) {
     if (rows <= 0) return;
+    // vectorised path: d a multiple of 1024 up to 8192, 16-byte aligned rows
+    const bool vec = d % 1024 == 0 && d <= 8192 && ldx % 4 == 0 && (!y || ldy % 4 == 0) &&
+                     (!y2 || ldy2 % 4 == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                     (!y || reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
+                     (!y2 || reinterpret_cast<uintptr_t>(y2) % 16 == 0) &&
+                     reinterpret_cast<uintptr_t>(gamma) % 16 == 0;
+    if (vec) {
+        const int V = d / 1024;
+#define OUTLETS_NORM_V(TY, TG)                                                                  \
+    switch (V) {                                                                                \
+        case 1: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 1>), dim3(rows), dim3(256), 0, st, d, x, ldx, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2); break; \
+        case 2: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 2>), dim3(rows), dim3(256), 0, st, d, x, ldx, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2); break; \
+        case 4: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 4>), dim3(rows), dim3(256), 0, st, d, x, ldx, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2); break; \
+        case 8: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 8>), dim3(rows), dim3(256), 0, st, d, x, ldx, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2); break; \
+        default: goto scalar;                                                                   \
+    }
+        if (act_fmt == FMT_F32) { OUTLETS_NORM_V(float, float) }
+        else if (gamma_fmt == FMT_F32) { OUTLETS_NORM_V(bf16_t, float) }
+        else { OUTLETS_NORM_V(bf16_t, bf16_t) }
+#undef OUTLETS_NORM_V
+        return;
+    }
+scalar:
     if (act_fmt == FMT_F32) {
         hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(rows), dim3(256), 0, st, d, x, ldx,
                            static_cast<const float*>(gamma), eps, static_cast<float*>(y), ldy, y2, ldy2);
@@ -227,6 +351,11 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
         hipLaunchKernelGGL((rope_kv_kernel<float>), dim3(ntok), dim3(256), 0, st,
                            static_cast<float*>(qkv), ld, tok_slot, tok_pos, page_table, max_pages,
                            static_cast<float*>(kpool), static_cast<float*>(vpool), cos_t, sin_t,
+                           n_q, n_kv, hd);
+    else if (hd % 8 == 0 && ld % 4 == 0 && reinterpret_cast<uintptr_t>(qkv) % 8 == 0)
+        hipLaunchKernelGGL(rope_kv_bf16_kernel, dim3((ntok + 3) / 4), dim3(256), 0, st, ntok,
+                           static_cast<bf16_t*>(qkv), ld, tok_slot, tok_pos, page_table, max_pages,
+                           static_cast<bf16_t*>(kpool), static_cast<bf16_t*>(vpool), cos_t, sin_t,
                            n_q, n_kv, hd);
     else
         hipLaunchKernelGGL((rope_kv_kernel<bf16_t>), dim3(ntok), dim3(256), 0, st,
