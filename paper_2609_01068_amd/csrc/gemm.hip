@@ -579,10 +579,21 @@ void launch_f32(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
     if (w_fmt == FMT_F32 || epi == EPI_PARTIAL) return 1;
     const int tiles = ((M + 255) / 256) * (N / 256);
-    if (tiles >= 192) return 1;
-    int s = (384 + tiles - 1) / tiles;
-    s = std::min(s, std::max(1, (K / BK) / 4));   // keep >= 4 K slices per split
-    return std::min(s, 16);
+    const int W = device_cus();
+    if (tiles >= W) return 1;
+    // Cost in units of one tile's full-K pass: ceil(tiles * s / W) rounds of
+    // 1/s of a pass, plus the fp32 partials written and re-read by the reduce
+    // (2 * 4 B * M * N per split at ~5 TB/s against ~1.3 us per 64-deep K
+    // slice of a tile).
+    const double alpha = 512.0 * M * N / (6.5e6 * K);
+    const int smax = std::min(16, std::max(1, (K / BK) / 4));   // keep >= 4 K slices per split
+    int best = 1;
+    double best_cost = 1.0;
+    for (int sp = 2; sp <= smax; ++sp) {
+        const double cost = (double)((tiles * sp + W - 1) / W) / sp + alpha * sp;
+        if (cost < best_cost) { best = sp; best_cost = cost; }
+    }
+    return best;
 }
 
 int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
