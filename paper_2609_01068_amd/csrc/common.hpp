@@ -35,14 +35,14 @@ template <typename T> __device__ __forceinline__ void store_act(T* p, float v);
 template <> __device__ __forceinline__ void store_act<float>(float* p, float v) { *p = v; }
 template <> __device__ __forceinline__ void store_act<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
 
-// OCP E4M3 code pair (bytes 0/1 or 2/3 of a dword) -> two binary32 values,
-// using gfx950's hardware fp8 conversion (OCP encoding on this target).
+// Four OCP E4M3 codes (one dword) -> four bf16 (two packed dwords), using
+// gfx950's hardware fp8 conversion (OCP encoding on this target).
 __device__ __forceinline__ void e4m3x4_to_bf16x4(uint32_t codes, uint32_t& lo, uint32_t& hi) {
-    auto a = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(codes), false);
-    auto b = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(codes), true);
-    // every e4m3 value is exactly representable in bf16: truncation is exact
-    lo = (__float_as_uint(a[0]) >> 16) | (__float_as_uint(a[1]) & 0xFFFF0000u);
-    hi = (__float_as_uint(b[0]) >> 16) | (__float_as_uint(b[1]) & 0xFFFF0000u);
+    // v_cvt_scalef32_pk_bf16_fp8 with scale 1: two OCP e4m3 codes (bytes 0-1,
+    // or 2-3 with op_sel) to two bf16 in one instruction; every e4m3 value is
+    // exactly representable in bf16, so the conversion is exact
+    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes, 1.0f, false));
+    hi = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes, 1.0f, true));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
