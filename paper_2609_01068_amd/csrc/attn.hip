@@ -14,6 +14,8 @@
 // pages are stored [hd][16 tokens]).
 //
 // Prefill (bf16, hd 128): a flash-attention kernel on MFMA, see below.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "outlets.h"
@@ -21,6 +23,10 @@
 namespace outlets {
 
 namespace {
+
+// 2^x with the hardware v_exp_f32 (results below 2^-126 flush to zero, which
+// only ever drops probabilities that vanish next to the running maximum).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 16-byte LDS DMA per lane (lane i writes lds_base + 16 i), its wait, and a
 // workgroup barrier without the release fence (the DMA is ordered by the
@@ -96,8 +102,8 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
 #pragma unroll
             for (int x = 1; x < 16; x <<= 1) mx = fmaxf(mx, __shfl_xor(mx, x, 64));
             const float mn = fmaxf(m[h], mx);   // finite: key 0 of the page is valid
-            const float corr = exp2f(m[h] - mn);
-            const float p = valid ? exp2f(s - mn) : 0.f;
+            const float corr = fast_exp2(m[h] - mn);
+            const float p = valid ? fast_exp2(s - mn) : 0.f;
             float ps = p;
 #pragma unroll
             for (int x = 1; x < 16; x <<= 1) ps += __shfl_xor(ps, x, 64);
@@ -131,7 +137,7 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
 #pragma unroll
         for (int v = 0; v < NW; ++v) {
             if (sm[v][h] == -INFINITY) continue;   // wave had no page
-            const float f = exp2f(sm[v][h] - mx);
+            const float f = fast_exp2(sm[v][h] - mx);
             L = fmaf(sl[v][h], f, L);
             O = fmaf(so[v][h][c], f, O);
         }
@@ -140,10 +146,14 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
 }
 
 // ---------------------------------------------------------------- prefill, MFMA
-// Query blocks per wave: two where the registers allow (G = 2, 4), one where
-// eight waves share a SIMD pair's register file (G = 8) or a lone wave would
-// spill (G = 1).
-constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? 2 : 1; }
+// Query blocks per wave (32 queries each).  One block keeps a wave within
+// 256 registers, so two waves share each SIMD and one's softmax overlaps the
+// other's MFMAs; this measured faster than two blocks per wave (which share
+// every K/V fragment read but need 400+ registers, one wave per SIMD).
+#ifndef OUTLETS_PREFILL_QB
+#define OUTLETS_PREFILL_QB 1   // query blocks per wave for 2 and 4 heads per group
+#endif
+constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? OUTLETS_PREFILL_QB : 1; }
 
 // One workgroup per (request, tile of 32 QB queries, KV head); wave w
 // computes query head g * G + w for the tile's QB blocks of 32 queries, so the
@@ -173,7 +183,7 @@ __device__ __forceinline__ uint4 zero_tail_bf16x8(uint4 v, int valid) {
 }
 
 template <int G, int QB>
-__global__ void __launch_bounds__(G * 64)
+__global__ void __launch_bounds__(G * 64, QB == 1 ? 2 : 1)
 attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
                   const int32_t* req_off, const int32_t* req_slot, const int32_t* page_table,
                   int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale) {
@@ -249,8 +259,12 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
         }
     };
 
-    issue(0, 0);
-    for (int kt = 0; kt < ntiles; ++kt) {
+    // One 64-key tile.  MASKED: apply the causal mask (tiles holding a key
+    // past the tile's first query); tiles wholly before it skip the mask.
+    // The running max m is kept pre-scaled (log2 units), so one FMA forms the
+    // exponent of each probability.
+    auto tile = [&](int kt, auto masked_tag) {
+        constexpr bool MASKED = decltype(masked_tag)::value;
         wait_vm0();
         block_barrier();      // tile kt is in LDS; every wave is done with tile kt-1
         issue(min(kt + 1, ntiles - 1), (kt + 1) & 1);
@@ -277,30 +291,39 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int kpos = k0 + 32 * kb + 16 * (e >> 3) + 8 * hf + (e & 7);
-                    const float v = (kpos <= tp[qb]) ? sacc[kb][e] * qscale : -INFINITY;
-                    sacc[kb][e] = v;
-                    mx = fmaxf(mx, v);
+                    if (MASKED) {
+                        const int kpos = k0 + 32 * kb + 16 * (e >> 3) + 8 * hf + (e & 7);
+                        if (kpos > tp[qb]) sacc[kb][e] = -INFINITY;
+                    }
+                    mx = fmaxf(mx, sacc[kb][e]);
                 }
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float mn = fmaxf(m[qb], mx);      // finite: key 0 <= every query position
-            const float corr = exp2f(m[qb] - mn);
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * qscale;   // finite: key 0 <= every query position
+            // The reference max m moves only when the tile's max exceeds it by
+            // more than 8 (probabilities then stay <= 2^8), so the rescaling of
+            // O and l is skipped, wave-uniformly, on most tiles; O / l is
+            // unchanged by the choice of reference.
+            const bool grow = mx > m[qb] + 8.f;
+            if (__any(grow)) {
+                const float mn = grow ? mx : m[qb];
+                const float corr = fast_exp2(m[qb] - mn);
+                m[qb] = mn;
+                lsum[qb] *= corr;
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) o[qb][b][e] *= corr;
+            }
+            const float nmn = -m[qb];
             float ps = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const float p = exp2f(sacc[kb][e] - mn);
+                    const float p = fast_exp2(fmaf(sacc[kb][e], qscale, nmn));
                     sacc[kb][e] = p;
                     ps += p;
                 }
-            ps += __shfl_xor(ps, 32, 64);
-            lsum[qb] = lsum[qb] * corr + ps;
-            m[qb] = mn;
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) o[qb][b][e] *= corr;
+            lsum[qb] += ps + __shfl_xor(ps, 32, 64);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -317,7 +340,13 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
                     }
                 }
         }
-    }
+    };
+
+    issue(0, 0);
+    // tiles whose last key (64 kt + 63) is at or before the first query qs
+    const int nfull = min(ntiles, (qs + 1) / BKV);
+    for (int kt = 0; kt < nfull; ++kt) tile(kt, std::false_type{});
+    for (int kt = nfull; kt < ntiles; ++kt) tile(kt, std::true_type{});
     wait_vm0();   // the last (duplicate) tile copy must land before the workgroup ends
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -427,12 +456,12 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
         mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
         const float mn = fmaxf(m, mx);                 // finite: key 16 pi < nkeys
-        const float corr = exp2f(m - mn);
+        const float corr = fast_exp2(m - mn);
         float ps = 0.f;
         s16x4 pb;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float pv = exp2f(v[i] - mn);
+            const float pv = fast_exp2(v[i] - mn);
             ps += pv;
             pb[i] = static_cast<short>(f32_to_bf16(pv));
         }
@@ -499,7 +528,7 @@ attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_
     float L = 0.f, O = 0.f;
     for (int c = c0; c < c1; ++c) {
         const float* rec = part + (((int64_t)c * n_kv + g) * G + col) * (HD + 2);
-        const float f = exp2f(rec[0] - M);
+        const float f = fast_exp2(rec[0] - M);
         L = fmaf(rec[1], f, L);
         O = fmaf(rec[2 + ch], f, O);
     }
