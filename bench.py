@@ -31,10 +31,11 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def gemm_flops(shape, T: int):
-    """Algorithmic FLOPs per launch of each GEMM group for T tokens."""
+def gemm_flops(shape, T: int, attn_gate: bool = False):
+    """Algorithmic FLOPs per launch of each GEMM group for T tokens (the QKV
+    GEMM also produces the Gated Attention gate when ``attn_gate``)."""
     d, hd = shape.d, shape.head_dim
-    qkv = (shape.n_q + 2 * shape.n_kv) * hd
+    qkv = (shape.n_q * (2 if attn_gate else 1) + 2 * shape.n_kv) * hd
     return {
         "FUSE_GEMM": 2.0 * T * d * 3 * d,
         "QKV_GEMM": 2.0 * T * qkv * d,
@@ -118,7 +119,7 @@ def bench_decode(a):
     from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
     from synth import device_states, make_lengths, make_weights, workload
 
-    wl = workload(3)
+    wl = workload(3, attn_gate=a.attn_gate)
     steps = a.steps
     print(f"[bench] generating {wl.name} weights", file=sys.stderr, flush=True)
     W = make_weights(wl, a.seed)
@@ -172,7 +173,8 @@ def bench_decode(a):
         "data": "synthetic (seeded on device; U[256,8192] cached prompt tokens; fresh N(0,1) x (1,4,16) states per step)",
         "config": {"workload": "8B-shaped bf16 draft layer + length head, dynamic re-prediction: 512 in-flight "
                                "requests with paged draft KV caches of U[256, 8192] tokens (page 16), one new "
-                               "token per request per step", "requests": B, "cached_tokens_at_start": cached0},
+                               "token per request per step", "requests": B, "cached_tokens_at_start": cached0,
+                   "attn_gate": wl.attn_gate},
         "roofline": {"kernel": "decode attention over the paged KV cache", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
                      "traffic": recorded_traffic("decode_attention_8b_b512.md", "attn.hip", "attn"),
@@ -190,7 +192,7 @@ def bench_prefill(a, cfg_id):
     from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
     from synth import device_states, make_lengths, make_weights, workload
 
-    wl = workload(cfg_id)
+    wl = workload(cfg_id, attn_gate=a.attn_gate)
     print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
     W = make_weights(wl, a.seed)
     lens = make_lengths(wl, a.seed)
@@ -221,7 +223,7 @@ def bench_prefill(a, cfg_id):
     prof = pred.profile_read("prefill")
     pred.profile(False)
     ms_per_step = max(ev0.elapsed_time(ev1), wall * 1e3) / a.steps
-    flops = gemm_flops(wl.shape, T)
+    flops = gemm_flops(wl.shape, T, wl.attn_gate)
     kernels = {}
     for name, (ms, n) in prof.items():
         if n:
@@ -237,7 +239,8 @@ def bench_prefill(a, cfg_id):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if wl.weight_fmt == "bf16" else "bf16 (e4m3 weights)",
         "data": "synthetic (seeded; lognormal prompt lengths; N(0,1) x (1,4,16) target states drawn on device)",
         "config": {"workload": wl.name, "requests": B, "prompt_tokens": T, "d": wl.shape.d,
-                   "heads": [wl.shape.n_q, wl.shape.n_kv], "ffn": wl.shape.ffn, "weights": wl.weight_fmt},
+                   "heads": [wl.shape.n_q, wl.shape.n_kv], "ffn": wl.shape.ffn, "weights": wl.weight_fmt,
+                   "attn_gate": wl.attn_gate},
         "draft_tokens_per_s": T / (ms_per_step / 1e3),
         "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -262,6 +265,8 @@ def main(argv=None):
                          "in-flight requests with 256..8192 cached tokens, timed decode steps; "
                          "prefill-8b-large: 256 requests (~466k tokens) in one call; "
                          "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests")
+    ap.add_argument("--attn-gate", action="store_true",
+                    help="draft layer with the Gated Attention output gate (Section 4.1)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 times); used to scale "
                          "rocprof's FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -292,7 +297,7 @@ def main(argv=None):
     if a.workload != "prefill-8b":
         return bench_prefill(a, {"prefill-8b-large": 2, "prefill-70b-e4m3": 4}[a.workload])
 
-    wl = workload(1)
+    wl = workload(1, attn_gate=a.attn_gate)
     print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
     W = make_weights(wl, a.seed)
     lens = make_lengths(wl, a.seed)
@@ -336,7 +341,7 @@ def main(argv=None):
     req_s = B / (ms_per_step / 1e3)
     tok_s = (T + B) / (ms_per_step / 1e3)
 
-    flops = gemm_flops(wl.shape, T)
+    flops = gemm_flops(wl.shape, T, wl.attn_gate)
     kernels = {}
     for name, (ms, n) in prof_pre.items():
         if n:
@@ -365,7 +370,7 @@ def main(argv=None):
                                "prompts clipped to [32, 4096], static prediction + 1 dynamic step per request",
                    "requests": B, "prompt_tokens": T, "d": wl.shape.d, "heads": [wl.shape.n_q, wl.shape.n_kv],
                    "head_dim": wl.shape.head_dim, "ffn": wl.shape.ffn, "head_hidden": wl.shape.head_hidden,
-                   "page_size": 16},
+                   "page_size": 16, "attn_gate": wl.attn_gate},
         "draft_tokens_per_s": tok_s,
         "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

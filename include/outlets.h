@@ -122,6 +122,12 @@ typedef struct outlets_config {
  *        (the weight value is decode(code) * scale[row]).
  *   gamma_attn, gamma_mlp, gamma_final [d]: RMSNorm gains
  *   head_w1 [H1, 2d], head_b1 [H1], head_w2 [H1], head_b2 [1]
+ *   w_attn_gate [n_q*hd, d] (optional, NULL = plain attention): Gated
+ *     Attention (Section 4.1, citing its source for the formula): the
+ *     attention output of query head h, channel c is multiplied by
+ *     sigmoid((a W_attn_gate^T)[h*hd + c]), a the normed layer input that
+ *     also feeds Q/K/V, before W_o.  Stored like the other big linears
+ *     (weight_fmt, with s_attn_gate row scales for E4M3).
  * Element format: weight_fmt for the big linears; F32 for the rest when
  * weight_fmt is F32, BF16 otherwise.
  */
@@ -141,6 +147,7 @@ typedef struct outlets_weights {
     const void* head_b1;
     const void* head_w2;
     const void* head_b2;
+    const void* w_attn_gate;  const void* s_attn_gate;
 } outlets_weights;
 
 typedef struct outlets_ctx outlets_ctx;

@@ -16,7 +16,13 @@ here is stated next to the code:
   before the SwiGLU MLP; bias-free linears; rotate-half RoPE with frequencies
   theta^(-2c/hd) and no frequency rescaling; grouped-query attention where
   query head h reads key/value head floor(h / (n_q / n_kv)); causal within
-  a request.  The paper's Gated Attention is not used (plain GQA).
+  a request.
+* Gated Attention (Section 4.1 names it and cites its source without giving
+  a formula): optional, off unless the weights carry ``w_attn_gate``.  The
+  reading taken is the elementwise output gate of the cited work: each
+  attention output element, per query head and channel, is multiplied by
+  sigmoid of a bias-free linear map of the same normed input that feeds
+  Q/K/V, before the heads are concatenated into W_o.
 * h^draft is the final RMSNorm of the layer output (both heads read it).
 * Length head (Section 4.2): the pooled state p = [mean over the request's
   tokens of h^draft ; h^draft of the newest token] goes through
@@ -54,9 +60,11 @@ class OracleShape:
 
 
 def decode_weights(stored: Dict[str, object]) -> Dict[str, np.ndarray]:
-    """Stored weights (as the seeded generator returns them) -> float64."""
+    """Stored weights (as the seeded generator returns them) -> float64.
+    The attention output gate ``w_attn_gate`` is carried over when present."""
     fmt = stored["_fmt"]
-    return {k: decode_weight(stored[k], fmt[k]) for k in WEIGHT_KEYS}
+    keys = WEIGHT_KEYS + (("w_attn_gate",) if "w_attn_gate" in stored else ())
+    return {k: decode_weight(stored[k], fmt[k]) for k in keys}
 
 
 # ------------------------------------------------------------------ layers
@@ -121,6 +129,16 @@ def silu(u: np.ndarray) -> np.ndarray:
     return u / (1.0 + np.exp(-u))
 
 
+def sigmoid(u: np.ndarray) -> np.ndarray:
+    return 1.0 / (1.0 + np.exp(-u))
+
+
+def attention_output_gate(o: np.ndarray, a: np.ndarray, w_attn_gate: np.ndarray) -> np.ndarray:
+    """Gated Attention output gate: o [n, n_q*hd] (heads concatenated) times
+    sigmoid(a W_g^T) elementwise, a the normed layer input [n, d]."""
+    return o * sigmoid(a @ w_attn_gate.T)
+
+
 def swiglu_mlp(b: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray,
                w_down: np.ndarray) -> np.ndarray:
     """(silu(b W_gate^T) * (b W_up^T)) W_down^T."""
@@ -169,14 +187,16 @@ class OracleModel:
         k_all = np.concatenate([k_prev, k], axis=0)
         v_all = np.concatenate([v_prev, v], axis=0)
         k_pos = np.concatenate([k_pos_prev, positions])
-        o = causal_gqa_attention(q, k_all, v_all, positions, k_pos)
-        x1 = f + o.reshape(n, s.n_q * s.head_dim) @ w["w_o"].T
+        o = causal_gqa_attention(q, k_all, v_all, positions, k_pos).reshape(n, s.n_q * s.head_dim)
+        if "w_attn_gate" in w:
+            o = attention_output_gate(o, a, w["w_attn_gate"])
+        x1 = f + o @ w["w_o"].T
         b = rms_norm(x1, w["gamma_mlp"], s.rms_eps)
         x2 = x1 + swiglu_mlp(b, w["w_gate"], w["w_up"], w["w_down"])
         h_draft = rms_norm(x2, w["gamma_final"], s.rms_eps)
         if capture is not None:
             capture.update(fused=f, norm_attn=a, q=q.reshape(n, -1), k=k, v=v,
-                           attn=o.reshape(n, -1), x1=x1, norm_mlp=b,
+                           attn=o, x1=x1, norm_mlp=b,
                            mlp_act=silu(b @ w["w_gate"].T) * (b @ w["w_up"].T), x2=x2,
                            hdraft=h_draft)
         return h_draft, k_all, v_all

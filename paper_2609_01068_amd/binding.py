@@ -63,7 +63,7 @@ class outlets_config(C.Structure):
 WEIGHT_FIELDS = [
     "w_proj", "s_proj", "w_q", "s_q", "w_k", "s_k", "w_v", "s_v", "w_o", "s_o",
     "w_gate", "s_gate", "w_up", "s_up", "w_down", "s_down", "gamma_attn", "gamma_mlp",
-    "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2",
+    "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2", "w_attn_gate", "s_attn_gate",
 ]
 
 

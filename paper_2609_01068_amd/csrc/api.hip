@@ -50,6 +50,7 @@ struct outlets_ctx {
     int device = 0;
     int act_fmt = 0, w_fmt = 0, small_fmt = 0;  // small_fmt: gains and head
     int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
+    bool gated = false;          // Gated Attention: q|k|v|g rows, output gate in attention
     std::unique_ptr<Pager> pager;
     int max_pages = 0;
 
@@ -203,7 +204,7 @@ GemmB gemm_b1(const void* p, const void* scale, int64_t rows, int64_t ld) {
     GemmB b{};
     b.p[0] = p;
     b.scale[0] = static_cast<const uint16_t*>(scale);
-    b.nend[0] = b.nend[1] = b.nend[2] = static_cast<int32_t>(rows);
+    b.nend[0] = b.nend[1] = b.nend[2] = b.nend[3] = static_cast<int32_t>(rows);
     b.ld = ld;
     return b;
 }
@@ -241,7 +242,13 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
     g.b_qkv.scale[2] = static_cast<const uint16_t*>(w.s_v);
     g.b_qkv.nend[0] = static_cast<int32_t>(c->qdim);
     g.b_qkv.nend[1] = static_cast<int32_t>(c->qdim + c->kvdim);
-    g.b_qkv.nend[2] = static_cast<int32_t>(c->qkv_dim);
+    g.b_qkv.nend[2] = static_cast<int32_t>(c->qdim + 2 * c->kvdim);
+    g.b_qkv.nend[3] = static_cast<int32_t>(c->qkv_dim);
+    if (c->gated) {
+        // Gated Attention: the gate projection is a fourth row segment
+        g.b_qkv.p[3] = w.w_attn_gate;
+        g.b_qkv.scale[3] = static_cast<const uint16_t*>(w.s_attn_gate);
+    }
     g.a_o = gemm_a(c->attn, c->qdim, c->qdim);
     g.b_o = gemm_b1(w.w_o, w.s_o, d, c->qdim);
     g.a_gu = gemm_a(c->b_norm, d, d);
@@ -305,19 +312,21 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
                      c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
                      c->cfg.head_dim, st); }
     { KTimer t(c, OUTLETS_K_ATTN, st);
+      const void* gate = c->gated ? static_cast<const char*>(c->qkv) + (c->qdim + 2 * c->kvdim) * fmt_bytes(af)
+                                  : nullptr;
       if (prefill && c->n_work > 0)
           launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->qkv, c->qkv_dim, c->attn, c->qdim,
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
-                              c->cfg.n_q_heads, c->cfg.n_kv_heads, st);
+                              c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
           launch_attn_decode(n, c->n_work, c->d_meta + c->work_off, c->d_meta + c->tiles_off, c->qkv,
                              c->qkv_dim, c->attn, c->qdim, req_slot, req_start, c->page_table,
                              c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
-                             c->decode_part, st);
+                             c->decode_part, gate, st);
       else
           launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
                             c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
-                            c->cfg.n_kv_heads, c->cfg.head_dim, st); }
+                            c->cfg.n_kv_heads, c->cfg.head_dim, gate, st); }
     { KTimer t(c, OUTLETS_K_O_GEMM, st);
       gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
@@ -434,6 +443,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         const void* sc[] = {w.s_proj, w.s_q, w.s_k, w.s_v, w.s_o, w.s_gate, w.s_up, w.s_down};
         for (const void* p : sc)
             if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
+        if (w.w_attn_gate && !w.s_attn_gate)
+            return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
     }
     HIP_TRY(hipSetDevice(device), "hipSetDevice");
 
@@ -453,7 +464,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     c->d = cfg->d_model;
     c->qdim = static_cast<int64_t>(cfg->n_q_heads) * cfg->head_dim;
     c->kvdim = static_cast<int64_t>(cfg->n_kv_heads) * cfg->head_dim;
-    c->qkv_dim = c->qdim + 2 * c->kvdim;
+    c->gated = w.w_attn_gate != nullptr;
+    c->qkv_dim = c->qdim + 2 * c->kvdim + (c->gated ? c->qdim : 0);
     c->F = cfg->ffn_dim;
     c->H1 = cfg->head_hidden;
     c->max_pages = c->pager->max_pages_per_seq();

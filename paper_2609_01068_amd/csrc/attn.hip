@@ -28,6 +28,12 @@ namespace {
 // only ever drops probabilities that vanish next to the running maximum).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Gated Attention output gate: sigmoid of the gate projection (gate values
+// sit in the q|k|v|g row, one per query-head channel).
+__device__ __forceinline__ float sigmoid_f(float x) {
+    return __builtin_amdgcn_rcpf(1.0f + fast_exp2(-1.4426950408889634f * x));
+}
+
 // 16-byte LDS DMA per lane (lane i writes lds_base + 16 i), its wait, and a
 // workgroup barrier without the release fence (the DMA is ordered by the
 // explicit wait; the empty asm statements keep the compiler from moving
@@ -46,7 +52,7 @@ template <typename T, int HD, int G>
 __global__ void __launch_bounds__(256)
 attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* tok_slot,
                   const int32_t* tok_pos, const int32_t* page_table, int max_pages,
-                  const T* kpool, const T* vpool, int n_kv, float qscale) {
+                  const T* kpool, const T* vpool, int n_kv, float qscale, const T* gate) {
     constexpr int NW = 4, DP = HD / 4, DV = HD / 64;
     __shared__ float qs[G][HD];
     __shared__ float sm[NW][G], sl[NW][G];
@@ -141,7 +147,9 @@ attn_paged_kernel(const T* q, int64_t ldq, T* out, int64_t ldo, const int32_t* t
             L = fmaf(sl[v][h], f, L);
             O = fmaf(so[v][h][c], f, O);
         }
-        store_act<T>(out + t * ldo + (int64_t)(g * G + h) * HD + c, O / L);
+        float y = O / L;
+        if (gate) y *= sigmoid_f(load_act<T>(gate + t * ldq + (int64_t)(g * G + h) * HD + c));
+        store_act<T>(out + t * ldo + (int64_t)(g * G + h) * HD + c, y);
     }
 }
 
@@ -186,7 +194,8 @@ template <int G, int QB>
 __global__ void __launch_bounds__(G * 64, QB == 1 ? 2 : 1)
 attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
                   const int32_t* req_off, const int32_t* req_slot, const int32_t* page_table,
-                  int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale) {
+                  int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale,
+                  const bf16_t* gate) {
     constexpr int HD = 128, NW = G, BKV = 64, NS = HD / 16, NB = HD / 32, QT = 32 * QB;
     constexpr int KB = BKV * HD * 2, STAGE = 2 * KB;    // K [64][128] + V^T [128][64], bf16
     constexpr int KCP = (KB / 1024) / NW;               // DMA copies per wave for K (and for V)
@@ -354,14 +363,25 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
         if (q >= n) continue;
         bf16_t* orow = out + (int64_t)(tok0 + q) * ldo + h * HD;
         const float inv = 1.0f / lsum[qb];
+        const bf16_t* grow = gate ? gate + (int64_t)(tok0 + q) * ldq + h * HD : nullptr;
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int c0 = 32 * b + 8 * j + 4 * hf;
+                float y[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) y[e] = o[qb][b][4 * j + e] * inv;
+                if (grow) {
+                    const uint2 gv = *reinterpret_cast<const uint2*>(grow + c0);
+                    y[0] *= sigmoid_f(__uint_as_float(gv.x << 16));
+                    y[1] *= sigmoid_f(__uint_as_float(gv.x & 0xffff0000u));
+                    y[2] *= sigmoid_f(__uint_as_float(gv.y << 16));
+                    y[3] *= sigmoid_f(__uint_as_float(gv.y & 0xffff0000u));
+                }
                 uint2 pk;
-                pk.x = f32_to_bf16(o[qb][b][4 * j + 0] * inv) | (uint32_t(f32_to_bf16(o[qb][b][4 * j + 1] * inv)) << 16);
-                pk.y = f32_to_bf16(o[qb][b][4 * j + 2] * inv) | (uint32_t(f32_to_bf16(o[qb][b][4 * j + 3] * inv)) << 16);
+                pk.x = f32_to_bf16(y[0]) | (uint32_t(f32_to_bf16(y[1])) << 16);
+                pk.y = f32_to_bf16(y[2]) | (uint32_t(f32_to_bf16(y[3])) << 16);
                 *reinterpret_cast<uint2*>(orow + c0) = pk;
             }
     }
@@ -518,7 +538,8 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
 // grid (n_req, n_q), 128 threads: merge the request's chunk partials in order.
 template <int G>
 __global__ void __launch_bounds__(128)
-attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_t* out, int64_t ldo) {
+attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_t* out, int64_t ldo,
+                    const bf16_t* gate, int64_t ldg) {
     constexpr int HD = 128;
     const int r = blockIdx.x, h = blockIdx.y, ch = threadIdx.x;
     const int g = h / G, col = h % G;
@@ -532,21 +553,24 @@ attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_
         L = fmaf(rec[1], f, L);
         O = fmaf(rec[2 + ch], f, O);
     }
-    out[(int64_t)r * ldo + (int64_t)h * HD + ch] = f32_to_bf16(O / L);
+    float y = O / L;
+    if (gate) y *= sigmoid_f(bf16_to_f32(gate[(int64_t)r * ldg + (int64_t)h * HD + ch]));
+    out[(int64_t)r * ldo + (int64_t)h * HD + ch] = f32_to_bf16(y);
 }
 
 template <typename T, int HD>
 bool launch_hd(int G, int ntok, const void* q, int64_t ldq, void* out, int64_t ldo,
                const int32_t* tok_slot, const int32_t* tok_pos, const int32_t* page_table,
                int max_pages, const void* kpool, const void* vpool, int n_kv, float qscale,
-               hipStream_t st) {
+               const void* gate, hipStream_t st) {
     dim3 grid(ntok, n_kv);
 #define OUTLETS_ATTN_G(GG)                                                                     \
     case GG:                                                                                   \
         hipLaunchKernelGGL((attn_paged_kernel<T, HD, GG>), grid, dim3(256), 0, st,             \
                            static_cast<const T*>(q), ldq, static_cast<T*>(out), ldo, tok_slot,  \
                            tok_pos, page_table, max_pages, static_cast<const T*>(kpool),       \
-                           static_cast<const T*>(vpool), n_kv, qscale);                        \
+                           static_cast<const T*>(vpool), n_kv, qscale,                         \
+                           static_cast<const T*>(gate));                                       \
         return true;
     switch (G) {
         OUTLETS_ATTN_G(1)
@@ -570,7 +594,7 @@ bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd) {
 void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64_t ldq, void* out,
                          int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
                          const int32_t* page_table, int max_pages, const void* kpool,
-                         const void* vpool, int n_q, int n_kv, hipStream_t st) {
+                         const void* vpool, int n_q, int n_kv, const void* gate, hipStream_t st) {
     if (n_work <= 0) return;
     const int G = n_q / n_kv;
     const float qscale = 1.4426950408889634f / sqrtf(128.0f);
@@ -581,7 +605,7 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
                            static_cast<const bf16_t*>(qkv), ldq, static_cast<bf16_t*>(out), ldo, \
                            work, req_off, req_slot, page_table, max_pages,                      \
                            static_cast<const bf16_t*>(kpool), static_cast<const bf16_t*>(vpool), \
-                           n_kv, qscale);                                                       \
+                           n_kv, qscale, static_cast<const bf16_t*>(gate));                     \
         break;
     switch (G) {
         OUTLETS_PF_G(1)
@@ -598,7 +622,7 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
-                        hipStream_t st) {
+                        const void* gate, hipStream_t st) {
     if (n_req <= 0 || n_work <= 0) return;
     const int G = n_q / n_kv;
     const float qscale = 1.4426950408889634f / sqrtf(128.0f);
@@ -609,7 +633,8 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
                            page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
                            static_cast<const bf16_t*>(vpool), n_kv, qscale, part);                 \
         hipLaunchKernelGGL((attn_decode_combine<GG>), dim3(n_req, n_q), dim3(128), 0, st,          \
-                           cu_chunks, part, n_kv, static_cast<bf16_t*>(out), ldo);                 \
+                           cu_chunks, part, n_kv, static_cast<bf16_t*>(out), ldo,                  \
+                           static_cast<const bf16_t*>(gate), ldq);                                 \
         break;
     switch (G) {
         OUTLETS_DEC_G(1)
@@ -629,16 +654,17 @@ bool attn_supported(int n_q, int n_kv, int hd) {
 void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* out,
                        int64_t ldo, const int32_t* tok_slot, const int32_t* tok_pos,
                        const int32_t* page_table, int max_pages, const void* kpool,
-                       const void* vpool, int n_q, int n_kv, int hd, hipStream_t st) {
+                       const void* vpool, int n_q, int n_kv, int hd, const void* gate,
+                       hipStream_t st) {
     if (ntok <= 0) return;
     const int G = n_q / n_kv;
     const float qscale = 1.4426950408889634f / sqrtf(static_cast<float>(hd));
     if (act_fmt == FMT_F32) {
-        if (hd == 64) launch_hd<float, 64>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, st);
-        else launch_hd<float, 128>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, st);
+        if (hd == 64) launch_hd<float, 64>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, gate, st);
+        else launch_hd<float, 128>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, gate, st);
     } else {
-        if (hd == 64) launch_hd<bf16_t, 64>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, st);
-        else launch_hd<bf16_t, 128>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, st);
+        if (hd == 64) launch_hd<bf16_t, 64>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, gate, st);
+        else launch_hd<bf16_t, 128>(G, ntok, q, ldq, out, ldo, tok_slot, tok_pos, page_table, max_pages, kpool, vpool, n_kv, qscale, gate, st);
     }
 }
 

@@ -57,7 +57,7 @@ __device__ __forceinline__ void b_row(const GemmB& B, int n, int& s, int& r) {
         s = blk & 1;
         r = (blk >> 1) * 32 + (n & 31);
     } else {
-        s = (n >= B.nend[0]) + (n >= B.nend[1]);
+        s = (n >= B.nend[0]) + (n >= B.nend[1]) + (n >= B.nend[2]);
         r = n - (s == 0 ? 0 : B.nend[s - 1]);
     }
 }
@@ -610,12 +610,12 @@ int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA
     if ((K / BK) < splits) { *why = "gemm: more K splits than K tiles"; return OUTLETS_ERR_UNSUPPORTED; }
     if (a.ld % 8 || b.ld % (w_fmt == FMT_E4M3 ? 16 : 8)) { *why = "gemm: row strides must keep 16-byte alignment"; return OUTLETS_ERR_UNSUPPORTED; }
     if (a.ld > (1 << 22) || b.ld > (1 << 22)) { *why = "gemm: row strides above 4M elements (tile offsets are 32-bit)"; return OUTLETS_ERR_UNSUPPORTED; }
-    for (int s = 0; s < 3; ++s) {
+    for (int s = 0; s < 3; ++s)
         if (a.p[s] && (reinterpret_cast<uintptr_t>(a.p[s]) & 15)) { *why = "gemm: A must be 16-byte aligned"; return OUTLETS_ERR_UNSUPPORTED; }
+    for (int s = 0; s < 4; ++s)
         if (b.p[s] && (reinterpret_cast<uintptr_t>(b.p[s]) & 15)) { *why = "gemm: B must be 16-byte aligned"; return OUTLETS_ERR_UNSUPPORTED; }
-    }
     if (!b.paired)
-        for (int s = 0; s < 2; ++s)
+        for (int s = 0; s < 3; ++s)
             if (b.nend[s] % 256) { *why = "gemm: B row blocks must be multiples of 256"; return OUTLETS_ERR_UNSUPPORTED; }
     if (epi == EPI_SWIGLU && !b.paired) { *why = "gemm: swiglu needs paired gate/up rows"; return OUTLETS_ERR_UNSUPPORTED; }
     return OUTLETS_OK;

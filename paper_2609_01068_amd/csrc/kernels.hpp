@@ -24,9 +24,9 @@ struct GemmA {
 };
 
 struct GemmB {
-    const void* p[3];
-    const uint16_t* scale[3];
-    int32_t nend[3];
+    const void* p[4];            // up to 4 row segments (e.g. Wq | Wk | Wv | W_gate)
+    const uint16_t* scale[4];
+    int32_t nend[4];             // cumulative row ends; unused entries = N
     int32_t paired;
     int64_t ld;
 };
@@ -90,12 +90,16 @@ bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd);
 // Queries per prefill attention work item (a multiple of 32).
 int attn_prefill_query_tile(int n_q, int n_kv);
 
+// Attention kernels: `gate` (nullable) points at the Gated Attention gate
+// values of token/request row 0, laid out like q (row stride ldq, query head h
+// at h * hd); each output element is multiplied by sigmoid of its gate value.
+//
 // Causal prefill attention on MFMA (bf16, hd 128).  work[2 * i], work[2 * i + 1]
-// = (request, 32-query tile) of workgroup row i; req_off = token offsets.
+// = (request, query tile) of workgroup row i; req_off = token offsets.
 void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64_t ldq, void* out,
                          int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
                          const int32_t* page_table, int max_pages, const void* kpool,
-                         const void* vpool, int n_q, int n_kv, hipStream_t st);
+                         const void* vpool, int n_q, int n_kv, const void* gate, hipStream_t st);
 
 // Decode attention (bf16, hd 128, one query per request, split over chunks of
 // attn_decode_chunk_pages() pages): work[2 i], work[2 i + 1] = (request, chunk);
@@ -106,13 +110,14 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
-                        hipStream_t st);
+                        const void* gate, hipStream_t st);
 
 // Attention of each token's queries over its slot's cached keys 0..pos.
 void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* out,
                        int64_t ldo, const int32_t* tok_slot, const int32_t* tok_pos,
                        const int32_t* page_table, int max_pages, const void* kpool,
-                       const void* vpool, int n_q, int n_kv, int hd, hipStream_t st);
+                       const void* vpool, int n_q, int n_kv, int hd, const void* gate,
+                       hipStream_t st);
 
 // Prefill pooling: pool_sum[slot] = sum of the request's h rows; pooled[i] =
 // [sum / n ; h[last]] (fp32; with pooled_bf16 != null also a bf16 hi/lo

@@ -17,6 +17,7 @@ from . import binding as B
 _FMT = {"f32": B.OUTLETS_FMT_F32, "bf16": B.OUTLETS_FMT_BF16, "e4m3": B.OUTLETS_FMT_E4M3}
 BIG_LINEARS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
 SMALL = ("gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2")
+GATE_NAME = "w_attn_gate"    # optional Gated Attention output-gate projection
 
 
 def to_device(arr, device="cuda") -> torch.Tensor:
@@ -67,6 +68,16 @@ class OutletsPredictor:
         for name in SMALL:
             self.tensors[name] = to_device(weights[name], self.device)
             setattr(w, name, _ptr(self.tensors[name]))
+        if weights.get(GATE_NAME) is not None:      # Gated Attention output gate
+            entry = weights[GATE_NAME]
+            if weight_fmt == "e4m3":
+                codes, scale = entry
+                self.tensors[GATE_NAME] = to_device(codes, self.device)
+                self.tensors["s_attn_gate"] = to_device(scale, self.device)
+                w.s_attn_gate = _ptr(self.tensors["s_attn_gate"])
+            else:
+                self.tensors[GATE_NAME] = to_device(entry, self.device)
+            w.w_attn_gate = _ptr(self.tensors[GATE_NAME])
         self._w = w
         cfg = B.outlets_config()
         cfg.d_model, cfg.n_q_heads, cfg.n_kv_heads = shape.d, shape.n_q, shape.n_kv

@@ -33,7 +33,7 @@ import numpy as np
 __all__ = [
     "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
     "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
-    "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS",
+    "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS", "GATE_NAME",
 ]
 
 # Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
@@ -42,6 +42,9 @@ BIG_LINEARS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
 WEIGHT_NAMES = BIG_LINEARS + (
     "gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1",
     "head_w2", "head_b2")
+# The attention output gate of Gated Attention (drawn only for workloads with
+# ``attn_gate``; its stream follows the others so they do not change).
+GATE_NAME = "w_attn_gate"
 
 
 @dataclasses.dataclass(frozen=True)
@@ -66,6 +69,7 @@ class DraftShape:
             "w_gate": (self.ffn, d),
             "w_up": (self.ffn, d),
             "w_down": (d, self.ffn),
+            "w_attn_gate": (self.n_q * hd, d),
             "gamma_attn": (d,),
             "gamma_mlp": (d,),
             "gamma_final": (d,),
@@ -88,6 +92,7 @@ class Workload:
     input_scales: Tuple[float, float, float]
     steps: int = 0             # decode steps (re-prediction) after the prefill
     page_size: int = 16
+    attn_gate: bool = False    # Gated Attention output gate in the draft layer
 
     @property
     def max_len(self) -> int:
@@ -169,7 +174,10 @@ def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
     shapes = wl.shape.weight_shapes()
     out: Dict[str, object] = {}
     fmt: Dict[str, str] = {}
-    for stream, name in enumerate(WEIGHT_NAMES):
+    names = list(enumerate(WEIGHT_NAMES))
+    if wl.attn_gate:
+        names.append((len(WEIGHT_NAMES), GATE_NAME))
+    for stream, name in names:
         rng = _rng(seed, wl.cfg_id, stream)
         shp = shapes[name]
         x = rng.standard_normal(shp, dtype=np.float32)
@@ -179,7 +187,7 @@ def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
             x = np.float32(0.02) * x
         if wl.weight_fmt == "f32":
             out[name], fmt[name] = x, "f32"
-        elif wl.weight_fmt == "e4m3" and name in BIG_LINEARS:
+        elif wl.weight_fmt == "e4m3" and (name in BIG_LINEARS or name == GATE_NAME):
             out[name], fmt[name] = encode_e4m3(x), "e4m3"
         else:
             out[name], fmt[name] = to_bf16_bits(x), "bf16"

@@ -127,11 +127,14 @@ def test_bf16_head_dim_64_shape():
     _run_prefill_case(case, keep=True, steps=1)
 
 
-def test_config1_full_shape_sampled_requests():
-    """8B shape, the 32-request lognormal batch; the oracle recomputes a sample."""
-    case = make_case(1)
+@pytest.mark.parametrize("gated", [False, True], ids=["plain", "gated"])
+def test_config1_full_shape_sampled_requests(gated):
+    """8B shape, the 32-request lognormal batch (also with the Gated Attention
+    output gate); the oracle recomputes a sample."""
+    case = make_case(1, attn_gate=gated)
     lens = case.lens
-    say(f"case: config-1 8B bf16, B={len(lens)}, T={int(lens.sum())}, sampled oracle")
+    say(f"case: config-1 8B bf16{' gated attention' if gated else ''}, B={len(lens)}, "
+        f"T={int(lens.sum())}, sampled oracle")
     pred = make_predictor(case)
     H = device_states(case)
     z, hd = pred.prefill(list(range(len(lens))), lens, *H, want_hdraft=True)
@@ -259,7 +262,7 @@ def test_error_paths_leave_state_unchanged():
 
 
 def test_decode_steps_over_long_caches_merge_chunks():
-    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (several 512-key chunks), 3 steps")
+    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (1024-key chunks), 3 steps")
     case = make_case(1, lens=[1100, 600, 40], shape=reduced_shape(), n_req=3)
     _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
 
@@ -268,3 +271,29 @@ def test_decode_steps_8b_shape():
     say("case: 8B bf16 shape, caches of 600/40 tokens, 2 steps")
     case = make_case(1, lens=[600, 40], n_req=2)
     _run_prefill_case(case, keep=False, steps=2, check_intermediates=False)
+
+
+# ------------------------------------------------------------- Gated Attention
+
+def test_gated_attention_tiny_fp32_intermediates_and_steps():
+    say("case: Gated Attention, tiny fp32 shape, 4 requests U[16,64], 8 steps")
+    _run_prefill_case(make_case(0, attn_gate=True), keep=True, steps=8)
+
+
+def test_gated_attention_bf16_reduced_shape_and_steps():
+    say("case: Gated Attention, bf16 d=512 8q/2kv hd128, lens [1,17,100,300,33], 3 steps")
+    case = make_case(1, lens=[1, 17, 100, 300, 33], shape=reduced_shape(), n_req=5, attn_gate=True)
+    _run_prefill_case(case, keep=True, steps=3)
+
+
+def test_gated_attention_e4m3_reduced_shape_and_steps():
+    say("case: Gated Attention, e4m3 weights d=512 16q/2kv hd128, lens [5,64,257,16], 2 steps")
+    case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=16, n_kv=2), n_req=4,
+                     attn_gate=True)
+    _run_prefill_case(case, keep=True, steps=2)
+
+
+def test_gated_attention_decode_over_multi_chunk_caches():
+    say("case: Gated Attention, bf16 d=512 8q/2kv hd128, caches of 2100/600/40 tokens, 3 steps")
+    case = make_case(1, lens=[2100, 600, 40], shape=reduced_shape(), n_req=3, attn_gate=True)
+    _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle.model as oracle_model
 from oracle import (OracleModel, OracleShape, causal_gqa_attention, decode_bf16,
                     decode_e4m3, fuse, length_head, rms_norm, rope, silu)
 
@@ -316,6 +317,55 @@ def test_packing_and_permutation():
         assert np.array_equal(hdp[offp[k]:offp[k + 1]], hd[off[i]:off[i + 1]])
 
 
+# ------------------------------------------------------------- gated attention
+
+def _gated_model(seed=11, zero_gate=False):
+    W = rand_weights(SMALL, seed=seed)
+    r = np.random.default_rng(seed + 1)
+    W["w_attn_gate"] = (np.zeros((SMALL.n_q * SMALL.head_dim, SMALL.d)) if zero_gate
+                        else r.standard_normal((SMALL.n_q * SMALL.head_dim, SMALL.d)) * 0.3)
+    return W
+
+
+def test_zero_gate_weights_halve_the_attention_output():
+    # sigmoid(0) = 1/2 exactly: the gated output is half the plain one
+    hl, hm, hh = rand_states(9, SMALL.d, 3)
+    W = _gated_model(zero_gate=True)
+    plain = {k: v for k, v in W.items() if k != "w_attn_gate"}
+    cg, cp = {}, {}
+    OracleModel(SMALL, W).prefill_one(hl, hm, hh, capture=cg)
+    OracleModel(SMALL, plain).prefill_one(hl, hm, hh, capture=cp)
+    assert np.array_equal(cg["attn"], 0.5 * cp["attn"])
+
+
+def _check_gated_layer():
+    # torch fp64 SDPA on the oracle's roped q/k/v, times torch.sigmoid of the
+    # gate projection of the normed input, must equal the oracle's output
+    n = 13
+    hl, hm, hh = rand_states(n, SMALL.d, 4)
+    W = _gated_model()
+    cap = {}
+    OracleModel(SMALL, W).prefill_one(hl, hm, hh, capture=cap)
+    q = cap["q"].reshape(n, SMALL.n_q, SMALL.head_dim)
+    o = _sdpa_ref(q, cap["k"], cap["v"], True).reshape(n, -1)
+    gate = torch.sigmoid(torch.from_numpy(cap["norm_attn"]) @ torch.from_numpy(W["w_attn_gate"]).T).numpy()
+    assert np.allclose(cap["attn"], o * gate, rtol=1e-12, atol=1e-12)
+
+
+def test_gated_attention_matches_torch_sdpa_times_sigmoid_gate():
+    _check_gated_layer()
+
+
+def test_gate_is_absent_without_gate_weights():
+    hl, hm, hh = rand_states(6, SMALL.d, 5)
+    W = rand_weights(SMALL, seed=12)
+    cap = {}
+    OracleModel(SMALL, W).prefill_one(hl, hm, hh, capture=cap)
+    q = cap["q"].reshape(6, SMALL.n_q, SMALL.head_dim)
+    assert np.allclose(cap["attn"], _sdpa_ref(q, cap["k"], cap["v"], True).reshape(6, -1),
+                       rtol=1e-12, atol=1e-12)
+
+
 # ------------------------------------------------------------- planted mistakes
 
 def _fails(fn, *args):
@@ -372,3 +422,17 @@ def test_planted_pool_order_error_is_caught():
             pooled = np.concatenate([hd[n - 1], hd.sum(axis=0) / n])[None, :]
             return float(self._head(pooled)[0]), hd, st
     assert _fails(_check_brute, SwappedPool, 5)
+
+
+@pytest.mark.parametrize("mistake", ["no_sigmoid", "pre_norm_input", "one_minus"])
+def test_planted_gate_mistakes_are_caught(monkeypatch, mistake):
+    real = oracle_model.attention_output_gate
+
+    def wrong(o, a, w):
+        if mistake == "no_sigmoid":
+            return o * (a @ w.T)
+        if mistake == "pre_norm_input":      # gate from a rescaled input (norm skipped)
+            return real(o, a * 1.7, w)
+        return o * (1.0 - oracle_model.sigmoid(a @ w.T))
+    monkeypatch.setattr(oracle_model, "attention_output_gate", wrong)
+    assert _fails(_check_gated_layer)
