@@ -251,6 +251,64 @@ def bench_prefill(a, cfg_id):
     return _emit(out)
 
 
+def bench_probe(a):
+    """The MLP-probe baseline on the config-1 batch: probe prefill over the
+    mid-depth target state of 32 requests + one probe step + release."""
+    import torch
+    from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
+    from synth import device_states, make_lengths, make_probe_weights, make_weights, workload
+
+    wl = workload(1)
+    print(f"[bench] generating {wl.name} probe weights and inputs", file=sys.stderr, flush=True)
+    W = make_weights(wl, a.seed)
+    PW = make_probe_weights(wl, a.seed)
+    W.update({k: v for k, v in PW.items() if k != "_fmt"})
+    lens = make_lengths(wl, a.seed)
+    T, B = int(lens.sum()), len(lens)
+    h = device_states(wl, T, a.seed, 300, 0)[1]
+    hs = device_states(wl, B, a.seed, 400, 1)[1]
+    pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B, max_seq_len=16,
+                            num_pages=1, max_batch_tokens=T, max_batch_requests=B)
+    del W
+    slots = list(range(B))
+    z = torch.empty(B, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pred.probe_prefill(slots, lens, h, z_out=z, stream=stream)
+        pred.probe_step(slots, hs, z_out=z, stream=stream)
+        pred.probe_release(slots)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(a.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = ev0.elapsed_time(ev1) / a.steps
+    ms_per_step = max(ev_ms, wall * 1e3 / a.steps)
+    in_bytes = (T + B) * wl.shape.d * 2 + 2 * wl.shape.head_hidden * 2 * wl.shape.d * 2
+    achieved = in_bytes / (ev_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": B / (ms_per_step / 1e3), "unit": "requests/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; lognormal prompt lengths; N(0,1) x 4 mid-depth target states drawn on device)",
+        "config": {"workload": "MLP-probe baseline on the 8B config-1 batch: 32 requests, probe prefill on the "
+                               "mid-depth state + one probe step per request", "requests": B, "prompt_tokens": T,
+                   "d": wl.shape.d, "head_hidden": wl.shape.head_hidden},
+        "roofline": {"kernel": "probe call (pooling + head), whole step", "bound": "hbm", "achieved": achieved,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "bytes_per_step": in_bytes, "avg_ms": ev_ms},
+    }
+    pred.close()
+    return _emit(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -260,11 +318,12 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--workload", default="prefill-8b",
-                    choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3"],
+                    choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3", "probe-8b"],
                     help="prefill-8b (default): 32-request 8B prefill + one step; decode-8b: 512 "
                          "in-flight requests with 256..8192 cached tokens, timed decode steps; "
                          "prefill-8b-large: 256 requests (~466k tokens) in one call; "
-                         "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests")
+                         "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests; probe-8b: the "
+                         "MLP-probe baseline on the config-1 batch")
     ap.add_argument("--attn-gate", action="store_true",
                     help="draft layer with the Gated Attention output gate (Section 4.1)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -294,6 +353,8 @@ def main(argv=None):
 
     if a.workload == "decode-8b":
         return bench_decode(a)
+    if a.workload == "probe-8b":
+        return bench_probe(a)
     if a.workload != "prefill-8b":
         return bench_prefill(a, {"prefill-8b-large": 2, "prefill-70b-e4m3": 4}[a.workload])
 

@@ -128,6 +128,10 @@ typedef struct outlets_config {
  *     sigmoid((a W_attn_gate^T)[h*hd + c]), a the normed layer input that
  *     also feeds Q/K/V, before W_o.  Stored like the other big linears
  *     (weight_fmt, with s_attn_gate row scales for E4M3).
+ *   probe_w1 [H1, 2d], probe_b1 [H1], probe_w2 [H1], probe_b2 [1]
+ *     (optional, all or none; small-weight format like head_*): the MLP-probe
+ *     baseline (Section 5.1 baselines: an MLP regressor on the frozen target
+ *     model's hidden states), see outlets_probe_prefill.
  * Element format: weight_fmt for the big linears; F32 for the rest when
  * weight_fmt is F32, BF16 otherwise.
  */
@@ -148,6 +152,10 @@ typedef struct outlets_weights {
     const void* head_w2;
     const void* head_b2;
     const void* w_attn_gate;  const void* s_attn_gate;
+    const void* probe_w1;
+    const void* probe_b1;
+    const void* probe_w2;
+    const void* probe_b2;
 } outlets_weights;
 
 typedef struct outlets_ctx outlets_ctx;
@@ -212,6 +220,32 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
 /* End requests: frees their pages and state.  Inactive slots are a no-op;
  * an out-of-range or repeated slot fails with no change. */
 int outlets_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);
+
+/*
+ * MLP-probe baseline (the comparison predictor of Section 5.1: an MLP on
+ * the target model's hidden states, no draft layer).  The probe reads one
+ * target-state tensor `h` (e.g. the mid-depth state) and runs the length
+ * head's pooling and MLP on it with the probe weights:
+ *   z_i = probe_w2 . relu(probe_w1 [mean of h over the tokens so far ;
+ *         h of the newest token] + probe_b1) + probe_b2.
+ * Probe slots are independent of the draft path's slots (same id range).
+ * Requires probe weights at create (else OUTLETS_ERR_UNSUPPORTED).
+ *
+ * outlets_probe_prefill: static probe prediction for n_req new requests;
+ *   h (device, act_fmt) packed like outlets_predict_prefill's states, row r at
+ *   element r * row_stride; z_out [n_req] device fp32.  Errors (state
+ *   unchanged): bad n_req / pointers / slot ids / repeats (INVALID_ARG),
+ *   an active probe slot (SLOT_BUSY), len < 1 or sum(lens) >
+ *   max_batch_tokens (INVALID_ARG).
+ * outlets_probe_step: one new token's state per active probe slot (row i of
+ *   h); updates the slot's running sum.  Inactive slot: SLOT_EMPTY.
+ * outlets_probe_release: ends probe slots (inactive ones are a no-op).
+ */
+int outlets_probe_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const int32_t* lens,
+                          const void* h, int64_t row_stride, float* z_out, void* stream);
+int outlets_probe_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h,
+                       int64_t row_stride, float* z_out, void* stream);
+int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);
 
 /* ------------------------------------------------------------ inspection */
 enum {

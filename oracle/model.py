@@ -258,6 +258,47 @@ class OracleModel:
         return np.array(zs), (np.stack(hs) if hs else np.zeros((0, self.s.d)))
 
 
+# ------------------------------------------------------------------ MLP probe
+
+PROBE_KEYS = ("probe_w1", "probe_b1", "probe_w2", "probe_b2")
+
+
+@dataclasses.dataclass
+class ProbeState:
+    pool_sum: np.ndarray
+    count: int
+
+
+class OracleProbe:
+    """The MLP-probe baseline of Section 5.1 (an MLP regressor on the frozen
+    target model's hidden states, no draft layer).  Reading: the probe sees
+    one target-state tensor and uses the length head's input and form,
+    [mean over the tokens so far ; newest token] -> Linear + ReLU -> Linear."""
+
+    def __init__(self, weights: Dict[str, np.ndarray]):
+        self.w = weights
+
+    def _z(self, pooled: np.ndarray) -> float:
+        w = self.w
+        return float(length_head(pooled[None, :], w["probe_w1"], w["probe_b1"], w["probe_w2"],
+                                 w["probe_b2"])[0])
+
+    def prefill_one(self, h: np.ndarray) -> Tuple[float, ProbeState]:
+        n = h.shape[0]
+        s = h.sum(axis=0)
+        return self._z(np.concatenate([s / n, h[n - 1]])), ProbeState(s, n)
+
+    def step_one(self, st: ProbeState, h_row: np.ndarray) -> float:
+        st.pool_sum = st.pool_sum + h_row
+        st.count += 1
+        return self._z(np.concatenate([st.pool_sum / st.count, h_row]))
+
+
+def probe_from_stored(stored: Dict[str, object]) -> OracleProbe:
+    fmt = stored["_fmt"]
+    return OracleProbe({k: decode_weight(stored[k], fmt[k]) for k in PROBE_KEYS})
+
+
 def oracle_from_workload(wl, stored_weights) -> OracleModel:
     """Build the oracle for a workload description (duck-typed: ``wl.shape``)."""
     sh = wl.shape

@@ -64,6 +64,7 @@ WEIGHT_FIELDS = [
     "w_proj", "s_proj", "w_q", "s_q", "w_k", "s_k", "w_v", "s_v", "w_o", "s_o",
     "w_gate", "s_gate", "w_up", "s_up", "w_down", "s_down", "gamma_attn", "gamma_mlp",
     "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2", "w_attn_gate", "s_attn_gate",
+    "probe_w1", "probe_b1", "probe_w2", "probe_b2",
 ]
 
 
@@ -81,6 +82,9 @@ _SIGS = {
     "outlets_predict_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
     "outlets_predict_step": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
     "outlets_release": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_probe_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, C.c_int64, _P, _P]),
+    "outlets_probe_step": (C.c_int, [_P, C.c_int32, _I32P, _P, C.c_int64, _P, _P]),
+    "outlets_probe_release": (C.c_int, [_P, C.c_int32, _I32P]),
     "outlets_get_meta": (C.c_int, [_P, C.c_int32, _I32P, C.c_int64, C.POINTER(C.c_int64)]),
     "outlets_get_buffer": (C.c_int, [_P, C.c_int32, _P, C.c_int64, C.POINTER(C.c_int64), _P]),
     "outlets_last_error": (C.c_char_p, []),
@@ -158,6 +162,20 @@ def outlets_predict_step(ctx, slots, h_low: int, h_mid: int, h_high: int, row_st
 
 def outlets_release(ctx, slots) -> int:
     return lib().outlets_release(ctx, len(slots), i32_array(slots))
+
+
+def outlets_probe_prefill(ctx, slots, lens, h: int, row_stride: int, z_out: int,
+                          stream: Optional[int]) -> int:
+    return lib().outlets_probe_prefill(ctx, len(slots), i32_array(slots), i32_array(lens), h, row_stride,
+                                       z_out, stream)
+
+
+def outlets_probe_step(ctx, slots, h: int, row_stride: int, z_out: int, stream: Optional[int]) -> int:
+    return lib().outlets_probe_step(ctx, len(slots), i32_array(slots), h, row_stride, z_out, stream)
+
+
+def outlets_probe_release(ctx, slots) -> int:
+    return lib().outlets_probe_release(ctx, len(slots), i32_array(slots))
 
 
 def outlets_get_meta(ctx, what: int, cap: int):

@@ -51,6 +51,10 @@ struct outlets_ctx {
     int act_fmt = 0, w_fmt = 0, small_fmt = 0;  // small_fmt: gains and head
     int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
     bool gated = false;          // Gated Attention: q|k|v|g rows, output gate in attention
+    bool probe = false;          // MLP probe weights present
+    std::vector<int32_t> probe_count;   // per slot: tokens pooled by the probe (0 = inactive)
+    float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
+    int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
     std::unique_ptr<Pager> pager;
     int max_pages = 0;
 
@@ -340,10 +344,10 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
     uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
     { KTimer t(c, OUTLETS_K_POOL, st);
       if (prefill)
-          launch_pool_prefill(n, c->n_tiles, d, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
+          launch_pool_prefill(n, c->n_tiles, d, FMT_F32, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
                               c->pool_part, c->pool_sum, c->pooled, pb, st);
       else
-          launch_pool_step(n, d, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
+          launch_pool_step(n, d, FMT_F32, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
     // bf16 heads read the hi/lo split of the pooled vector: 2n rows
     const int head_rows = (wf == FMT_F32) ? n : 2 * n;
@@ -439,6 +443,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
                          w.head_w2, w.head_b2};
     for (const void* p : req)
         if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "a weight pointer is null");
+    if (w.probe_w1 && (!w.probe_b1 || !w.probe_w2 || !w.probe_b2))
+        return fail(OUTLETS_ERR_INVALID_ARG, "probe weights need w1, b1, w2 and b2");
     if (cfg->weight_fmt == OUTLETS_FMT_E4M3) {
         const void* sc[] = {w.s_proj, w.s_q, w.s_k, w.s_v, w.s_o, w.s_gate, w.s_up, w.s_down};
         for (const void* p : sc)
@@ -465,6 +471,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     c->qdim = static_cast<int64_t>(cfg->n_q_heads) * cfg->head_dim;
     c->kvdim = static_cast<int64_t>(cfg->n_kv_heads) * cfg->head_dim;
     c->gated = w.w_attn_gate != nullptr;
+    c->probe = w.probe_w1 != nullptr;
     c->qkv_dim = c->qdim + 2 * c->kvdim + (c->gated ? c->qdim : 0);
     c->F = cfg->ffn_dim;
     c->H1 = cfg->head_hidden;
@@ -532,6 +539,11 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         if (need) ALLOC(c->splitk_ws, need);
     }
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
+    if (c->probe) {
+        ALLOC(c->probe_sum, sizeof(float) * cfg->max_slots * c->d);
+        ALLOC(c->probe_meta, sizeof(int32_t) * c->meta_cap);
+        c->probe_count.assign(cfg->max_slots, 0);
+    }
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
         HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->meta_cap, 0),
@@ -556,6 +568,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     }
     HIP_TRY(hipMemset(c->page_table, 0xFF, sizeof(int32_t) * c->pager->table().size()), "hipMemset");
     HIP_TRY(hipMemset(c->pool_sum, 0, sizeof(float) * cfg->max_slots * c->d), "hipMemset");
+    if (c->probe) HIP_TRY(hipMemset(c->probe_sum, 0, sizeof(float) * cfg->max_slots * c->d), "hipMemset");
     // attention kernels may read (and give zero weight to) rows of a page no
     // token has written yet: start from zeros so those rows are finite
     HIP_TRY(hipMemset(c->kpool, 0, pool_elems * ab), "hipMemset");
@@ -662,6 +675,134 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     if (rc) return rc;   // device work may be partly queued; the slot lengths advanced
     ctx->last_n = n_req;
     ctx->last_T = n_req;
+    return OUTLETS_OK;
+}
+
+// ---------------------------------------------------------------- MLP probe
+// The probe baseline: the length head's pooling and MLP applied directly to a
+// target-model hidden state (no draft layer), with its own weights and
+// per-slot running sums.
+
+// Stage int32 metadata through the pinned double buffer into probe_meta.
+int upload_probe_meta(outlets_ctx* c, const std::vector<int32_t>& v, hipStream_t st) {
+    if (static_cast<int64_t>(v.size()) > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
+    const int s = c->stage;
+    if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
+    std::memcpy(c->h_stage[s], v.data(), sizeof(int32_t) * v.size());
+    HIP_TRY(hipMemcpyAsync(c->probe_meta, c->h_stage[s], sizeof(int32_t) * v.size(), hipMemcpyHostToDevice, st),
+            "hipMemcpyAsync");
+    HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
+    c->ev_used[s] = true;
+    c->stage ^= 1;
+    return OUTLETS_OK;
+}
+
+// z_out[i] = probe MLP of pooled row i (pooled / pooled_bf16 already filled).
+int run_probe_head(outlets_ctx* c, int n, float* z_out, hipStream_t st) {
+    const int af = c->act_fmt, wf = c->w_fmt;
+    const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
+    const int64_t d = c->d;
+    const GemmA a = (wf == FMT_F32) ? gemm_a(c->pooled, 2 * d, 2 * d) : gemm_a(c->pooled_bf16, 2 * d, 2 * d);
+    const GemmB b = gemm_b1(c->w.probe_w1, nullptr, c->H1, 2 * d);
+    const int rows = (wf == FMT_F32) ? n : 2 * n;
+    GemmC hc = gemm_c(c->head_part, c->H1);
+    hc.split_stride = static_cast<int64_t>(rows) * c->H1;
+    gemm_launch(af, hf, EPI_PARTIAL, rows, c->H1, 2 * d, a, b, hc, kHeadSplits, st);
+    launch_head_finish(c->small_fmt, n, c->H1, kHeadSplits, c->head_part, c->w.probe_b1, c->w.probe_w2,
+                       c->w.probe_b2, z_out, st);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return OUTLETS_OK;
+}
+
+int check_probe_call(const outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h,
+                     int64_t row_stride, const float* z_out) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (!ctx->probe) return fail(OUTLETS_ERR_UNSUPPORTED, "the context was created without probe weights");
+    if (n_req < 0 || n_req > ctx->cfg.max_batch_requests)
+        return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
+    if (n_req == 0) return OUTLETS_OK;
+    if (!slots || !h || !z_out) return fail(OUTLETS_ERR_INVALID_ARG, "null slots, state or output pointer");
+    if (row_stride < ctx->d) return fail(OUTLETS_ERR_INVALID_ARG, "row_stride < d_model");
+    std::vector<char> seen(ctx->cfg.max_slots, 0);
+    for (int i = 0; i < n_req; ++i) {
+        if (slots[i] < 0 || slots[i] >= ctx->cfg.max_slots) return fail(OUTLETS_ERR_INVALID_ARG, "slot id out of range");
+        if (seen[slots[i]]) return fail(OUTLETS_ERR_INVALID_ARG, "duplicate slot");
+        seen[slots[i]] = 1;
+    }
+    return OUTLETS_OK;
+}
+
+int outlets_probe_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const int32_t* lens,
+                          const void* h, int64_t row_stride, float* z_out, void* stream) {
+    int rc = check_probe_call(ctx, n_req, slots, h, row_stride, z_out);
+    if (rc || n_req == 0) return rc;
+    if (!lens) return fail(OUTLETS_ERR_INVALID_ARG, "null lens");
+    int64_t T = 0;
+    for (int i = 0; i < n_req; ++i) {
+        if (ctx->probe_count[slots[i]] != 0) return fail(OUTLETS_ERR_SLOT_BUSY, "probe slot already active");
+        if (lens[i] <= 0) return fail(OUTLETS_ERR_INVALID_ARG, "prompt length must be >= 1");
+        T += lens[i];
+    }
+    if (T > ctx->cfg.max_batch_tokens) return fail(OUTLETS_ERR_INVALID_ARG, "total prompt tokens exceed max_batch_tokens");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // req_off [n+1] | req_slot [n] | cu_tiles [n+1]
+    std::vector<int32_t> v(3 * n_req + 2);
+    int32_t* off = v.data();
+    int32_t* sl = off + n_req + 1;
+    int32_t* cu = sl + n_req;
+    off[0] = cu[0] = 0;
+    for (int i = 0; i < n_req; ++i) {
+        off[i + 1] = off[i] + lens[i];
+        sl[i] = slots[i];
+        cu[i + 1] = cu[i] + (lens[i] + 31) / 32;
+    }
+    if ((rc = upload_probe_meta(ctx, v, st)) != OUTLETS_OK) return rc;
+    const int32_t* d_off = ctx->probe_meta;
+    launch_pool_prefill(n_req, cu[n_req], static_cast<int>(ctx->d), ctx->act_fmt, h, row_stride, d_off,
+                        d_off + n_req + 1, d_off + 2 * n_req + 1, ctx->pool_part, ctx->probe_sum, ctx->pooled,
+                        ctx->w_fmt == FMT_F32 ? nullptr : ctx->pooled_bf16, st);
+    if ((rc = run_probe_head(ctx, n_req, z_out, st)) != OUTLETS_OK) return rc;
+    for (int i = 0; i < n_req; ++i) ctx->probe_count[slots[i]] = lens[i];
+    return OUTLETS_OK;
+}
+
+int outlets_probe_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h,
+                       int64_t row_stride, float* z_out, void* stream) {
+    int rc = check_probe_call(ctx, n_req, slots, h, row_stride, z_out);
+    if (rc || n_req == 0) return rc;
+    for (int i = 0; i < n_req; ++i)
+        if (ctx->probe_count[slots[i]] == 0) return fail(OUTLETS_ERR_SLOT_EMPTY, "probe slot not active");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // req_slot [n] | req_start [n] (tokens pooled before this one)
+    std::vector<int32_t> v(2 * n_req);
+    for (int i = 0; i < n_req; ++i) {
+        v[i] = slots[i];
+        v[n_req + i] = ctx->probe_count[slots[i]];
+    }
+    if ((rc = upload_probe_meta(ctx, v, st)) != OUTLETS_OK) return rc;
+    launch_pool_step(n_req, static_cast<int>(ctx->d), ctx->act_fmt, h, row_stride, ctx->probe_meta,
+                     ctx->probe_meta + n_req, ctx->probe_sum, ctx->pooled,
+                     ctx->w_fmt == FMT_F32 ? nullptr : ctx->pooled_bf16, st);
+    if ((rc = run_probe_head(ctx, n_req, z_out, st)) != OUTLETS_OK) return rc;
+    for (int i = 0; i < n_req; ++i) ctx->probe_count[slots[i]] += 1;
+    return OUTLETS_OK;
+}
+
+int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (!ctx->probe) return fail(OUTLETS_ERR_UNSUPPORTED, "the context was created without probe weights");
+    if (n < 0 || (n > 0 && !slots)) return fail(OUTLETS_ERR_INVALID_ARG, "bad slot list");
+    for (int i = 0; i < n; ++i)
+        if (slots[i] < 0 || slots[i] >= ctx->cfg.max_slots) return fail(OUTLETS_ERR_INVALID_ARG, "slot id out of range");
+    std::vector<char> seen(ctx->cfg.max_slots, 0);
+    for (int i = 0; i < n; ++i) {
+        if (seen[slots[i]]) return fail(OUTLETS_ERR_INVALID_ARG, "duplicate slot");
+        seen[slots[i]] = 1;
+    }
+    for (int i = 0; i < n; ++i) ctx->probe_count[slots[i]] = 0;
     return OUTLETS_OK;
 }
 

@@ -123,12 +123,12 @@ void launch_attn_paged(int act_fmt, int ntok, const void* q, int64_t ldq, void* 
 // [sum / n ; h[last]] (fp32; with pooled_bf16 != null also a bf16 hi/lo
 // split: hi in rows [0, n), lo in rows [n, 2n)).
 // cu_tiles[n_req + 1]: prefix sum of ceil(n_i / 32); part: [n_tiles, d] scratch.
-void launch_pool_prefill(int n_req, int n_tiles, int d, const float* h, int64_t ldh,
+void launch_pool_prefill(int n_req, int n_tiles, int d, int h_fmt, const void* h, int64_t ldh,
                          const int32_t* req_off, const int32_t* req_slot, const int32_t* cu_tiles,
                          float* part, float* pool_sum, float* pooled, uint16_t* pooled_bf16,
                          hipStream_t st);
 // Step pooling: pool_sum[slot] += h[i]; pooled[i] = [pool_sum / (start + 1) ; h[i]].
-void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_slot,
+void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,
                       uint16_t* pooled_bf16, hipStream_t st);
 

@@ -200,8 +200,9 @@ __device__ __forceinline__ void split_bf16(float v, uint16_t* hi_row, int64_t lo
 // + k) sums its rows in order.  Stage 2, grid (n_req, ceil(d / 256)): each
 // request sums its tiles in order.  Tiles are relative to the request start,
 // so the result does not depend on the rest of the batch.
+template <typename TH>
 __global__ void __launch_bounds__(256)
-pool_tiles_kernel(int d, int n_req, const float* h, int64_t ldh, const int32_t* req_off,
+pool_tiles_kernel(int d, int n_req, const TH* h, int64_t ldh, const int32_t* req_off,
                   const int32_t* cu_tiles, float* part) {
     const int t = blockIdx.x;
     const int c = blockIdx.y * 256 + threadIdx.x;
@@ -214,12 +215,13 @@ pool_tiles_kernel(int d, int n_req, const float* h, int64_t ldh, const int32_t* 
     const int b = req_off[lo] + (t - cu_tiles[lo]) * 32;
     const int e = min(b + 32, req_off[lo + 1]);
     float s = 0.f;
-    for (int r = b; r < e; ++r) s += h[(int64_t)r * ldh + c];
+    for (int r = b; r < e; ++r) s += load_act<TH>(h + (int64_t)r * ldh + c);
     part[(int64_t)t * d + c] = s;
 }
 
+template <typename TH>
 __global__ void __launch_bounds__(256)
-pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
+pool_prefill_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_off,
                     const int32_t* req_slot, const int32_t* cu_tiles, const float* part,
                     float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
     const int i = blockIdx.x;
@@ -230,7 +232,7 @@ pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
     for (int t = cu_tiles[i]; t < cu_tiles[i + 1]; ++t) s += part[(int64_t)t * d + c];
     pool_sum[(int64_t)req_slot[i] * d + c] = s;
     const float mean = s / static_cast<float>(e - b);
-    const float last = h[(int64_t)(e - 1) * ldh + c];
+    const float last = load_act<TH>(h + (int64_t)(e - 1) * ldh + c);
     pooled[(int64_t)i * 2 * d + c] = mean;
     pooled[(int64_t)i * 2 * d + d + c] = last;
     if (pooled_bf16) {
@@ -239,13 +241,14 @@ pool_prefill_kernel(int d, const float* h, int64_t ldh, const int32_t* req_off,
     }
 }
 
+template <typename TH>
 __global__ void __launch_bounds__(256)
-pool_step_kernel(int d, const float* h, int64_t ldh, const int32_t* req_slot,
+pool_step_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_slot,
                  const int32_t* req_start, float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
     const int i = blockIdx.x;
     const int c = blockIdx.y * 256 + threadIdx.x;
     if (c >= d) return;
-    const float x = h[(int64_t)i * ldh + c];
+    const float x = load_act<TH>(h + (int64_t)i * ldh + c);
     float* ps = pool_sum + (int64_t)req_slot[i] * d + c;
     const float s = *ps + x;
     *ps = s;
@@ -364,23 +367,36 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
                            n_q, n_kv, hd);
 }
 
-void launch_pool_prefill(int n_req, int n_tiles, int d, const float* h, int64_t ldh,
+void launch_pool_prefill(int n_req, int n_tiles, int d, int h_fmt, const void* h, int64_t ldh,
                          const int32_t* req_off, const int32_t* req_slot, const int32_t* cu_tiles,
                          float* part, float* pool_sum, float* pooled, uint16_t* pooled_bf16,
                          hipStream_t st) {
     if (n_req <= 0) return;
-    hipLaunchKernelGGL(pool_tiles_kernel, dim3(n_tiles, (d + 255) / 256), dim3(256), 0, st, d, n_req,
-                       h, ldh, req_off, cu_tiles, part);
-    hipLaunchKernelGGL(pool_prefill_kernel, dim3(n_req, (d + 255) / 256), dim3(256), 0, st, d, h,
-                       ldh, req_off, req_slot, cu_tiles, part, pool_sum, pooled, pooled_bf16);
+    const dim3 gt(n_tiles, (d + 255) / 256), gr(n_req, (d + 255) / 256);
+    if (h_fmt == FMT_F32) {
+        const float* hh = static_cast<const float*>(h);
+        hipLaunchKernelGGL(pool_tiles_kernel<float>, gt, dim3(256), 0, st, d, n_req, hh, ldh, req_off, cu_tiles, part);
+        hipLaunchKernelGGL(pool_prefill_kernel<float>, gr, dim3(256), 0, st, d, hh, ldh, req_off, req_slot,
+                           cu_tiles, part, pool_sum, pooled, pooled_bf16);
+    } else {
+        const bf16_t* hh = static_cast<const bf16_t*>(h);
+        hipLaunchKernelGGL(pool_tiles_kernel<bf16_t>, gt, dim3(256), 0, st, d, n_req, hh, ldh, req_off, cu_tiles, part);
+        hipLaunchKernelGGL(pool_prefill_kernel<bf16_t>, gr, dim3(256), 0, st, d, hh, ldh, req_off, req_slot,
+                           cu_tiles, part, pool_sum, pooled, pooled_bf16);
+    }
 }
 
-void launch_pool_step(int n_req, int d, const float* h, int64_t ldh, const int32_t* req_slot,
+void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,
                       uint16_t* pooled_bf16, hipStream_t st) {
     if (n_req <= 0) return;
-    hipLaunchKernelGGL(pool_step_kernel, dim3(n_req, (d + 255) / 256), dim3(256), 0, st, d, h, ldh,
-                       req_slot, req_start, pool_sum, pooled, pooled_bf16);
+    const dim3 g(n_req, (d + 255) / 256);
+    if (h_fmt == FMT_F32)
+        hipLaunchKernelGGL(pool_step_kernel<float>, g, dim3(256), 0, st, d, static_cast<const float*>(h), ldh,
+                           req_slot, req_start, pool_sum, pooled, pooled_bf16);
+    else
+        hipLaunchKernelGGL(pool_step_kernel<bf16_t>, g, dim3(256), 0, st, d, static_cast<const bf16_t*>(h), ldh,
+                           req_slot, req_start, pool_sum, pooled, pooled_bf16);
 }
 
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,

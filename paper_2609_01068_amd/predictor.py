@@ -18,6 +18,7 @@ _FMT = {"f32": B.OUTLETS_FMT_F32, "bf16": B.OUTLETS_FMT_BF16, "e4m3": B.OUTLETS_
 BIG_LINEARS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
 SMALL = ("gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2")
 GATE_NAME = "w_attn_gate"    # optional Gated Attention output-gate projection
+PROBE = ("probe_w1", "probe_b1", "probe_w2", "probe_b2")   # optional MLP-probe baseline
 
 
 def to_device(arr, device="cuda") -> torch.Tensor:
@@ -78,6 +79,10 @@ class OutletsPredictor:
             else:
                 self.tensors[GATE_NAME] = to_device(entry, self.device)
             w.w_attn_gate = _ptr(self.tensors[GATE_NAME])
+        if weights.get("probe_w1") is not None:          # MLP-probe baseline
+            for name in PROBE:
+                self.tensors[name] = to_device(weights[name], self.device)
+                setattr(w, name, _ptr(self.tensors[name]))
         self._w = w
         cfg = B.outlets_config()
         cfg.d_model, cfg.n_q_heads, cfg.n_kv_heads = shape.d, shape.n_q, shape.n_kv
@@ -126,6 +131,30 @@ class OutletsPredictor:
 
     def release(self, slots: Sequence[int]) -> None:
         B.check(B.outlets_release(self.ctx, list(slots)), "outlets_release")
+
+    # ------------------------------------------------------------ MLP probe
+    def probe_prefill(self, slots: Sequence[int], lens: Sequence[int], h: torch.Tensor,
+                      row_stride: Optional[int] = None, z_out: Optional[torch.Tensor] = None, stream=None):
+        n = len(slots)
+        if z_out is None:
+            z_out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
+        stride = h.stride(0) if row_stride is None else row_stride
+        B.check(B.outlets_probe_prefill(self.ctx, list(slots), list(lens), h.data_ptr(), stride,
+                                        z_out.data_ptr(), _stream_ptr(stream)), "outlets_probe_prefill")
+        return z_out[:n]
+
+    def probe_step(self, slots: Sequence[int], h: torch.Tensor, row_stride: Optional[int] = None,
+                   z_out: Optional[torch.Tensor] = None, stream=None):
+        n = len(slots)
+        if z_out is None:
+            z_out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
+        stride = h.stride(0) if row_stride is None else row_stride
+        B.check(B.outlets_probe_step(self.ctx, list(slots), h.data_ptr(), stride, z_out.data_ptr(),
+                                     _stream_ptr(stream)), "outlets_probe_step")
+        return z_out[:n]
+
+    def probe_release(self, slots: Sequence[int]) -> None:
+        B.check(B.outlets_probe_release(self.ctx, list(slots)), "outlets_probe_release")
 
     # ------------------------------------------------------------ inspection
     def profile(self, enable: bool) -> None:

@@ -34,6 +34,7 @@ __all__ = [
     "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
     "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
     "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS", "GATE_NAME",
+    "make_probe_weights",
 ]
 
 # Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
@@ -192,6 +193,26 @@ def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
         else:
             out[name], fmt[name] = to_bf16_bits(x), "bf16"
         del x
+    out["_fmt"] = fmt
+    return out
+
+
+def make_probe_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
+    """Weights of the MLP-probe baseline (same form as the length head:
+    probe_w1 [H1, 2d], probe_b1 [H1], probe_w2 [H1], probe_b2 [1]), drawn
+    N(0, 0.02^2) from streams after every other weight's, stored in the
+    small-weight format.  Returns a dict with its own ``_fmt`` entries."""
+    d, h1 = wl.shape.d, wl.shape.head_hidden
+    shapes = {"probe_w1": (h1, 2 * d), "probe_b1": (h1,), "probe_w2": (h1,), "probe_b2": (1,)}
+    out: Dict[str, object] = {}
+    fmt: Dict[str, str] = {}
+    for k, (name, shp) in enumerate(shapes.items()):
+        rng = _rng(seed, wl.cfg_id, len(WEIGHT_NAMES) + 1 + k)
+        x = np.float32(0.02) * rng.standard_normal(shp, dtype=np.float32)
+        if wl.weight_fmt == "f32":
+            out[name], fmt[name] = x, "f32"
+        else:
+            out[name], fmt[name] = to_bf16_bits(x), "bf16"
     out["_fmt"] = fmt
     return out
 

@@ -297,3 +297,71 @@ def test_gated_attention_decode_over_multi_chunk_caches():
     say("case: Gated Attention, bf16 d=512 8q/2kv hd128, caches of 2100/600/40 tokens, 3 steps")
     case = make_case(1, lens=[2100, 600, 40], shape=reduced_shape(), n_req=3, attn_gate=True)
     _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
+
+
+# ------------------------------------------------------------- MLP probe
+
+@pytest.mark.parametrize("cfg", [0, 1], ids=["tiny-fp32", "bf16-reduced"])
+def test_mlp_probe_prefill_steps_and_errors(cfg):
+    import dataclasses
+    from paper_2609_01068_amd import binding as B
+    from oracle import probe_from_stored
+    from synth import make_probe_weights
+    if cfg == 0:
+        case = make_case(0)
+    else:
+        case = make_case(1, lens=[1, 17, 100, 300, 33], shape=reduced_shape(), n_req=5)
+    lens = case.lens
+    n = len(lens)
+    say(f"case: MLP probe on the mid-depth state, cfg {cfg}, lens {list(lens)}, 3 steps")
+    PW = make_probe_weights(case.wl)
+    W = dict(case.weights)
+    W.update({k: v for k, v in PW.items() if k != "_fmt"})
+    W["_fmt"] = {**case.weights["_fmt"], **PW["_fmt"]}
+    case = dataclasses.replace(case, weights=W)
+    pred = make_predictor(case, max_slots=n + 2)
+    probe = probe_from_stored(PW)
+    H = device_states(case)
+    O = oracle_states(case)
+    slots = list(range(n))
+    off = np.concatenate([[0], np.cumsum(lens)])
+    z = tensor_to_f64(pred.probe_prefill(slots, lens, H[1]))
+    states, z_ref = [], []
+    for i in range(n):
+        zi, st = probe.prefill_one(O[1][off[i]:off[i + 1]])
+        z_ref.append(zi)
+        states.append(st)
+    ez = z_errors(z, z_ref)
+    say(f"  probe prefill z max rel err {ez.max():.3e}")
+    assert ez.max() <= TOL_Z[case.fmt]
+    for t in range(1, 4):
+        S = step_inputs(case, t)
+        zs = tensor_to_f64(pred.probe_step(slots, device_states(case, S)[1]))
+        OS = oracle_states(case, S)
+        zr = [probe.step_one(states[i], OS[1][i]) for i in range(n)]
+        assert z_errors(zs, zr).max() <= TOL_Z[case.fmt], t
+    # probe slots are independent of the draft path's slots
+    zd, _ = pred.prefill([0], [int(lens[0])], *[x[:int(lens[0])] for x in H])
+    codes = []
+    for call in (lambda: pred.probe_prefill([0], [1], H[1][:1]),
+                 lambda: pred.probe_step([n], H[1][:1]),
+                 lambda: pred.probe_prefill([n, n], [1, 1], H[1][:2])):
+        with pytest.raises(B.OutletsError) as e:
+            call()
+        codes.append(e.value.rc)
+    assert codes == [B.OUTLETS_ERR_SLOT_BUSY, B.OUTLETS_ERR_SLOT_EMPTY, B.OUTLETS_ERR_INVALID_ARG]
+    pred.probe_release(slots + [n])          # inactive slots are a no-op
+    z2 = tensor_to_f64(pred.probe_prefill([n], [int(lens[1])], H[1][off[1]:off[2]]))
+    assert abs(z2[0] - z[1]) <= 1e-5 * max(abs(z[1]), 1e-3)
+    pred.close()
+
+
+def test_mlp_probe_needs_probe_weights():
+    from paper_2609_01068_amd import binding as B
+    case = make_case(0, lens=[8])
+    pred = make_predictor(case)
+    H = device_states(case)
+    with pytest.raises(B.OutletsError) as e:
+        pred.probe_prefill([0], [8], H[1])
+    assert e.value.rc == B.OUTLETS_ERR_UNSUPPORTED
+    pred.close()

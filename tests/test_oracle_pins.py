@@ -366,6 +366,47 @@ def test_gate_is_absent_without_gate_weights():
                        rtol=1e-12, atol=1e-12)
 
 
+# ------------------------------------------------------------- MLP probe
+
+def _probe_weights(seed=21):
+    r = np.random.default_rng(seed)
+    d, h1 = SMALL.d, SMALL.head_hidden
+    return {"probe_w1": r.standard_normal((h1, 2 * d)) * 0.3, "probe_b1": r.standard_normal(h1) * 0.3,
+            "probe_w2": r.standard_normal(h1) * 0.3, "probe_b2": r.standard_normal(1) * 0.3}
+
+
+def _torch_probe(W, h):
+    t = torch.from_numpy
+    mlp = torch.nn.Sequential(torch.nn.Linear(2 * SMALL.d, SMALL.head_hidden), torch.nn.ReLU(),
+                              torch.nn.Linear(SMALL.head_hidden, 1)).double()
+    with torch.no_grad():
+        mlp[0].weight.copy_(t(W["probe_w1"])); mlp[0].bias.copy_(t(W["probe_b1"]))
+        mlp[2].weight.copy_(t(W["probe_w2"])[None, :]); mlp[2].bias.copy_(t(W["probe_b2"]))
+        x = torch.cat([t(h).mean(dim=0), t(h)[-1]])
+        return float(mlp(x)[0])
+
+
+def test_probe_matches_torch_mlp_on_mean_and_last():
+    from oracle import OracleProbe
+    W = _probe_weights()
+    h = np.random.default_rng(22).standard_normal((11, SMALL.d)) * 2.0
+    z, _ = OracleProbe(W).prefill_one(h)
+    assert abs(z - _torch_probe(W, h)) <= 1e-12 * max(1.0, abs(z))
+
+
+def test_probe_steps_equal_prefill_recompute():
+    from oracle import OracleProbe
+    W = _probe_weights()
+    h = np.random.default_rng(23).standard_normal((9, SMALL.d))
+    p = OracleProbe(W)
+    _, st = p.prefill_one(h[:4])
+    for t in range(4, 9):
+        zs = p.step_one(st, h[t])
+        zf, _ = OracleProbe(W).prefill_one(h[:t + 1])
+        assert abs(zs - zf) <= 1e-12 * max(1.0, abs(zf))
+        assert abs(zs - _torch_probe(W, h[:t + 1])) <= 1e-12 * max(1.0, abs(zs))
+
+
 # ------------------------------------------------------------- planted mistakes
 
 def _fails(fn, *args):
