@@ -326,6 +326,9 @@ def main(argv=None):
                          "MLP-probe baseline on the config-1 batch")
     ap.add_argument("--attn-gate", action="store_true",
                     help="draft layer with the Gated Attention output gate (Section 4.1)")
+    ap.add_argument("--draft-head", action="store_true",
+                    help="prefill-8b: also run the draft model head (Eq. 2, V = 128,256) after the "
+                         "prefill and after the step")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 times); used to scale "
                          "rocprof's FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -361,6 +364,9 @@ def main(argv=None):
     wl = workload(1, attn_gate=a.attn_gate)
     print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
     W = make_weights(wl, a.seed)
+    if a.draft_head:
+        from synth import make_lm_weights
+        W["w_lm"] = make_lm_weights(wl, a.seed)["w_lm"]
     lens = make_lengths(wl, a.seed)
     T, B = int(lens.sum()), len(lens)
     H = [to_device(x) for x in make_prompt_states(wl, lens, a.seed)]
@@ -372,10 +378,15 @@ def main(argv=None):
     z = torch.empty(B, dtype=torch.float32, device="cuda")
     z1 = torch.empty(B, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
+    probs = torch.empty((B, wl.shape.vocab), dtype=torch.float32, device="cuda") if a.draft_head else None
 
     def one_step():
         pred.prefill(slots, lens, *H, z_out=z, stream=stream)
+        if probs is not None:
+            pred.draft_distribution(B, p_out=probs, stream=stream)
         pred.step(slots, *S, z_out=z1, stream=stream)
+        if probs is not None:
+            pred.draft_distribution(B, p_out=probs, stream=stream)
         pred.release(slots)
 
     print(f"[bench] warmup {a.warmup} steps (T={T} tokens, B={B})", file=sys.stderr, flush=True)
@@ -431,7 +442,8 @@ def main(argv=None):
                                "prompts clipped to [32, 4096], static prediction + 1 dynamic step per request",
                    "requests": B, "prompt_tokens": T, "d": wl.shape.d, "heads": [wl.shape.n_q, wl.shape.n_kv],
                    "head_dim": wl.shape.head_dim, "ffn": wl.shape.ffn, "head_hidden": wl.shape.head_hidden,
-                   "page_size": 16, "attn_gate": wl.attn_gate},
+                   "page_size": 16, "attn_gate": wl.attn_gate,
+                   "draft_head_vocab": wl.shape.vocab if a.draft_head else 0},
         "draft_tokens_per_s": tok_s,
         "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

@@ -111,6 +111,7 @@ typedef struct outlets_config {
     int32_t max_batch_tokens;
     int32_t max_batch_requests;
     int32_t keep_intermediates;
+    int32_t vocab;        /* draft model head vocabulary V (Eq. 2); 0 = no draft head */
 } outlets_config;
 
 /*
@@ -132,6 +133,9 @@ typedef struct outlets_config {
  *     (optional, all or none; small-weight format like head_*): the MLP-probe
  *     baseline (Section 5.1 baselines: an MLP regressor on the frozen target
  *     model's hidden states), see outlets_probe_prefill.
+ *   w_lm [V, d] (required iff cfg.vocab > 0; weight_fmt, with s_lm row
+ *     scales for E4M3): the draft model head of Eq. 2, see
+ *     outlets_draft_distribution.
  * Element format: weight_fmt for the big linears; F32 for the rest when
  * weight_fmt is F32, BF16 otherwise.
  */
@@ -156,6 +160,7 @@ typedef struct outlets_weights {
     const void* probe_b1;
     const void* probe_w2;
     const void* probe_b2;
+    const void* w_lm;    const void* s_lm;
 } outlets_weights;
 
 typedef struct outlets_ctx outlets_ctx;
@@ -246,6 +251,19 @@ int outlets_probe_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
 int outlets_probe_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h,
                        int64_t row_stride, float* z_out, void* stream);
 int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);
+
+/*
+ * Draft model head (Eq. 2): for each request of the last outlets_predict_*
+ * call, P_draft(y_{t+1} | y_{1:t}) = softmax(W_lm h_t^draft) over the V
+ * vocabulary entries, h_t^draft the draft state of the request's newest
+ * token (the same state the length head reads).
+ *   n_req: must equal the last predict call's request count.
+ *   p_out (device): fp32 [n_req, V] row-major probabilities.
+ * Must be queued before the next predict or probe call on the context (it
+ * reads that call's pooled draft states).  Errors: no draft head
+ * (UNSUPPORTED), n_req mismatch or null p_out (INVALID_ARG).
+ */
+int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, void* stream);
 
 /* ------------------------------------------------------------ inspection */
 enum {

@@ -152,6 +152,14 @@ def length_head(p: np.ndarray, w1: np.ndarray, b1: np.ndarray, w2: np.ndarray,
     return u @ w2 + b2[0]
 
 
+def draft_distribution(h_draft: np.ndarray, w_lm: np.ndarray) -> np.ndarray:
+    """Eq. 2, the draft model head: P_draft(y_{t+1} | y_{1:t}) =
+    softmax(W_lm h_t^draft) over the vocabulary, rows of h_draft."""
+    logits = h_draft @ w_lm.T
+    e = np.exp(logits - logits.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
 def predicted_remaining(z_hat: np.ndarray) -> np.ndarray:
     """r_hat = max(0, exp(z_hat) - 1): inverts the z = log(1 + length) target."""
     return np.maximum(0.0, np.expm1(z_hat))

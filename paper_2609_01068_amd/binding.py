@@ -56,7 +56,7 @@ class outlets_config(C.Structure):
         ("rope_theta", C.c_double), ("rms_eps", C.c_float), ("weight_fmt", C.c_int32),
         ("act_fmt", C.c_int32), ("page_size", C.c_int32), ("max_slots", C.c_int32),
         ("max_seq_len", C.c_int32), ("num_pages", C.c_int32), ("max_batch_tokens", C.c_int32),
-        ("max_batch_requests", C.c_int32), ("keep_intermediates", C.c_int32),
+        ("max_batch_requests", C.c_int32), ("keep_intermediates", C.c_int32), ("vocab", C.c_int32),
     ]
 
 
@@ -64,7 +64,7 @@ WEIGHT_FIELDS = [
     "w_proj", "s_proj", "w_q", "s_q", "w_k", "s_k", "w_v", "s_v", "w_o", "s_o",
     "w_gate", "s_gate", "w_up", "s_up", "w_down", "s_down", "gamma_attn", "gamma_mlp",
     "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2", "w_attn_gate", "s_attn_gate",
-    "probe_w1", "probe_b1", "probe_w2", "probe_b2",
+    "probe_w1", "probe_b1", "probe_w2", "probe_b2", "w_lm", "s_lm",
 ]
 
 
@@ -85,6 +85,7 @@ _SIGS = {
     "outlets_probe_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, C.c_int64, _P, _P]),
     "outlets_probe_step": (C.c_int, [_P, C.c_int32, _I32P, _P, C.c_int64, _P, _P]),
     "outlets_probe_release": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_draft_distribution": (C.c_int, [_P, C.c_int32, _P, _P]),
     "outlets_get_meta": (C.c_int, [_P, C.c_int32, _I32P, C.c_int64, C.POINTER(C.c_int64)]),
     "outlets_get_buffer": (C.c_int, [_P, C.c_int32, _P, C.c_int64, C.POINTER(C.c_int64), _P]),
     "outlets_last_error": (C.c_char_p, []),
@@ -176,6 +177,10 @@ def outlets_probe_step(ctx, slots, h: int, row_stride: int, z_out: int, stream: 
 
 def outlets_probe_release(ctx, slots) -> int:
     return lib().outlets_probe_release(ctx, len(slots), i32_array(slots))
+
+
+def outlets_draft_distribution(ctx, n_req: int, p_out: int, stream: Optional[int]) -> int:
+    return lib().outlets_draft_distribution(ctx, n_req, p_out, stream)
 
 
 def outlets_get_meta(ctx, what: int, cap: int):

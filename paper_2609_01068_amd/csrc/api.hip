@@ -55,6 +55,7 @@ struct outlets_ctx {
     std::vector<int32_t> probe_count;   // per slot: tokens pooled by the probe (0 = inactive)
     float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
     int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
+    float* lm_logits = nullptr;  // draft model head logits [2 * max_batch_requests, V]
     std::unique_ptr<Pager> pager;
     int max_pages = 0;
 
@@ -192,6 +193,9 @@ int check_config(const outlets_config& c, const char** why) {
         return bad(OUTLETS_ERR_UNSUPPORTED, "f32 weights need f32 activations");
     if (c.weight_fmt != OUTLETS_FMT_F32 && c.act_fmt != OUTLETS_FMT_BF16)
         return bad(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 weights need bf16 activations");
+    if (c.vocab < 0) return bad(OUTLETS_ERR_INVALID_ARG, "vocab must be >= 0");
+    if (c.vocab > 0 && c.weight_fmt != OUTLETS_FMT_F32 && c.vocab % 256)
+        return bad(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 draft heads need vocab a multiple of 256");
     *why = nullptr;
     return OUTLETS_OK;
 }
@@ -275,6 +279,13 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
     return g;
 }
 
+// Draft model head input: the newest token's h_draft is the second half of
+// each pooled row ([mean ; newest]); bf16 weights read its hi/lo split.
+GemmA lm_input(const outlets_ctx* c) {
+    return (c->w_fmt == FMT_F32) ? gemm_a(c->pooled + c->d, 2 * c->d, c->d)
+                                 : gemm_a(c->pooled_bf16 + c->d, 2 * c->d, c->d);
+}
+
 int check_gemms(const outlets_ctx* c) {
     // Dummy 16-byte aligned pointers stand in for the per-call A operands.
     LayerGemms g = layer_gemms(c, c->a_norm, c->a_norm, c->a_norm, c->d);
@@ -289,6 +300,12 @@ int check_gemms(const outlets_ctx* c) {
         (rc = gemm_check(af, wf, EPI_RESID_F32, 1, c->d, c->F, g.a_down, g.b_down, 1, &why)) ||
         (rc = gemm_check(af, hf, EPI_PARTIAL, 1, c->H1, 2 * c->d, g.a_head, g.b_head, kHeadSplits, &why)))
         return fail(rc, std::string("unsupported shape: ") + why);
+    if (c->cfg.vocab > 0) {
+        const GemmA a = lm_input(c);
+        const GemmB b = gemm_b1(c->w.w_lm, c->w.s_lm, c->cfg.vocab, c->d);
+        if ((rc = gemm_check(af, wf, EPI_STORE_F32, 1, c->cfg.vocab, c->d, a, b, 1, &why)))
+            return fail(rc, std::string("unsupported draft head shape: ") + why);
+    }
     return OUTLETS_OK;
 }
 
@@ -443,6 +460,10 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
                          w.head_w2, w.head_b2};
     for (const void* p : req)
         if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "a weight pointer is null");
+    if ((cfg->vocab > 0) != (w.w_lm != nullptr))
+        return fail(OUTLETS_ERR_INVALID_ARG, "w_lm must be given exactly when vocab > 0");
+    if (cfg->vocab > 0 && cfg->weight_fmt == OUTLETS_FMT_E4M3 && !w.s_lm)
+        return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
     if (w.probe_w1 && (!w.probe_b1 || !w.probe_w2 || !w.probe_b2))
         return fail(OUTLETS_ERR_INVALID_ARG, "probe weights need w1, b1, w2 and b2");
     if (cfg->weight_fmt == OUTLETS_FMT_E4M3) {
@@ -539,6 +560,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         if (need) ALLOC(c->splitk_ws, need);
     }
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
+    if (cfg->vocab > 0) ALLOC(c->lm_logits, sizeof(float) * 2 * Bm * cfg->vocab);
     if (c->probe) {
         ALLOC(c->probe_sum, sizeof(float) * cfg->max_slots * c->d);
         ALLOC(c->probe_meta, sizeof(int32_t) * c->meta_cap);
@@ -803,6 +825,26 @@ int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots) {
         seen[slots[i]] = 1;
     }
     for (int i = 0; i < n; ++i) ctx->probe_count[slots[i]] = 0;
+    return OUTLETS_OK;
+}
+
+int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, void* stream) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (ctx->cfg.vocab <= 0) return fail(OUTLETS_ERR_UNSUPPORTED, "the context has no draft model head (vocab 0)");
+    if (n_req <= 0 || n_req != ctx->last_n)
+        return fail(OUTLETS_ERR_INVALID_ARG, "n_req must equal the last predict call's request count");
+    if (!p_out) return fail(OUTLETS_ERR_INVALID_ARG, "null p_out");
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int V = ctx->cfg.vocab;
+    const bool split = ctx->w_fmt != FMT_F32;          // hi rows [0, n), lo rows [n, 2n)
+    const int rows = split ? 2 * n_req : n_req;
+    gemm_launch(ctx->act_fmt, ctx->w_fmt, EPI_STORE_F32, rows, V, static_cast<int>(ctx->d), lm_input(ctx),
+                gemm_b1(ctx->w.w_lm, ctx->w.s_lm, V, ctx->d), gemm_c(ctx->lm_logits, V), 1, st,
+                ctx->splitk_ws, ctx->splitk_bytes);
+    launch_lm_softmax(n_req, V, ctx->lm_logits, split, p_out, st);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return OUTLETS_OK;
 }
 

@@ -137,6 +137,10 @@ void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, c
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
                         const void* b1, const void* w2, const void* b2, float* z, hipStream_t st);
 
+// Draft model head (Eq. 2): p[i] = softmax over v of logits row i (plus row
+// n + i when two_rows: the hi/lo halves of a bf16-split input).
+void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* p, hipStream_t st);
+
 void launch_copy_rows_act(int act_fmt, int rows, int d, const float* src, int64_t lds,
                           void* dst, int64_t ldd, hipStream_t st);
 

@@ -399,6 +399,41 @@ void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, c
                            req_slot, req_start, pool_sum, pooled, pooled_bf16);
 }
 
+namespace {
+
+// Draft model head softmax (Eq. 2): one 1024-thread block per request over
+// its V logits; with two_rows the logits are the sum of row i (bf16 hi part
+// of the draft state) and row n + i (lo part).
+__global__ void __launch_bounds__(1024)
+lm_softmax_kernel(int n, int v, const float* logits, int two_rows, float* p) {
+    __shared__ float red[16];
+    const int i = blockIdx.x;
+    const float* hi = logits + (int64_t)i * v;
+    const float* lo = logits + (int64_t)(n + i) * v;
+    auto x = [&](int j) { return two_rows ? hi[j] + lo[j] : hi[j]; };
+    float mx = -INFINITY;
+    for (int j = threadIdx.x; j < v; j += 1024) mx = fmaxf(mx, x(j));
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    mx = red[0];
+    for (int k = 1; k < 16; ++k) mx = fmaxf(mx, red[k]);
+    __syncthreads();
+    float sum = 0.f;
+    for (int j = threadIdx.x; j < v; j += 1024) sum += __expf(x(j) - mx);
+    sum = block_sum<1024>(sum, red);
+    const float inv = 1.0f / sum;
+    float* pr = p + (int64_t)i * v;
+    for (int j = threadIdx.x; j < v; j += 1024) pr[j] = __expf(x(j) - mx) * inv;
+}
+
+}  // namespace
+
+void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* p, hipStream_t st) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(lm_softmax_kernel, dim3(n), dim3(1024), 0, st, n, v, logits, two_rows ? 1 : 0, p);
+}
+
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
                         const void* b1, const void* w2, const void* b2, float* z, hipStream_t st) {
     if (n_req <= 0) return;

@@ -79,6 +79,18 @@ class OutletsPredictor:
             else:
                 self.tensors[GATE_NAME] = to_device(entry, self.device)
             w.w_attn_gate = _ptr(self.tensors[GATE_NAME])
+        self.vocab = 0
+        if weights.get("w_lm") is not None:              # draft model head (Eq. 2)
+            entry = weights["w_lm"]
+            if weight_fmt == "e4m3":
+                codes, scale = entry
+                self.tensors["w_lm"] = to_device(codes, self.device)
+                self.tensors["s_lm"] = to_device(scale, self.device)
+                w.s_lm = _ptr(self.tensors["s_lm"])
+            else:
+                self.tensors["w_lm"] = to_device(entry, self.device)
+            w.w_lm = _ptr(self.tensors["w_lm"])
+            self.vocab = int(shape.vocab)
         if weights.get("probe_w1") is not None:          # MLP-probe baseline
             for name in PROBE:
                 self.tensors[name] = to_device(weights[name], self.device)
@@ -92,6 +104,7 @@ class OutletsPredictor:
         cfg.max_slots, cfg.max_seq_len, cfg.num_pages = max_slots, max_seq_len, num_pages
         cfg.max_batch_tokens, cfg.max_batch_requests = max_batch_tokens, max_batch_requests
         cfg.keep_intermediates = int(bool(keep_intermediates))
+        cfg.vocab = self.vocab
         self.cfg = cfg
         torch.cuda.synchronize(self.device)
         self.ctx = B.outlets_create(cfg, w, device)
@@ -155,6 +168,15 @@ class OutletsPredictor:
 
     def probe_release(self, slots: Sequence[int]) -> None:
         B.check(B.outlets_probe_release(self.ctx, list(slots)), "outlets_probe_release")
+
+    # ------------------------------------------------------------ draft model head
+    def draft_distribution(self, n_req: int, p_out: Optional[torch.Tensor] = None, stream=None):
+        """Eq. 2 for the requests of the last prefill/step call: [n_req, V] fp32."""
+        if p_out is None:
+            p_out = torch.empty((max(n_req, 1), self.vocab), dtype=torch.float32, device=self.device)
+        B.check(B.outlets_draft_distribution(self.ctx, n_req, p_out.data_ptr(), _stream_ptr(stream)),
+                "outlets_draft_distribution")
+        return p_out[:n_req]
 
     # ------------------------------------------------------------ inspection
     def profile(self, enable: bool) -> None:

@@ -34,7 +34,7 @@ __all__ = [
     "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
     "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
     "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS", "GATE_NAME",
-    "make_probe_weights",
+    "make_probe_weights", "make_lm_weights",
 ]
 
 # Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
@@ -58,6 +58,7 @@ class DraftShape:
     head_hidden: int  # width of the length head's hidden layer
     rope_theta: float
     rms_eps: float = 1e-5
+    vocab: int = 0    # vocabulary of the draft model head (Eq. 2)
 
     def weight_shapes(self) -> Dict[str, Tuple[int, ...]]:
         d, hd = self.d, self.head_dim
@@ -101,11 +102,12 @@ class Workload:
 
 
 SHAPE_TINY = DraftShape(d=256, n_q=4, n_kv=2, head_dim=64, ffn=688,
-                        head_hidden=128, rope_theta=1e4)
+                        head_hidden=128, rope_theta=1e4, vocab=512)
+# Llama-3 vocabulary (128,256 entries) for the draft model head of the 8B/70B shapes
 SHAPE_8B = DraftShape(d=4096, n_q=32, n_kv=8, head_dim=128, ffn=14336,
-                      head_hidden=1024, rope_theta=5e5)
+                      head_hidden=1024, rope_theta=5e5, vocab=128256)
 SHAPE_70B = DraftShape(d=8192, n_q=64, n_kv=8, head_dim=128, ffn=28672,
-                       head_hidden=2048, rope_theta=5e5)
+                       head_hidden=2048, rope_theta=5e5, vocab=128256)
 
 WORKLOADS: Dict[int, Workload] = {
     0: Workload(0, "tiny-fp32", SHAPE_TINY, "f32", "f32", 4,
@@ -215,6 +217,20 @@ def make_probe_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
             out[name], fmt[name] = to_bf16_bits(x), "bf16"
     out["_fmt"] = fmt
     return out
+
+
+def make_lm_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
+    """W_lm [vocab, d] of the draft model head (Eq. 2), N(0, 0.02^2), from the
+    stream after the probe's, stored like the big linears (``w_lm``; for
+    e4m3 a ``(codes, scale_bits)`` tuple).  Returns a dict with ``_fmt``."""
+    v, d = wl.shape.vocab, wl.shape.d
+    rng = _rng(seed, wl.cfg_id, len(WEIGHT_NAMES) + 5)
+    x = np.float32(0.02) * rng.standard_normal((v, d), dtype=np.float32)
+    if wl.weight_fmt == "f32":
+        return {"w_lm": x, "_fmt": {"w_lm": "f32"}}
+    if wl.weight_fmt == "e4m3":
+        return {"w_lm": encode_e4m3(x), "_fmt": {"w_lm": "e4m3"}}
+    return {"w_lm": to_bf16_bits(x), "_fmt": {"w_lm": "bf16"}}
 
 
 def make_lengths(wl: Workload, seed: int = 0, n_req: Optional[int] = None) -> np.ndarray:

@@ -100,9 +100,9 @@ def step_inputs(case: Case, step: int, requests=None):
     return make_step_states(case.wl, len(case.lens), step, requests=requests)
 
 
-def reduced_shape(d=512, n_q=8, n_kv=2, hd=128, ffn=1024, head_hidden=256, theta=5e5):
+def reduced_shape(d=512, n_q=8, n_kv=2, hd=128, ffn=1024, head_hidden=256, theta=5e5, vocab=1024):
     return DraftShape(d=d, n_q=n_q, n_kv=n_kv, head_dim=hd, ffn=ffn, head_hidden=head_hidden,
-                      rope_theta=theta)
+                      rope_theta=theta, vocab=vocab)
 
 
 def mixed_prompt_states(wl, lens, sample, seed=0):

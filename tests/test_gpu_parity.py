@@ -365,3 +365,107 @@ def test_mlp_probe_needs_probe_weights():
         pred.probe_prefill([0], [8], H[1])
     assert e.value.rc == B.OUTLETS_ERR_UNSUPPORTED
     pred.close()
+
+
+# ------------------------------------------------------------- draft model head (Eq. 2)
+
+def _with_lm(case):
+    import dataclasses
+    from synth import make_lm_weights
+    LW = make_lm_weights(case.wl)
+    W = dict(case.weights)
+    W["w_lm"] = LW["w_lm"]
+    W["_fmt"] = {**case.weights["_fmt"], **LW["_fmt"]}
+    return dataclasses.replace(case, weights=W)
+
+
+def _check_distribution(p_gpu, h_last, w_lm, fmt, label):
+    from oracle import draft_distribution
+    ref = draft_distribution(h_last[None, :], w_lm)[0]
+    err = rel_fro(p_gpu, ref)
+    assert abs(p_gpu.sum() - 1.0) <= 1e-4, label
+    assert err <= TOL_HDRAFT[fmt], (label, err)
+    return err
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 4], ids=["tiny-fp32", "bf16-reduced", "e4m3-reduced"])
+def test_draft_head_prefill_and_steps(cfg):
+    from paper_2609_01068_amd import binding as B
+    from oracle.formats import decode_weight
+    if cfg == 0:
+        case = make_case(0)
+    elif cfg == 1:
+        case = make_case(1, lens=[1, 17, 100, 300, 33], shape=reduced_shape(), n_req=5)
+    else:
+        case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=16, n_kv=2), n_req=4)
+    case = _with_lm(case)
+    lens = case.lens
+    n = len(lens)
+    say(f"case: draft model head (V={case.wl.shape.vocab}), cfg {cfg}, lens {list(lens)}, 2 steps")
+    pred = make_predictor(case, max_seq_len=int(lens.max()) + 8)
+    H = device_states(case)
+    slots = list(range(n))
+    pred.prefill(slots, lens, *H)
+    p = tensor_to_f64(pred.draft_distribution(n))
+    orc = oracle_for(case)
+    w_lm = decode_weight(case.weights["w_lm"], case.weights["_fmt"]["w_lm"])
+    O = oracle_states(case)
+    off = np.concatenate([[0], np.cumsum(lens)])
+    states, worst = [], 0.0
+    for i in range(n):
+        _, hi, st = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O))
+        states.append(st)
+        worst = max(worst, _check_distribution(p[i], hi[-1], w_lm, case.fmt, ("prefill", i)))
+    for t in range(1, 3):
+        S = step_inputs(case, t)
+        pred.step(slots, *device_states(case, S))
+        p = tensor_to_f64(pred.draft_distribution(n))
+        _, hr = orc.step(states, *oracle_states(case, S))
+        for i in range(n):
+            worst = max(worst, _check_distribution(p[i], hr[i], w_lm, case.fmt, ("step", t, i)))
+    say(f"  worst distribution rel err {worst:.3e}")
+    with pytest.raises(B.OutletsError) as e:
+        pred.draft_distribution(n - 1 if n > 1 else 2)
+    assert e.value.rc == B.OUTLETS_ERR_INVALID_ARG
+    pred.close()
+
+
+def test_draft_head_absent_without_vocab():
+    from paper_2609_01068_amd import binding as B
+    case = make_case(0, lens=[8])
+    pred = make_predictor(case)
+    H = device_states(case)
+    pred.prefill([0], [8], *H)
+    with pytest.raises(B.OutletsError) as e:
+        pred.draft_distribution(1)
+    assert e.value.rc == B.OUTLETS_ERR_UNSUPPORTED
+    pred.close()
+
+
+def test_config1_draft_head_sampled_requests():
+    """Eq. 2 at the 8B shape (V = 128,256) on the 32-request batch; the oracle
+    recomputes two sampled requests."""
+    from oracle.formats import decode_weight
+    from synth import make_prompt_states
+    case = _with_lm(make_case(1))
+    lens = case.lens
+    say(f"case: config-1 draft model head, V={case.wl.shape.vocab}, B={len(lens)}, T={int(lens.sum())}")
+    pred = make_predictor(case)
+    H = device_states(case)
+    pred.prefill(list(range(len(lens))), lens, *H)
+    p = tensor_to_f64(pred.draft_distribution(len(lens)))
+    assert np.all(np.isfinite(p))
+    assert np.allclose(p.sum(axis=1), 1.0, atol=1e-4)
+    order = np.argsort(lens)
+    sample = [int(order[0]), int(order[len(order) // 3])]
+    orc = oracle_for(case)
+    w_lm = decode_weight(case.weights["w_lm"], case.weights["_fmt"]["w_lm"])
+    O = oracle_states(case, make_prompt_states(case.wl, lens, requests=sample))
+    o_off = 0
+    for i in sample:
+        n = int(lens[i])
+        _, hi, _ = orc.prefill_one(*(x[o_off:o_off + n] for x in O))
+        o_off += n
+        err = _check_distribution(p[i], hi[-1], w_lm, "bf16", ("request", i))
+        say(f"  request {i} (n={n}) distribution rel err {err:.3e}")
+    pred.close()

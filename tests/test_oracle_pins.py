@@ -407,6 +407,19 @@ def test_probe_steps_equal_prefill_recompute():
         assert abs(zs - _torch_probe(W, h[:t + 1])) <= 1e-12 * max(1.0, abs(zs))
 
 
+# ------------------------------------------------------------- draft model head
+
+def test_draft_distribution_matches_torch_softmax():
+    from oracle import draft_distribution
+    r = np.random.default_rng(31)
+    h = r.standard_normal((3, 16)) * 2.0
+    w = r.standard_normal((50, 16))
+    p = draft_distribution(h, w)
+    ref = torch.softmax(torch.from_numpy(h) @ torch.from_numpy(w).T, dim=-1).numpy()
+    assert np.allclose(p, ref, rtol=1e-12, atol=1e-15)
+    assert np.allclose(p.sum(axis=1), 1.0, rtol=0, atol=1e-12)
+
+
 # ------------------------------------------------------------- planted mistakes
 
 def _fails(fn, *args):
