@@ -31,14 +31,15 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def gemm_flops(shape, T: int, attn_gate: bool = False):
+def gemm_flops(shape, T: int, attn_gate: bool = False, input_embed: bool = False):
     """Algorithmic FLOPs per launch of each GEMM group for T tokens (the QKV
-    GEMM also produces the Gated Attention gate when ``attn_gate``)."""
+    GEMM also produces the Gated Attention gate when ``attn_gate``, and reads
+    2d columns with input embeddings)."""
     d, hd = shape.d, shape.head_dim
     qkv = (shape.n_q * (2 if attn_gate else 1) + 2 * shape.n_kv) * hd
     return {
         "FUSE_GEMM": 2.0 * T * d * 3 * d,
-        "QKV_GEMM": 2.0 * T * qkv * d,
+        "QKV_GEMM": 2.0 * T * qkv * d * (2 if input_embed else 1),
         "O_GEMM": 2.0 * T * d * shape.n_q * hd,
         "GATE_UP_GEMM": 2.0 * T * 2 * shape.ffn * d,
         "DOWN_GEMM": 2.0 * T * d * shape.ffn,
@@ -70,16 +71,19 @@ def cpu_baseline(wl, W, lens, budget_s: float = 12.0):
     work; scaled to requests/s of the batch's mean request length."""
     import numpy as np
     from oracle import oracle_from_workload, states_to_f64
-    from synth import make_prompt_states, make_step_states
+    from synth import make_prompt_states, make_prompt_tokens, make_step_states, make_step_tokens
 
     orc = oracle_from_workload(wl, W)
     t_total, tok, done = 0.0, 0, []
+    emb = getattr(wl, "input_embed", False)
     for i in range(len(lens)):
         st = states_to_f64(make_prompt_states(wl, lens, requests=[i]), wl.act_fmt)
         sp = states_to_f64(make_step_states(wl, len(lens), 1, requests=[i]), wl.act_fmt)
+        tp = make_prompt_tokens(wl, lens, requests=[i]) if emb else None
+        ts = make_step_tokens(wl, len(lens), 1, requests=[i]) if emb else None
         t0 = time.perf_counter()
-        _, _, s = orc.prefill([int(lens[i])], *st)
-        orc.step(s, *sp)
+        _, _, s = orc.prefill([int(lens[i])], *st, tokens=tp)
+        orc.step(s, *sp, tokens=ts)
         t_total += time.perf_counter() - t0
         tok += int(lens[i]) + 1
         done.append(i)
@@ -223,7 +227,7 @@ def bench_prefill(a, cfg_id):
     prof = pred.profile_read("prefill")
     pred.profile(False)
     ms_per_step = max(ev0.elapsed_time(ev1), wall * 1e3) / a.steps
-    flops = gemm_flops(wl.shape, T, wl.attn_gate)
+    flops = gemm_flops(wl.shape, T, wl.attn_gate, wl.input_embed)
     kernels = {}
     for name, (ms, n) in prof.items():
         if n:
@@ -329,6 +333,9 @@ def main(argv=None):
     ap.add_argument("--draft-head", action="store_true",
                     help="prefill-8b: also run the draft model head (Eq. 2, V = 128,256) after the "
                          "prefill and after the step")
+    ap.add_argument("--input-embed", action="store_true",
+                    help="prefill-8b: draft layer with EAGLE-3 input embeddings (QKV over [emb ; f_ctx], "
+                         "V = 128,256 embedding table)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 times); used to scale "
                          "rocprof's FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -336,6 +343,10 @@ def main(argv=None):
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the path shards over "
               "requests and this build measures one GPU's share", file=sys.stderr)
+        return 2
+
+    if a.input_embed and a.workload != "prefill-8b":
+        print("--input-embed is measured on the prefill-8b workload only", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -361,7 +372,7 @@ def main(argv=None):
     if a.workload != "prefill-8b":
         return bench_prefill(a, {"prefill-8b-large": 2, "prefill-70b-e4m3": 4}[a.workload])
 
-    wl = workload(1, attn_gate=a.attn_gate)
+    wl = workload(1, attn_gate=a.attn_gate, input_embed=a.input_embed)
     print(f"[bench] generating {wl.name} weights and inputs", file=sys.stderr, flush=True)
     W = make_weights(wl, a.seed)
     if a.draft_head:
@@ -371,6 +382,11 @@ def main(argv=None):
     T, B = int(lens.sum()), len(lens)
     H = [to_device(x) for x in make_prompt_states(wl, lens, a.seed)]
     S = [to_device(x) for x in make_step_states(wl, B, 1, a.seed)]
+    tok_p = tok_step = None
+    if wl.input_embed:
+        from synth import make_prompt_tokens, make_step_tokens
+        tok_p = torch.from_numpy(make_prompt_tokens(wl, lens, a.seed)).cuda()
+        tok_step = torch.from_numpy(make_step_tokens(wl, B, 1, a.seed)).cuda()
     pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B,
                             max_seq_len=int(lens.max()) + 16, num_pages=B * ((int(lens.max()) + 16 + 15) // 16),
                             max_batch_tokens=T, max_batch_requests=B)
@@ -381,10 +397,10 @@ def main(argv=None):
     probs = torch.empty((B, wl.shape.vocab), dtype=torch.float32, device="cuda") if a.draft_head else None
 
     def one_step():
-        pred.prefill(slots, lens, *H, z_out=z, stream=stream)
+        pred.prefill(slots, lens, *H, z_out=z, stream=stream, tokens=tok_p)
         if probs is not None:
             pred.draft_distribution(B, p_out=probs, stream=stream)
-        pred.step(slots, *S, z_out=z1, stream=stream)
+        pred.step(slots, *S, z_out=z1, stream=stream, tokens=tok_step)
         if probs is not None:
             pred.draft_distribution(B, p_out=probs, stream=stream)
         pred.release(slots)
@@ -413,7 +429,7 @@ def main(argv=None):
     req_s = B / (ms_per_step / 1e3)
     tok_s = (T + B) / (ms_per_step / 1e3)
 
-    flops = gemm_flops(wl.shape, T, wl.attn_gate)
+    flops = gemm_flops(wl.shape, T, wl.attn_gate, wl.input_embed)
     kernels = {}
     for name, (ms, n) in prof_pre.items():
         if n:
@@ -442,7 +458,7 @@ def main(argv=None):
                                "prompts clipped to [32, 4096], static prediction + 1 dynamic step per request",
                    "requests": B, "prompt_tokens": T, "d": wl.shape.d, "heads": [wl.shape.n_q, wl.shape.n_kv],
                    "head_dim": wl.shape.head_dim, "ffn": wl.shape.ffn, "head_hidden": wl.shape.head_hidden,
-                   "page_size": 16, "attn_gate": wl.attn_gate,
+                   "page_size": 16, "attn_gate": wl.attn_gate, "input_embed": wl.input_embed,
                    "draft_head_vocab": wl.shape.vocab if a.draft_head else 0},
         "draft_tokens_per_s": tok_s,
         "roofline": {"kernel": "gate/up GEMM + SwiGLU epilogue (prefill)", "bound": "mfma",

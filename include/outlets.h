@@ -20,7 +20,9 @@
  *   - rotate-half RoPE: channel pair (c, c + hd/2) rotated by
  *     p * theta^(-2c/hd), no frequency rescaling;
  *   - plain grouped-query attention (query head h reads KV head
- *     h / (n_q / n_kv)), causal within a request; no attention gate;
+ *     h / (n_q / n_kv)), causal within a request; the attention output gate
+ *     (Gated Attention) and the input-embedding concat are optional, off
+ *     unless their weights are given;
  *   - head input p = [mean of h_draft over the request's tokens so far ;
  *     h_draft of the newest token], then Linear(2d, H1) + ReLU +
  *     Linear(H1, 1), both with biases.
@@ -133,9 +135,17 @@ typedef struct outlets_config {
  *     (optional, all or none; small-weight format like head_*): the MLP-probe
  *     baseline (Section 5.1 baselines: an MLP regressor on the frozen target
  *     model's hidden states), see outlets_probe_prefill.
- *   w_lm [V, d] (required iff cfg.vocab > 0; weight_fmt, with s_lm row
- *     scales for E4M3): the draft model head of Eq. 2, see
- *     outlets_draft_distribution.
+ *   w_lm [V, d] (optional, NULL = no draft head; needs cfg.vocab = V > 0;
+ *     weight_fmt, with s_lm row scales for E4M3): the draft model head of
+ *     Eq. 2, see outlets_draft_distribution.
+ *   embed [V, d] (act_fmt) and gamma_emb [d] (optional, both or none; need
+ *     cfg.vocab = V > 0): EAGLE-3 input embeddings, the backbone component
+ *     of the Section 5 ablation.  The attention block then reads the 2d-wide
+ *     row x = [RMSNorm(embed[token]) * gamma_emb ; RMSNorm(f_ctx) *
+ *     gamma_attn]: w_q, w_k, w_v (and w_attn_gate) become [out, 2d] with
+ *     the embedding columns first; the residual stream still starts at
+ *     f_ctx.  The predict calls then take one token id per row.
+ * cfg.vocab > 0 needs w_lm or embed (or both).
  * Element format: weight_fmt for the big linears; F32 for the rest when
  * weight_fmt is F32, BF16 otherwise.
  */
@@ -161,6 +171,8 @@ typedef struct outlets_weights {
     const void* probe_w2;
     const void* probe_b2;
     const void* w_lm;    const void* s_lm;
+    const void* embed;
+    const void* gamma_emb;
 } outlets_weights;
 
 typedef struct outlets_ctx outlets_ctx;
@@ -188,6 +200,11 @@ int outlets_destroy(outlets_ctx* ctx);
  *     cu_0 = 0, cu_{i+1} = cu_i + lens[i]; row r starts at element
  *     r * row_stride (row_stride >= d_model).  One [T, 3d] tensor may be
  *     passed as base, base + d, base + 2d with row_stride 3d.
+ *   tokens (device, int32 [T], packed like the states; ignored unless the
+ *     context has input embeddings, then required): the token id paired
+ *     with each row (in EAGLE-3 the token that follows the row's position;
+ *     the caller decides the pairing).  An id outside [0, V) cannot be
+ *     reported from the device: its embedding row is taken as zero.
  *   z_out (device, float32 [n_req]): z_hat_i, the predicted log(1 + L_i).
  *   hdraft_out (device, act_fmt [T, d] or NULL): h_draft of every token.
  *   stream: hipStream_t (NULL = default stream).
@@ -200,14 +217,15 @@ int outlets_destroy(outlets_ctx* ctx);
  */
 int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
                             const int32_t* lens, const void* h_low, const void* h_mid,
-                            const void* h_high, int64_t row_stride, float* z_out,
-                            void* hdraft_out, void* stream);
+                            const void* h_high, int64_t row_stride, const int32_t* tokens,
+                            float* z_out, void* hdraft_out, void* stream);
 
 /*
  * Dynamic prediction (Section 3.2, t >= 1): one generated token per request.
  *   slots [n_req] (host): active, distinct slots.
  *   h_low, h_mid, h_high (device, act_fmt [n_req rows], row_stride): states
  *     of the newly generated token y_t, row i for slots[i].
+ *   tokens (device int32 [n_req]; as in outlets_predict_prefill).
  *   z_out (device float32 [n_req]): z_hat_t, the predicted log(1 + r_t).
  *   hdraft_out (device act_fmt [n_req, d] or NULL).
  * The token takes position (cached length) and attends over every cached key
@@ -220,7 +238,8 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
  */
 int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
                          const void* h_low, const void* h_mid, const void* h_high,
-                         int64_t row_stride, float* z_out, void* hdraft_out, void* stream);
+                         int64_t row_stride, const int32_t* tokens, float* z_out,
+                         void* hdraft_out, void* stream);
 
 /* End requests: frees their pages and state.  Inactive slots are a no-op;
  * an out-of-range or repeated slot fails with no change. */
@@ -260,8 +279,8 @@ int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);
  *   n_req: must equal the last predict call's request count.
  *   p_out (device): fp32 [n_req, V] row-major probabilities.
  * Must be queued before the next predict or probe call on the context (it
- * reads that call's pooled draft states).  Errors: no draft head
- * (UNSUPPORTED), n_req mismatch or null p_out (INVALID_ARG).
+ * reads that call's pooled draft states).  Errors: no draft head, w_lm
+ * NULL (UNSUPPORTED), n_req mismatch or null p_out (INVALID_ARG).
  */
 int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, void* stream);
 
@@ -295,14 +314,16 @@ enum {
     OUTLETS_BUF_HDRAFT = 8,     /* h_draft, float32 [T, d] */
     OUTLETS_BUF_POOLED = 9,     /* head input p, float32 [n_req, 2d] */
     OUTLETS_BUF_K_POOL = 10,    /* key pages, act [num_pages, n_kv, 16, hd] */
-    OUTLETS_BUF_V_POOL = 11     /* value pages, act [num_pages, n_kv, 16, hd] */
+    OUTLETS_BUF_V_POOL = 11,    /* value pages, act [num_pages, n_kv, 16, hd] */
+    OUTLETS_BUF_NORM_EMB = 12   /* RMSNorm(embed[token]) * gamma_emb, act [T, d] (input embeddings) */
 };
 
 /*
  * Copy an activation of the last call (rows of that call only) or a KV pool
  * into caller device memory `dst` (`nbytes` capacity) on `stream`;
- * *n_bytes receives the size.  Buffers 0..8 need keep_intermediates (except
- * HDRAFT, POOLED and the pools, always kept).
+ * *n_bytes receives the size.  Buffers 0..8 and 12 need keep_intermediates
+ * (HDRAFT, POOLED and the pools are always kept); NORM_EMB needs input
+ * embeddings.
  */
 int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbytes,
                        int64_t* n_bytes, void* stream);
@@ -311,7 +332,7 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
 enum {
     OUTLETS_K_META = 0,         /* page-table scatter + token metadata */
     OUTLETS_K_FUSE_GEMM = 1,    /* Eq. 1 projection */
-    OUTLETS_K_NORM = 2,         /* the three RMSNorms */
+    OUTLETS_K_NORM = 2,         /* the RMSNorms (and the embedding gather + norm) */
     OUTLETS_K_QKV_GEMM = 3,
     OUTLETS_K_ROPE_KV = 4,      /* rotary embedding + paged K/V write */
     OUTLETS_K_ATTN = 5,

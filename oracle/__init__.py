@@ -12,5 +12,5 @@ from .model import (OracleShape, OracleModel, RequestState, oracle_from_workload
                     decode_weights, fuse, rms_norm, rope, causal_gqa_attention, silu,
                     swiglu_mlp, length_head, predicted_remaining, states_to_f64,
                     sigmoid, attention_output_gate, OracleProbe, ProbeState, probe_from_stored,
-                    draft_distribution)
+                    draft_distribution, embedded_attention_input)
 from . import meta  # noqa: F401

@@ -23,6 +23,14 @@ here is stated next to the code:
   attention output element, per query head and channel, is multiplied by
   sigmoid of a bias-free linear map of the same normed input that feeds
   Q/K/V, before the heads are concatenated into W_o.
+* Input embeddings (the EAGLE-3 component the Section 5 ablation lists,
+  no formula given): optional, off unless the weights carry ``embed``.  The
+  reading taken is EAGLE-3's: the attention block reads the 2d-wide row
+  [RMSNorm(embed[token]) * gamma_emb ; RMSNorm(f_ctx) * gamma_attn], so
+  W_q, W_k, W_v (and the gate) have 2d input columns, embedding columns
+  first; the residual stream still starts at f_ctx.  Which token is paired
+  with a row is the caller's choice (EAGLE-3 pairs a position with the
+  token that follows it).
 * h^draft is the final RMSNorm of the layer output (both heads read it).
 * Length head (Section 4.2): the pooled state p = [mean over the request's
   tokens of h^draft ; h^draft of the newest token] goes through
@@ -61,9 +69,10 @@ class OracleShape:
 
 def decode_weights(stored: Dict[str, object]) -> Dict[str, np.ndarray]:
     """Stored weights (as the seeded generator returns them) -> float64.
-    The attention output gate ``w_attn_gate`` is carried over when present."""
+    The attention output gate ``w_attn_gate`` and the input-embedding table
+    ``embed`` with its gain ``gamma_emb`` are carried over when present."""
     fmt = stored["_fmt"]
-    keys = WEIGHT_KEYS + (("w_attn_gate",) if "w_attn_gate" in stored else ())
+    keys = WEIGHT_KEYS + tuple(k for k in ("w_attn_gate", "embed", "gamma_emb") if k in stored)
     return {k: decode_weight(stored[k], fmt[k]) for k in keys}
 
 
@@ -139,6 +148,14 @@ def attention_output_gate(o: np.ndarray, a: np.ndarray, w_attn_gate: np.ndarray)
     return o * sigmoid(a @ w_attn_gate.T)
 
 
+def embedded_attention_input(emb_rows: np.ndarray, gamma_emb: np.ndarray, a: np.ndarray,
+                             eps: float) -> Tuple[np.ndarray, np.ndarray]:
+    """EAGLE-3 input embeddings: e = RMSNorm(emb_rows) * gamma_emb and the
+    attention block's input row [e ; a], a the normed f_ctx.  Returns (e, x)."""
+    e = rms_norm(emb_rows, gamma_emb, eps)
+    return e, np.concatenate([e, a], axis=1)
+
+
 def swiglu_mlp(b: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray,
                w_down: np.ndarray) -> np.ndarray:
     """(silu(b W_gate^T) * (b W_up^T)) W_down^T."""
@@ -182,14 +199,20 @@ class OracleModel:
         self.w = weights
 
     # one pass of the draft layer over new tokens at known positions
-    def _layer(self, h_low, h_mid, h_high, positions, k_prev, v_prev, k_pos_prev, capture=None):
+    def _layer(self, h_low, h_mid, h_high, positions, k_prev, v_prev, k_pos_prev, capture=None,
+               tokens=None):
         s, w = self.s, self.w
         n = h_low.shape[0]
         f = fuse(w["w_proj"], h_low, h_mid, h_high)
         a = rms_norm(f, w["gamma_attn"], s.rms_eps)
-        q = (a @ w["w_q"].T).reshape(n, s.n_q, s.head_dim)
-        k = (a @ w["w_k"].T).reshape(n, s.n_kv, s.head_dim)
-        v = (a @ w["w_v"].T).reshape(n, s.n_kv, s.head_dim)
+        if "embed" in w:
+            e, x_attn = embedded_attention_input(w["embed"][np.asarray(tokens)], w["gamma_emb"], a,
+                                                 s.rms_eps)
+        else:
+            e, x_attn = None, a
+        q = (x_attn @ w["w_q"].T).reshape(n, s.n_q, s.head_dim)
+        k = (x_attn @ w["w_k"].T).reshape(n, s.n_kv, s.head_dim)
+        v = (x_attn @ w["w_v"].T).reshape(n, s.n_kv, s.head_dim)
         q = rope(q, positions, s.rope_theta)
         k = rope(k, positions, s.rope_theta)
         k_all = np.concatenate([k_prev, k], axis=0)
@@ -197,12 +220,14 @@ class OracleModel:
         k_pos = np.concatenate([k_pos_prev, positions])
         o = causal_gqa_attention(q, k_all, v_all, positions, k_pos).reshape(n, s.n_q * s.head_dim)
         if "w_attn_gate" in w:
-            o = attention_output_gate(o, a, w["w_attn_gate"])
+            o = attention_output_gate(o, x_attn, w["w_attn_gate"])
         x1 = f + o @ w["w_o"].T
         b = rms_norm(x1, w["gamma_mlp"], s.rms_eps)
         x2 = x1 + swiglu_mlp(b, w["w_gate"], w["w_up"], w["w_down"])
         h_draft = rms_norm(x2, w["gamma_final"], s.rms_eps)
         if capture is not None:
+            if e is not None:
+                capture["norm_emb"] = e
             capture.update(fused=f, norm_attn=a, q=q.reshape(n, -1), k=k, v=v,
                            attn=o, x1=x1, norm_mlp=b,
                            mlp_act=silu(b @ w["w_gate"].T) * (b @ w["w_up"].T), x2=x2,
@@ -213,15 +238,17 @@ class OracleModel:
         w = self.w
         return length_head(pooled, w["head_w1"], w["head_b1"], w["head_w2"], w["head_b2"])
 
-    def prefill_one(self, h_low, h_mid, h_high, capture=None) -> Tuple[float, np.ndarray, RequestState]:
+    def prefill_one(self, h_low, h_mid, h_high, capture=None, tokens=None
+                    ) -> Tuple[float, np.ndarray, RequestState]:
         """Static prediction (Section 3.2, t = 0) for one prompt of n tokens.
-        ``capture`` (a dict) receives the layer's intermediate activations."""
+        ``capture`` (a dict) receives the layer's intermediate activations;
+        ``tokens`` [n] are the ids paired with the rows (input embeddings)."""
         s = self.s
         n = h_low.shape[0]
         empty = np.zeros((0, s.n_kv, s.head_dim))
         pos = np.arange(n)
         h_draft, k, v = self._layer(h_low, h_mid, h_high, pos, empty, empty,
-                                    np.zeros(0, dtype=np.int64), capture)
+                                    np.zeros(0, dtype=np.int64), capture, tokens)
         pool_sum = h_draft.sum(axis=0)
         pooled = np.concatenate([pool_sum / n, h_draft[n - 1]])[None, :]
         if capture is not None:
@@ -229,13 +256,14 @@ class OracleModel:
         z = float(self._head(pooled)[0])
         return z, h_draft, RequestState(k, v, pool_sum, n)
 
-    def step_one(self, st: RequestState, h_low, h_mid, h_high) -> Tuple[float, np.ndarray]:
+    def step_one(self, st: RequestState, h_low, h_mid, h_high, token=None) -> Tuple[float, np.ndarray]:
         """Dynamic prediction (Section 3.2, t >= 1): one new token for one request.
         Updates ``st`` in place."""
         p = st.count
         pos = np.array([p])
         h_draft, k, v = self._layer(h_low[None, :], h_mid[None, :], h_high[None, :], pos,
-                                    st.k, st.v, np.arange(p))
+                                    st.k, st.v, np.arange(p), None,
+                                    None if token is None else [token])
         st.k, st.v = k, v
         st.pool_sum = st.pool_sum + h_draft[0]
         st.count = p + 1
@@ -243,24 +271,26 @@ class OracleModel:
         return float(self._head(pooled)[0]), h_draft[0]
 
     # batched API: requests one by one, packed outputs
-    def prefill(self, lens: Sequence[int], h_low, h_mid, h_high):
+    def prefill(self, lens: Sequence[int], h_low, h_mid, h_high, tokens=None):
         """Packed prompts -> (z [B], h_draft [T, d], states)."""
         offs = np.concatenate([[0], np.cumsum(np.asarray(lens, dtype=np.int64))])
         zs, hs, states = [], [], []
         for i in range(len(lens)):
             a, b = offs[i], offs[i + 1]
-            z, h, st = self.prefill_one(h_low[a:b], h_mid[a:b], h_high[a:b])
+            z, h, st = self.prefill_one(h_low[a:b], h_mid[a:b], h_high[a:b],
+                                        tokens=None if tokens is None else tokens[a:b])
             zs.append(z)
             hs.append(h)
             states.append(st)
         hd = np.concatenate(hs, axis=0) if hs else np.zeros((0, self.s.d))
         return np.array(zs), hd, states
 
-    def step(self, states: List[RequestState], h_low, h_mid, h_high):
+    def step(self, states: List[RequestState], h_low, h_mid, h_high, tokens=None):
         """One decode step for every request in ``states`` (rows in order)."""
         zs, hs = [], []
         for i, st in enumerate(states):
-            z, h = self.step_one(st, h_low[i], h_mid[i], h_high[i])
+            z, h = self.step_one(st, h_low[i], h_mid[i], h_high[i],
+                                 None if tokens is None else int(tokens[i]))
             zs.append(z)
             hs.append(h)
         return np.array(zs), (np.stack(hs) if hs else np.zeros((0, self.s.d)))

@@ -40,7 +40,7 @@ KERNELS = ["META", "FUSE_GEMM", "NORM", "QKV_GEMM", "ROPE_KV", "ATTN", "O_GEMM",
 
 BUF = {name: i for i, name in enumerate(
     ["FUSED", "NORM_ATTN", "Q", "ATTN", "X1", "NORM_MLP", "MLP_ACT", "X2", "HDRAFT",
-     "POOLED", "K_POOL", "V_POOL"])}
+     "POOLED", "K_POOL", "V_POOL", "NORM_EMB"])}
 
 
 class OutletsError(RuntimeError):
@@ -64,7 +64,7 @@ WEIGHT_FIELDS = [
     "w_proj", "s_proj", "w_q", "s_q", "w_k", "s_k", "w_v", "s_v", "w_o", "s_o",
     "w_gate", "s_gate", "w_up", "s_up", "w_down", "s_down", "gamma_attn", "gamma_mlp",
     "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2", "w_attn_gate", "s_attn_gate",
-    "probe_w1", "probe_b1", "probe_w2", "probe_b2", "w_lm", "s_lm",
+    "probe_w1", "probe_b1", "probe_w2", "probe_b2", "w_lm", "s_lm", "embed", "gamma_emb",
 ]
 
 
@@ -79,8 +79,8 @@ _I32P = C.POINTER(C.c_int32)
 _SIGS = {
     "outlets_create": (C.c_int, [C.POINTER(outlets_config), C.POINTER(outlets_weights), C.c_int32, C.POINTER(_P)]),
     "outlets_destroy": (C.c_int, [_P]),
-    "outlets_predict_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
-    "outlets_predict_step": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P]),
+    "outlets_predict_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P, _P]),
+    "outlets_predict_step": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P, _P]),
     "outlets_release": (C.c_int, [_P, C.c_int32, _I32P]),
     "outlets_probe_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, C.c_int64, _P, _P]),
     "outlets_probe_step": (C.c_int, [_P, C.c_int32, _I32P, _P, C.c_int64, _P, _P]),
@@ -149,16 +149,18 @@ def outlets_destroy(ctx) -> None:
 
 
 def outlets_predict_prefill(ctx, slots, lens, h_low: int, h_mid: int, h_high: int, row_stride: int,
-                            z_out: int, hdraft_out: Optional[int], stream: Optional[int]) -> int:
+                            tokens: Optional[int], z_out: int, hdraft_out: Optional[int],
+                            stream: Optional[int]) -> int:
     n = len(slots)
     return lib().outlets_predict_prefill(ctx, n, i32_array(slots), i32_array(lens), h_low, h_mid, h_high,
-                                         row_stride, z_out, hdraft_out, stream)
+                                         row_stride, tokens, z_out, hdraft_out, stream)
 
 
 def outlets_predict_step(ctx, slots, h_low: int, h_mid: int, h_high: int, row_stride: int,
-                         z_out: int, hdraft_out: Optional[int], stream: Optional[int]) -> int:
+                         tokens: Optional[int], z_out: int, hdraft_out: Optional[int],
+                         stream: Optional[int]) -> int:
     return lib().outlets_predict_step(ctx, len(slots), i32_array(slots), h_low, h_mid, h_high, row_stride,
-                                      z_out, hdraft_out, stream)
+                                      tokens, z_out, hdraft_out, stream)
 
 
 def outlets_release(ctx, slots) -> int:

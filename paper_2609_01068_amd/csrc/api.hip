@@ -52,6 +52,9 @@ struct outlets_ctx {
     int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
     bool gated = false;          // Gated Attention: q|k|v|g rows, output gate in attention
     bool probe = false;          // MLP probe weights present
+    bool embed_in = false;       // EAGLE-3 input embeddings: attention reads [emb ; norm(f)] (2d)
+    int64_t k_attn = 0;          // width of the attention block's input row: d or 2d
+    void* e_norm = nullptr;      // [T, d] act: RMSNorm(embed[token]) * gamma_emb
     std::vector<int32_t> probe_count;   // per slot: tokens pooled by the probe (0 = inactive)
     float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
     int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
@@ -194,8 +197,6 @@ int check_config(const outlets_config& c, const char** why) {
     if (c.weight_fmt != OUTLETS_FMT_F32 && c.act_fmt != OUTLETS_FMT_BF16)
         return bad(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 weights need bf16 activations");
     if (c.vocab < 0) return bad(OUTLETS_ERR_INVALID_ARG, "vocab must be >= 0");
-    if (c.vocab > 0 && c.weight_fmt != OUTLETS_FMT_F32 && c.vocab % 256)
-        return bad(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 draft heads need vocab a multiple of 256");
     *why = nullptr;
     return OUTLETS_OK;
 }
@@ -242,8 +243,14 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
     g.a_fuse.p[1] = hm;
     g.a_fuse.p[2] = hh;
     g.b_fuse = gemm_b1(w.w_proj, w.s_proj, d, 3 * d);
-    g.a_qkv = gemm_a(c->a_norm, d, d);
-    g.b_qkv = gemm_b1(w.w_q, w.s_q, c->qdim, d);
+    if (c->embed_in) {
+        // input embeddings: K = 2d over [normed embedding | normed f_ctx]
+        g.a_qkv = gemm_a(c->e_norm, d, d);
+        g.a_qkv.p[1] = c->a_norm;
+    } else {
+        g.a_qkv = gemm_a(c->a_norm, d, d);
+    }
+    g.b_qkv = gemm_b1(w.w_q, w.s_q, c->qdim, c->k_attn);
     g.b_qkv.p[1] = w.w_k;
     g.b_qkv.p[2] = w.w_v;
     g.b_qkv.scale[1] = static_cast<const uint16_t*>(w.s_k);
@@ -294,13 +301,13 @@ int check_gemms(const outlets_ctx* c) {
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
     int rc;
     if ((rc = gemm_check(af, wf, EPI_STORE_F32, 1, c->d, 3 * c->d, g.a_fuse, g.b_fuse, 1, &why)) ||
-        (rc = gemm_check(af, wf, EPI_STORE_ACT, 1, c->qkv_dim, c->d, g.a_qkv, g.b_qkv, 1, &why)) ||
+        (rc = gemm_check(af, wf, EPI_STORE_ACT, 1, c->qkv_dim, c->k_attn, g.a_qkv, g.b_qkv, 1, &why)) ||
         (rc = gemm_check(af, wf, EPI_RESID_F32, 1, c->d, c->qdim, g.a_o, g.b_o, 1, &why)) ||
         (rc = gemm_check(af, wf, EPI_SWIGLU, 1, g.n_gu, c->d, g.a_gu, g.b_gu, 1, &why)) ||
         (rc = gemm_check(af, wf, EPI_RESID_F32, 1, c->d, c->F, g.a_down, g.b_down, 1, &why)) ||
         (rc = gemm_check(af, hf, EPI_PARTIAL, 1, c->H1, 2 * c->d, g.a_head, g.b_head, kHeadSplits, &why)))
         return fail(rc, std::string("unsupported shape: ") + why);
-    if (c->cfg.vocab > 0) {
+    if (c->w.w_lm) {
         const GemmA a = lm_input(c);
         const GemmB b = gemm_b1(c->w.w_lm, c->w.s_lm, c->cfg.vocab, c->d);
         if ((rc = gemm_check(af, wf, EPI_STORE_F32, 1, c->cfg.vocab, c->d, a, b, 1, &why)))
@@ -312,7 +319,8 @@ int check_gemms(const outlets_ctx* c) {
 // Queue the draft layer + head for `T` tokens of `n` requests whose
 // metadata is already on the device.
 int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const void* hm,
-              const void* hh, int64_t row_stride, float* z_out, void* hdraft_out, hipStream_t st) {
+              const void* hh, int64_t row_stride, const int32_t* tokens, float* z_out,
+              void* hdraft_out, hipStream_t st) {
     const int af = c->act_fmt, wf = c->w_fmt;
     const int64_t d = c->d;
     LayerGemms g = layer_gemms(c, hl, hm, hh, row_stride);
@@ -325,9 +333,12 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
     { KTimer t(c, OUTLETS_K_FUSE_GEMM, st);
       gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, c->r_f, d, c->w.gamma_attn, eps, c->a_norm, d, nullptr, 0, st); }
+      launch_rmsnorm(af, c->small_fmt, T, d, c->r_f, d, c->w.gamma_attn, eps, c->a_norm, d, nullptr, 0, st);
+      if (c->embed_in)
+          launch_embed_norm(af, c->small_fmt, T, static_cast<int>(d), c->cfg.vocab, tokens, c->w.embed,
+                            c->w.gamma_emb, eps, c->e_norm, d, st); }
     { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, d, g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
+      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_ROPE_KV, st);
       launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
                      c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
@@ -432,8 +443,9 @@ std::vector<int32_t> attention_work(int n, const int32_t* lens, int qt) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 int check_states(const outlets_ctx* c, const void* hl, const void* hm, const void* hh,
-                 int64_t row_stride, const float* z_out) {
+                 int64_t row_stride, const int32_t* tokens, const float* z_out) {
     if (!hl || !hm || !hh || !z_out) return fail(OUTLETS_ERR_INVALID_ARG, "null state or output pointer");
+    if (c->embed_in && !tokens) return fail(OUTLETS_ERR_INVALID_ARG, "input embeddings need token ids");
     if (row_stride < c->d) return fail(OUTLETS_ERR_INVALID_ARG, "row_stride < d_model");
     if (c->act_fmt == FMT_BF16 && (row_stride % 8 || !aligned16(hl) || !aligned16(hm) || !aligned16(hh)))
         return fail(OUTLETS_ERR_UNSUPPORTED, "bf16 states need 16-byte aligned rows (row_stride % 8 == 0)");
@@ -460,10 +472,14 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
                          w.head_w2, w.head_b2};
     for (const void* p : req)
         if (!p) return fail(OUTLETS_ERR_INVALID_ARG, "a weight pointer is null");
-    if ((cfg->vocab > 0) != (w.w_lm != nullptr))
-        return fail(OUTLETS_ERR_INVALID_ARG, "w_lm must be given exactly when vocab > 0");
-    if (cfg->vocab > 0 && cfg->weight_fmt == OUTLETS_FMT_E4M3 && !w.s_lm)
+    if ((w.embed != nullptr) != (w.gamma_emb != nullptr))
+        return fail(OUTLETS_ERR_INVALID_ARG, "input embeddings need embed and gamma_emb");
+    if ((cfg->vocab > 0) != (w.w_lm != nullptr || w.embed != nullptr))
+        return fail(OUTLETS_ERR_INVALID_ARG, "vocab > 0 exactly when w_lm or embed is given");
+    if (w.w_lm && cfg->weight_fmt == OUTLETS_FMT_E4M3 && !w.s_lm)
         return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
+    if (w.w_lm && cfg->weight_fmt != OUTLETS_FMT_F32 && cfg->vocab % 256)
+        return fail(OUTLETS_ERR_UNSUPPORTED, "bf16/e4m3 draft heads need vocab a multiple of 256");
     if (w.probe_w1 && (!w.probe_b1 || !w.probe_w2 || !w.probe_b2))
         return fail(OUTLETS_ERR_INVALID_ARG, "probe weights need w1, b1, w2 and b2");
     if (cfg->weight_fmt == OUTLETS_FMT_E4M3) {
@@ -494,6 +510,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     c->gated = w.w_attn_gate != nullptr;
     c->probe = w.probe_w1 != nullptr;
     c->qkv_dim = c->qdim + 2 * c->kvdim + (c->gated ? c->qdim : 0);
+    c->embed_in = w.embed != nullptr;
+    c->k_attn = (c->embed_in ? 2 : 1) * c->d;
     c->F = cfg->ffn_dim;
     c->H1 = cfg->head_hidden;
     c->max_pages = c->pager->max_pages_per_seq();
@@ -524,6 +542,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         c->r_x1 = c->r_x2 = c->r_h = c->r_f;
     }
     ALLOC(c->a_norm, ab * Tm * c->d);
+    if (c->embed_in) ALLOC(c->e_norm, ab * Tm * c->d);
     if (keep) ALLOC(c->b_norm, ab * Tm * c->d);
     else c->b_norm = c->a_norm;
     ALLOC(c->qkv, ab * Tm * c->qkv_dim);
@@ -542,7 +561,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
     {
         // split-K scratch: the largest plan over the layer's GEMMs for M up to 1024
-        const int64_t gemm_nk[5][2] = {{c->d, 3 * c->d}, {c->qkv_dim, c->d}, {c->d, c->qdim},
+        const int64_t gemm_nk[5][2] = {{c->d, 3 * c->d}, {c->qkv_dim, c->k_attn}, {c->d, c->qdim},
                                        {(c->w_fmt == FMT_F32 ? 1 : 2) * c->F, c->d}, {c->d, c->F}};
         const int epis[5] = {EPI_STORE_F32, EPI_STORE_ACT, EPI_RESID_F32, EPI_SWIGLU, EPI_RESID_F32};
         size_t need = 0;
@@ -560,7 +579,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         if (need) ALLOC(c->splitk_ws, need);
     }
     ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
-    if (cfg->vocab > 0) ALLOC(c->lm_logits, sizeof(float) * 2 * Bm * cfg->vocab);
+    if (w.w_lm) ALLOC(c->lm_logits, sizeof(float) * 2 * Bm * cfg->vocab);
     if (c->probe) {
         ALLOC(c->probe_sum, sizeof(float) * cfg->max_slots * c->d);
         ALLOC(c->probe_meta, sizeof(int32_t) * c->meta_cap);
@@ -607,14 +626,14 @@ int outlets_destroy(outlets_ctx* ctx) {
 
 int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
                             const int32_t* lens, const void* h_low, const void* h_mid,
-                            const void* h_high, int64_t row_stride, float* z_out,
-                            void* hdraft_out, void* stream) {
+                            const void* h_high, int64_t row_stride, const int32_t* tokens,
+                            float* z_out, void* hdraft_out, void* stream) {
     if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
     if (n_req < 0 || n_req > ctx->cfg.max_batch_requests)
         return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
     if (n_req == 0) return OUTLETS_OK;
     if (!slots || !lens) return fail(OUTLETS_ERR_INVALID_ARG, "null slots or lens");
-    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, z_out);
+    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, tokens, z_out);
     if (rc) return rc;
     if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
         return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
@@ -644,8 +663,8 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
     rc = upload_meta(ctx, n_req, off, slots, start, updates, work, cu_tiles, st);
     if (rc == OUTLETS_OK)
-        rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, z_out,
-                       hdraft_out, st);
+        rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, tokens,
+                       z_out, hdraft_out, st);
     if (rc) {
         std::string msg = g_err;
         ctx->pager->release(n_req, slots, &why);
@@ -657,14 +676,14 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
 }
 
 int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h_low,
-                         const void* h_mid, const void* h_high, int64_t row_stride, float* z_out,
-                         void* hdraft_out, void* stream) {
+                         const void* h_mid, const void* h_high, int64_t row_stride,
+                         const int32_t* tokens, float* z_out, void* hdraft_out, void* stream) {
     if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
     if (n_req < 0 || n_req > ctx->cfg.max_batch_requests || n_req > ctx->cfg.max_batch_tokens)
         return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
     if (n_req == 0) return OUTLETS_OK;
     if (!slots) return fail(OUTLETS_ERR_INVALID_ARG, "null slots");
-    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, z_out);
+    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, tokens, z_out);
     if (rc) return rc;
     if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
         return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
@@ -693,7 +712,8 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     }
     rc = upload_meta(ctx, n_req, off, slots, start, updates, dwork, cu_chunks, st);
     if (rc == OUTLETS_OK)
-        rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, z_out, hdraft_out, st);
+        rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, tokens, z_out,
+                       hdraft_out, st);
     if (rc) return rc;   // device work may be partly queued; the slot lengths advanced
     ctx->last_n = n_req;
     ctx->last_T = n_req;
@@ -830,7 +850,7 @@ int outlets_probe_release(outlets_ctx* ctx, int32_t n, const int32_t* slots) {
 
 int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, void* stream) {
     if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
-    if (ctx->cfg.vocab <= 0) return fail(OUTLETS_ERR_UNSUPPORTED, "the context has no draft model head (vocab 0)");
+    if (!ctx->w.w_lm) return fail(OUTLETS_ERR_UNSUPPORTED, "the context has no draft model head (no w_lm)");
     if (n_req <= 0 || n_req != ctx->last_n)
         return fail(OUTLETS_ERR_INVALID_ARG, "n_req must equal the last predict call's request count");
     if (!p_out) return fail(OUTLETS_ERR_INVALID_ARG, "null p_out");
@@ -904,6 +924,9 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
         case OUTLETS_BUF_X2: src = ctx->r_x2; size = 4 * T * d; break;
         case OUTLETS_BUF_HDRAFT: src = ctx->r_h; size = 4 * T * d; needs_keep = false; break;
         case OUTLETS_BUF_POOLED: src = ctx->pooled; size = 4 * n * 2 * d; needs_keep = false; break;
+        case OUTLETS_BUF_NORM_EMB:
+            if (!ctx->embed_in) return fail(OUTLETS_ERR_INVALID_ARG, "the context has no input embeddings");
+            src = ctx->e_norm; size = ab * T * d; break;
         case OUTLETS_BUF_K_POOL:
         case OUTLETS_BUF_V_POOL:
             src = which == OUTLETS_BUF_K_POOL ? ctx->kpool : ctx->vpool;

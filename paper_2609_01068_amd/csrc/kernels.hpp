@@ -79,6 +79,13 @@ void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x,
                     const void* gamma, float eps, void* y, int64_t ldy, float* y2,
                     int64_t ldy2, hipStream_t st);
 
+// EAGLE-3 input embeddings: y[r] = RMSNorm(embed[tok[r]]) * gamma for `rows`
+// token ids; embed [vocab, d] and y in act format, gamma in gamma_fmt.  Ids
+// outside [0, vocab) give zero rows.
+void launch_embed_norm(int act_fmt, int gamma_fmt, int rows, int d, int vocab, const int32_t* tok,
+                       const void* embed, const void* gamma, float eps, void* y, int64_t ldy,
+                       hipStream_t st);
+
 // RoPE on q (in place) and k; k, v scattered into the page pools.
 void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t* tok_slot,
                     const int32_t* tok_pos, const int32_t* page_table, int max_pages,

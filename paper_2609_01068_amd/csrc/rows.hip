@@ -97,6 +97,67 @@ rmsnorm_vec_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float ep
     }
 }
 
+// EAGLE-3 input embeddings: y[r] = RMSNorm(embed[tok[r]]) * gamma, one
+// 256-thread block per row.  An id outside [0, vocab) reads nothing and
+// gives a zero row.  V > 0: bf16 rows with d = 1024 V, four elements per
+// thread and step (8-byte loads and stores); V = 0: any d and format.
+template <typename TE, typename TG, int V>
+__global__ void __launch_bounds__(256)
+embed_norm_kernel(int d, int vocab, const int32_t* tok, const TE* embed, const TG* gamma, float eps,
+                  TE* y, int64_t ldy) {
+    __shared__ float red[4];
+    const int64_t row = blockIdx.x;
+    const int t = threadIdx.x;
+    const int id = tok[row];
+    const bool ok = id >= 0 && id < vocab;
+    const TE* er = embed + (int64_t)(ok ? id : 0) * d;
+    TE* yr = y + row * ldy;
+    if constexpr (V > 0) {
+        float v[V][4];
+        float ss = 0.f;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            const uint2 u = ok ? reinterpret_cast<const uint2*>(er)[j * 256 + t] : make_uint2(0u, 0u);
+            v[j][0] = __uint_as_float(u.x << 16); v[j][1] = __uint_as_float(u.x & 0xffff0000u);
+            v[j][2] = __uint_as_float(u.y << 16); v[j][3] = __uint_as_float(u.y & 0xffff0000u);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ss = fmaf(v[j][e], v[j][e], ss);
+        }
+        ss = block_sum<256>(ss, red);
+        const float inv = ok ? 1.0f / sqrtf(ss / d + eps) : 0.f;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            const int c = (j * 256 + t) * 4;
+            float g[4];
+            if constexpr (sizeof(TG) == 4) {
+                const float4 gv = *reinterpret_cast<const float4*>(gamma + c);
+                g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
+            } else {
+                const uint2 gv = *reinterpret_cast<const uint2*>(gamma + c);
+                g[0] = __uint_as_float(gv.x << 16); g[1] = __uint_as_float(gv.x & 0xffff0000u);
+                g[2] = __uint_as_float(gv.y << 16); g[3] = __uint_as_float(gv.y & 0xffff0000u);
+            }
+            uint2 pk;
+            pk.x = f32_to_bf16(v[j][0] * inv * g[0]) | (uint32_t(f32_to_bf16(v[j][1] * inv * g[1])) << 16);
+            pk.y = f32_to_bf16(v[j][2] * inv * g[2]) | (uint32_t(f32_to_bf16(v[j][3] * inv * g[3])) << 16);
+            *reinterpret_cast<uint2*>(yr + c) = pk;
+        }
+    } else {
+        float ss = 0.f;
+        if (ok)
+            for (int c = t; c < d; c += 256) {
+                const float x = load_act<TE>(er + c);
+                ss = fmaf(x, x, ss);
+            }
+        ss = block_sum<256>(ss, red);
+        const float inv = ok ? 1.0f / sqrtf(ss / d + eps) : 0.f;
+        for (int c = t; c < d; c += 256) {
+            const float x = ok ? load_act<TE>(er + c) : 0.f;
+            store_act<TE>(yr + c, x * inv * load_act<TG>(gamma + c));
+        }
+    }
+}
+
 // One block per token; thread work items are rotation pairs of the q and k
 // heads and value elements.
 template <typename T>
@@ -343,6 +404,39 @@ scalar:
         hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(rows), dim3(256), 0, st, d, x, ldx,
                            static_cast<const bf16_t*>(gamma), eps, static_cast<bf16_t*>(y), ldy, y2, ldy2);
     }
+}
+
+void launch_embed_norm(int act_fmt, int gamma_fmt, int rows, int d, int vocab, const int32_t* tok,
+                       const void* embed, const void* gamma, float eps, void* y, int64_t ldy,
+                       hipStream_t st) {
+    if (rows <= 0) return;
+    const dim3 grid(rows), blk(256);
+    if (act_fmt == FMT_F32) {
+        hipLaunchKernelGGL((embed_norm_kernel<float, float, 0>), grid, blk, 0, st, d, vocab, tok,
+                           static_cast<const float*>(embed), static_cast<const float*>(gamma), eps,
+                           static_cast<float*>(y), ldy);
+        return;
+    }
+    const bool vec = d % 1024 == 0 && d <= 8192 && ldy % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(embed) % 8 == 0 && reinterpret_cast<uintptr_t>(y) % 8 == 0 &&
+                     reinterpret_cast<uintptr_t>(gamma) % 16 == 0;
+    const int V = vec ? d / 1024 : 0;
+#define OUTLETS_EMB(TG, VV)                                                                        \
+    hipLaunchKernelGGL((embed_norm_kernel<bf16_t, TG, VV>), grid, blk, 0, st, d, vocab, tok,      \
+                       static_cast<const bf16_t*>(embed), static_cast<const TG*>(gamma), eps,     \
+                       static_cast<bf16_t*>(y), ldy)
+#define OUTLETS_EMB_G(TG)                                       \
+    switch (V) {                                                \
+        case 1: OUTLETS_EMB(TG, 1); break;                      \
+        case 2: OUTLETS_EMB(TG, 2); break;                      \
+        case 4: OUTLETS_EMB(TG, 4); break;                      \
+        case 8: OUTLETS_EMB(TG, 8); break;                      \
+        default: OUTLETS_EMB(TG, 0); break;                     \
+    }
+    if (gamma_fmt == FMT_F32) { OUTLETS_EMB_G(float) }
+    else { OUTLETS_EMB_G(bf16_t) }
+#undef OUTLETS_EMB_G
+#undef OUTLETS_EMB
 }
 
 void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t* tok_slot,

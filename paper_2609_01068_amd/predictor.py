@@ -19,6 +19,7 @@ BIG_LINEARS = ("w_proj", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
 SMALL = ("gamma_attn", "gamma_mlp", "gamma_final", "head_w1", "head_b1", "head_w2", "head_b2")
 GATE_NAME = "w_attn_gate"    # optional Gated Attention output-gate projection
 PROBE = ("probe_w1", "probe_b1", "probe_w2", "probe_b2")   # optional MLP-probe baseline
+EMBED = ("embed", "gamma_emb")   # optional EAGLE-3 input embeddings
 
 
 def to_device(arr, device="cuda") -> torch.Tensor:
@@ -38,6 +39,14 @@ def to_device(arr, device="cuda") -> torch.Tensor:
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
+
+
+def _tokens_ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous():
+        raise TypeError("token ids must be a contiguous int32 device tensor")
+    return t.data_ptr()
 
 
 def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
@@ -91,6 +100,13 @@ class OutletsPredictor:
                 self.tensors["w_lm"] = to_device(entry, self.device)
             w.w_lm = _ptr(self.tensors["w_lm"])
             self.vocab = int(shape.vocab)
+        self.input_embed = weights.get("embed") is not None
+        for name in EMBED:                               # EAGLE-3 input embeddings
+            if weights.get(name) is not None:            # (the library checks both are given)
+                self.tensors[name] = to_device(weights[name], self.device)
+                setattr(w, name, _ptr(self.tensors[name]))
+        if self.input_embed:
+            self.vocab = int(shape.vocab)
         if weights.get("probe_w1") is not None:          # MLP-probe baseline
             for name in PROBE:
                 self.tensors[name] = to_device(weights[name], self.device)
@@ -113,7 +129,9 @@ class OutletsPredictor:
     def prefill(self, slots: Sequence[int], lens: Sequence[int], h_low: torch.Tensor,
                 h_mid: torch.Tensor, h_high: torch.Tensor, row_stride: Optional[int] = None,
                 want_hdraft: bool = False, z_out: Optional[torch.Tensor] = None,
-                hdraft_out: Optional[torch.Tensor] = None, stream=None):
+                hdraft_out: Optional[torch.Tensor] = None, stream=None,
+                tokens: Optional[torch.Tensor] = None):
+        """``tokens``: device int32 [T] ids paired with the rows (input embeddings)."""
         n, T = len(slots), int(sum(int(x) for x in lens))
         if z_out is None:
             z_out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
@@ -121,15 +139,15 @@ class OutletsPredictor:
             hdraft_out = torch.empty((max(T, 1), self.shape.d), dtype=self.act_dtype, device=self.device)
         stride = h_low.stride(0) if row_stride is None else row_stride
         rc = B.outlets_predict_prefill(self.ctx, list(slots), list(lens), h_low.data_ptr(), h_mid.data_ptr(),
-                                       h_high.data_ptr(), stride, z_out.data_ptr(), _ptr(hdraft_out),
-                                       _stream_ptr(stream))
+                                       h_high.data_ptr(), stride, _tokens_ptr(tokens), z_out.data_ptr(),
+                                       _ptr(hdraft_out), _stream_ptr(stream))
         B.check(rc, "outlets_predict_prefill")
         return z_out[:n], (hdraft_out[:T] if hdraft_out is not None else None)
 
     def step(self, slots: Sequence[int], h_low: torch.Tensor, h_mid: torch.Tensor,
              h_high: torch.Tensor, row_stride: Optional[int] = None, want_hdraft: bool = False,
              z_out: Optional[torch.Tensor] = None, hdraft_out: Optional[torch.Tensor] = None,
-             stream=None):
+             stream=None, tokens: Optional[torch.Tensor] = None):
         n = len(slots)
         if z_out is None:
             z_out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
@@ -137,8 +155,8 @@ class OutletsPredictor:
             hdraft_out = torch.empty((max(n, 1), self.shape.d), dtype=self.act_dtype, device=self.device)
         stride = h_low.stride(0) if row_stride is None else row_stride
         rc = B.outlets_predict_step(self.ctx, list(slots), h_low.data_ptr(), h_mid.data_ptr(),
-                                    h_high.data_ptr(), stride, z_out.data_ptr(), _ptr(hdraft_out),
-                                    _stream_ptr(stream))
+                                    h_high.data_ptr(), stride, _tokens_ptr(tokens), z_out.data_ptr(),
+                                    _ptr(hdraft_out), _stream_ptr(stream))
         B.check(rc, "outlets_predict_step")
         return z_out[:n], (hdraft_out[:n] if hdraft_out is not None else None)
 

@@ -34,7 +34,8 @@ __all__ = [
     "DraftShape", "Workload", "WORKLOADS", "workload", "to_bf16_bits",
     "encode_e4m3", "make_weights", "make_lengths", "make_prompt_states",
     "make_step_states", "device_states", "WEIGHT_NAMES", "BIG_LINEARS", "GATE_NAME",
-    "make_probe_weights", "make_lm_weights",
+    "make_probe_weights", "make_lm_weights", "make_embed_weights", "make_prompt_tokens",
+    "make_step_tokens",
 ]
 
 # Linear layers of the draft backbone, the ones stored as e4m3 in the 70B
@@ -95,6 +96,7 @@ class Workload:
     steps: int = 0             # decode steps (re-prediction) after the prefill
     page_size: int = 16
     attn_gate: bool = False    # Gated Attention output gate in the draft layer
+    input_embed: bool = False  # EAGLE-3 input embeddings: attention reads [emb ; f_ctx] (2d)
 
     @property
     def max_len(self) -> int:
@@ -175,6 +177,10 @@ def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
     are ``(codes uint8, scale_bits uint16)`` tuples and the rest bf16 bits.
     ``out['_fmt']`` records the format of each entry."""
     shapes = wl.shape.weight_shapes()
+    if wl.input_embed:
+        # the attention projections read [normed embedding ; normed f_ctx]
+        for name in ("w_q", "w_k", "w_v", GATE_NAME):
+            shapes[name] = (shapes[name][0], 2 * wl.shape.d)
     out: Dict[str, object] = {}
     fmt: Dict[str, str] = {}
     names = list(enumerate(WEIGHT_NAMES))
@@ -195,6 +201,10 @@ def make_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
         else:
             out[name], fmt[name] = to_bf16_bits(x), "bf16"
         del x
+    if wl.input_embed:
+        emb = make_embed_weights(wl, seed)
+        fmt.update(emb.pop("_fmt"))
+        out.update(emb)
     out["_fmt"] = fmt
     return out
 
@@ -231,6 +241,38 @@ def make_lm_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
     if wl.weight_fmt == "e4m3":
         return {"w_lm": encode_e4m3(x), "_fmt": {"w_lm": "e4m3"}}
     return {"w_lm": to_bf16_bits(x), "_fmt": {"w_lm": "bf16"}}
+
+
+def make_embed_weights(wl: Workload, seed: int = 0) -> Dict[str, object]:
+    """The target model's (frozen) token embedding table ``embed`` [vocab, d]
+    (N(0, 0.02^2), activation format) and the draft layer's RMSNorm gain for
+    it, ``gamma_emb`` [d] (1 + 0.02 N(0, 1), small-weight format), for the
+    EAGLE-3 input-embedding concat.  Streams follow the draft head's."""
+    v, d = wl.shape.vocab, wl.shape.d
+    e = np.float32(0.02) * _rng(seed, wl.cfg_id, len(WEIGHT_NAMES) + 6).standard_normal((v, d), dtype=np.float32)
+    g = np.float32(1.0) + np.float32(0.02) * _rng(seed, wl.cfg_id, len(WEIGHT_NAMES) + 7).standard_normal(d, dtype=np.float32)
+    if wl.act_fmt == "f32":
+        return {"embed": e, "gamma_emb": g, "_fmt": {"embed": "f32", "gamma_emb": "f32"}}
+    return {"embed": to_bf16_bits(e), "gamma_emb": to_bf16_bits(g), "_fmt": {"embed": "bf16", "gamma_emb": "bf16"}}
+
+
+def make_prompt_tokens(wl: Workload, lengths, seed: int = 0,
+                       requests: Optional[List[int]] = None) -> np.ndarray:
+    """Prompt token ids (int32, uniform over the vocabulary), packed like
+    make_prompt_states; request ``i`` draws from its own generator."""
+    lengths = np.asarray(lengths)
+    idx = range(len(lengths)) if requests is None else requests
+    parts = [_rng(seed, wl.cfg_id, 500, int(i)).integers(0, wl.shape.vocab, int(lengths[i]))
+             for i in idx]
+    return (np.concatenate(parts) if parts else np.zeros(0)).astype(np.int32)
+
+
+def make_step_tokens(wl: Workload, n_req: int, step: int, seed: int = 0,
+                     requests: Optional[List[int]] = None) -> np.ndarray:
+    """Token ids generated at decode step ``step``, one per request."""
+    idx = range(n_req) if requests is None else requests
+    return np.array([_rng(seed, wl.cfg_id, 501, step * 1_000_003 + int(i)).integers(0, wl.shape.vocab)
+                     for i in idx], dtype=np.int32)
 
 
 def make_lengths(wl: Workload, seed: int = 0, n_req: Optional[int] = None) -> np.ndarray:

@@ -4,12 +4,13 @@ from __future__ import annotations
 
 import dataclasses
 import sys
+from typing import Optional
 
 import numpy as np
 import pytest
 
-from synth import (DraftShape, make_lengths, make_prompt_states, make_step_states,
-                   make_weights, workload)
+from synth import (DraftShape, make_lengths, make_prompt_states, make_prompt_tokens,
+                   make_step_states, make_step_tokens, make_weights, workload)
 from oracle import oracle_from_workload, states_to_f64
 
 # Tolerances: draft states as a relative Frobenius error per request, the
@@ -54,6 +55,7 @@ class Case:
     lens: np.ndarray
     states: list            # stored (low, mid, high) packed
     fmt: str
+    tokens: Optional[np.ndarray] = None    # packed int32 token ids (input embeddings)
 
 
 def make_case(cfg_id: int, lens=None, seed: int = 0, **overrides) -> Case:
@@ -63,7 +65,8 @@ def make_case(cfg_id: int, lens=None, seed: int = 0, **overrides) -> Case:
         lens = make_lengths(wl, seed)
     lens = np.asarray(lens, dtype=np.int32)
     st = make_prompt_states(wl, lens, seed)
-    return Case(wl, W, lens, st, wl.weight_fmt)
+    tok = make_prompt_tokens(wl, lens, seed) if wl.input_embed else None
+    return Case(wl, W, lens, st, wl.weight_fmt, tok)
 
 
 def make_predictor(case: Case, *, max_slots=None, num_pages=None, max_seq_len=None,
@@ -98,6 +101,20 @@ def oracle_states(case: Case, arrays=None):
 
 def step_inputs(case: Case, step: int, requests=None):
     return make_step_states(case.wl, len(case.lens), step, requests=requests)
+
+
+def step_tokens(case: Case, step: int, requests=None):
+    """Token ids of decode step ``step`` (None without input embeddings)."""
+    if not case.wl.input_embed:
+        return None
+    return make_step_tokens(case.wl, len(case.lens), step, requests=requests)
+
+
+def device_tokens(arr):
+    import torch
+    if arr is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.int32)).cuda()
 
 
 def reduced_shape(d=512, n_q=8, n_kv=2, hd=128, ffn=1024, head_hidden=256, theta=5e5, vocab=1024):

@@ -9,9 +9,9 @@ import numpy as np
 import pytest
 
 from oracle import meta
-from gpu_common import (TOL_HDRAFT, TOL_Z, device_states, make_case, make_predictor, oracle_for,
-                        oracle_states, reduced_shape, rel_fro, require_gpu, say, step_inputs,
-                        tensor_to_f64, z_errors)
+from gpu_common import (TOL_HDRAFT, TOL_Z, device_states, device_tokens, make_case, make_predictor,
+                        oracle_for, oracle_states, reduced_shape, rel_fro, require_gpu, say, step_inputs,
+                        step_tokens, tensor_to_f64, z_errors)
 
 pytestmark = pytest.mark.gpu
 
@@ -46,7 +46,7 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
     slots = list(range(n))
     pred = make_predictor(case, keep=keep, max_seq_len=int(lens.max()) + steps + 16)
     H = device_states(case)
-    z, hd = pred.prefill(slots, lens, *H, want_hdraft=True)
+    z, hd = pred.prefill(slots, lens, *H, want_hdraft=True, tokens=device_tokens(case.tokens))
     z = tensor_to_f64(z)
     hd = tensor_to_f64(hd)
     orc = oracle_for(case)
@@ -56,7 +56,8 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
     caps = []
     for i in range(n):
         cap = {}
-        zi, hi, st = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O), capture=cap)
+        tok = None if case.tokens is None else case.tokens[off[i]:off[i + 1]]
+        zi, hi, st = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O), capture=cap, tokens=tok)
         z_ref.append(zi)
         states.append(st)
         caps.append(cap)
@@ -72,6 +73,8 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
         act = pred.act_dtype
         names += [("NORM_ATTN", "norm_attn", act), ("Q", "q", act), ("ATTN", "attn", act),
                   ("NORM_MLP", "norm_mlp", act), ("MLP_ACT", "mlp_act", act)]
+        if case.tokens is not None:
+            names.append(("NORM_EMB", "norm_emb", act))
         for buf, key, dt in names:
             g = tensor_to_f64(pred.buffer(buf, dt))
             g = g.reshape(int(lens.sum()), -1)
@@ -86,10 +89,10 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
     _check_meta(pred, lens, np.array(slots), alloc)
 
     for t in range(1, steps + 1):
-        S = step_inputs(case, t)
-        zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True)
+        S, tk = step_inputs(case, t), step_tokens(case, t)
+        zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True, tokens=device_tokens(tk))
         zs, hs = tensor_to_f64(zs), tensor_to_f64(hs)
-        zr, hr = orc.step(states, *oracle_states(case, S))
+        zr, hr = orc.step(states, *oracle_states(case, S), tokens=tk)
         for i in range(n):
             assert rel_fro(hs[i], hr[i]) <= TOL_HDRAFT[fmt], (t, i)
         ez = z_errors(zs, zr)
@@ -127,32 +130,35 @@ def test_bf16_head_dim_64_shape():
     _run_prefill_case(case, keep=True, steps=1)
 
 
-@pytest.mark.parametrize("gated", [False, True], ids=["plain", "gated"])
-def test_config1_full_shape_sampled_requests(gated):
+@pytest.mark.parametrize("variant", ["plain", "gated", "embed"])
+def test_config1_full_shape_sampled_requests(variant):
     """8B shape, the 32-request lognormal batch (also with the Gated Attention
-    output gate); the oracle recomputes a sample."""
-    case = make_case(1, attn_gate=gated)
+    output gate, and with EAGLE-3 input embeddings over the 128,256-entry
+    vocabulary); the oracle recomputes a sample."""
+    case = make_case(1, attn_gate=variant == "gated", input_embed=variant == "embed")
     lens = case.lens
-    say(f"case: config-1 8B bf16{' gated attention' if gated else ''}, B={len(lens)}, "
-        f"T={int(lens.sum())}, sampled oracle")
+    say(f"case: config-1 8B bf16 ({variant}), B={len(lens)}, T={int(lens.sum())}, sampled oracle")
     pred = make_predictor(case)
     H = device_states(case)
-    z, hd = pred.prefill(list(range(len(lens))), lens, *H, want_hdraft=True)
+    z, hd = pred.prefill(list(range(len(lens))), lens, *H, want_hdraft=True,
+                         tokens=device_tokens(case.tokens))
     z = tensor_to_f64(z)
     assert np.all(np.isfinite(z))
     order = np.argsort(lens)
     sample = [int(order[0]), int(order[1]), int(order[len(order) // 3])]
     orc = oracle_for(case)
     off = np.concatenate([[0], np.cumsum(lens)])
-    from synth import make_prompt_states
+    from synth import make_prompt_states, make_prompt_tokens
     sub = make_prompt_states(case.wl, lens, requests=sample)
+    sub_tok = make_prompt_tokens(case.wl, lens, requests=sample) if case.tokens is not None else None
     O = oracle_states(case, sub)
     z_ref = []
     o_off = 0
     hd64 = None
     for i in sample:
         n = int(lens[i])
-        zi, hi, _ = orc.prefill_one(*(x[o_off:o_off + n] for x in O))
+        tok = None if sub_tok is None else sub_tok[o_off:o_off + n]
+        zi, hi, _ = orc.prefill_one(*(x[o_off:o_off + n] for x in O), tokens=tok)
         o_off += n
         z_ref.append(zi)
         hd64 = tensor_to_f64(hd[off[i]:off[i + 1]])
@@ -469,3 +475,76 @@ def test_config1_draft_head_sampled_requests():
         err = _check_distribution(p[i], hi[-1], w_lm, "bf16", ("request", i))
         say(f"  request {i} (n={n}) distribution rel err {err:.3e}")
     pred.close()
+
+
+# ------------------------------------------------------------- input embeddings
+
+def test_input_embeddings_tiny_fp32_intermediates_and_steps():
+    say("case: input embeddings, tiny fp32 shape (V=512), 4 requests U[16,64], 6 steps")
+    _run_prefill_case(make_case(0, input_embed=True), keep=True, steps=6)
+
+
+def test_input_embeddings_bf16_reduced_shape_and_steps():
+    say("case: input embeddings, bf16 d=512 8q/2kv hd128 V=1024, lens [1,17,100,300,33], 3 steps")
+    case = make_case(1, lens=[1, 17, 100, 300, 33], shape=reduced_shape(), n_req=5, input_embed=True)
+    _run_prefill_case(case, keep=True, steps=3)
+
+
+def test_input_embeddings_e4m3_gated_reduced_shape_and_steps():
+    say("case: input embeddings + Gated Attention, e4m3 weights d=512 16q/2kv hd128, lens [5,64,257,16], 2 steps")
+    case = make_case(4, lens=[5, 64, 257, 16], shape=reduced_shape(n_q=16, n_kv=2), n_req=4,
+                     attn_gate=True, input_embed=True)
+    _run_prefill_case(case, keep=True, steps=2)
+
+
+def test_input_embeddings_odd_width_scalar_path():
+    say("case: input embeddings, bf16 d=256 4q/4kv hd64 (non-vector gather), lens [3,40,90], 1 step")
+    case = make_case(1, lens=[3, 40, 90], shape=reduced_shape(d=256, n_q=4, n_kv=4, hd=64, ffn=512,
+                                                             head_hidden=256), n_req=3, input_embed=True)
+    _run_prefill_case(case, keep=True, steps=1)
+
+
+def test_input_embeddings_out_of_range_ids_read_a_zero_row():
+    """Ids outside [0, V) cannot be reported from the device: they take a zero
+    embedding row (checked against the oracle with an appended zero row)."""
+    import torch
+    case = make_case(1, lens=[7, 20], shape=reduced_shape(), n_req=2, input_embed=True)
+    V = case.wl.shape.vocab
+    tok = case.tokens.copy()
+    tok[[0, 3, 9, 26]] = [-1, V, -(2 ** 31), 2 ** 31 - 1]
+    say(f"case: input embeddings with out-of-range ids {tok[[0, 3, 9, 26]].tolist()}, V={V}")
+    pred = make_predictor(case, keep=True)
+    z, hd = pred.prefill([0, 1], case.lens, *device_states(case), want_hdraft=True, tokens=device_tokens(tok))
+    hd, z = tensor_to_f64(hd), tensor_to_f64(z)
+    e = tensor_to_f64(pred.buffer("NORM_EMB", torch.bfloat16)).reshape(len(tok), -1)
+    assert np.all(e[[0, 3, 9, 26]] == 0.0)
+    orc = oracle_for(case)
+    orc.w["embed"] = np.vstack([orc.w["embed"], np.zeros((1, case.wl.shape.d))])
+    ref_tok = np.where((tok < 0) | (tok >= V), V, tok)
+    O = oracle_states(case)
+    zr, hr, _ = orc.prefill(case.lens, *O, tokens=ref_tok)
+    for i, (a, b) in enumerate([(0, 7), (7, 27)]):
+        assert rel_fro(hd[a:b], hr[a:b]) <= TOL_HDRAFT["bf16"], i
+    assert z_errors(z, zr).max() <= TOL_Z["bf16"]
+    pred.close()
+
+
+def test_input_embeddings_need_token_ids_and_weights():
+    from paper_2609_01068_amd import binding as B
+    case = make_case(1, lens=[4], shape=reduced_shape(), n_req=1, input_embed=True)
+    say("case: input-embedding argument errors")
+    pred = make_predictor(case)
+    H = device_states(case)
+    with pytest.raises(B.OutletsError) as ei:
+        pred.prefill([0], case.lens, *H)                   # no token ids
+    assert ei.value.rc == B.OUTLETS_ERR_INVALID_ARG
+    z, _ = pred.prefill([0], case.lens, *H, tokens=device_tokens(case.tokens))   # state unchanged
+    assert np.isfinite(tensor_to_f64(z)).all()
+    pred.close()
+    W = dict(case.weights)
+    W.pop("gamma_emb")
+    bad = make_case(1, lens=[4], shape=reduced_shape(), n_req=1, input_embed=True)
+    bad.weights = W
+    with pytest.raises(B.OutletsError) as ei:
+        make_predictor(bad)
+    assert ei.value.rc == B.OUTLETS_ERR_INVALID_ARG

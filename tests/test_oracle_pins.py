@@ -366,6 +366,100 @@ def test_gate_is_absent_without_gate_weights():
                        rtol=1e-12, atol=1e-12)
 
 
+# ------------------------------------------------------------- input embeddings
+
+VOCAB = 23
+
+
+def _embed_model(seed=41, gated=False):
+    """SMALL model with EAGLE-3 input embeddings: Q/K/V (and gate) over 2d."""
+    W = _gated_model(seed) if gated else rand_weights(SMALL, seed=seed)
+    r = np.random.default_rng(seed + 1)
+    for k in ("w_q", "w_k", "w_v") + (("w_attn_gate",) if gated else ()):
+        W[k] = np.concatenate([r.standard_normal(W[k].shape) * 0.3, W[k]], axis=1)
+    W["embed"] = r.standard_normal((VOCAB, SMALL.d)) * 0.5
+    W["gamma_emb"] = 1 + r.standard_normal(SMALL.d) * 0.3
+    return W
+
+
+def _check_embed_layer(gated=False):
+    # torch's own rms_norm of the gathered embedding rows and of f_ctx,
+    # concatenated embedding-first, must give the oracle's values (v has no
+    # RoPE; q at position 0 is unrotated) and, when gated, its gate input
+    import torch.nn.functional as F
+    n = 11
+    hl, hm, hh = rand_states(n, SMALL.d, 42)
+    tok = np.random.default_rng(43).integers(0, VOCAB, n)
+    W = _embed_model(gated=gated)
+    cap = {}
+    OracleModel(SMALL, W).prefill_one(hl, hm, hh, capture=cap, tokens=tok)
+    t = torch.from_numpy
+    e = F.rms_norm(t(W["embed"])[t(tok)], (SMALL.d,), t(W["gamma_emb"]), SMALL.rms_eps)
+    a = F.rms_norm(t(cap["fused"]), (SMALL.d,), t(W["gamma_attn"]), SMALL.rms_eps)
+    x = torch.cat([e, a], dim=1)
+    assert np.allclose(cap["norm_emb"], e.numpy(), rtol=1e-12, atol=1e-12)
+    v = (x @ t(W["w_v"]).T).reshape(n, SMALL.n_kv, SMALL.head_dim).numpy()
+    assert np.allclose(cap["v"], v, rtol=1e-12, atol=1e-12)
+    q0 = (x[:1] @ t(W["w_q"]).T).numpy()
+    assert np.allclose(cap["q"][:1], q0, rtol=1e-12, atol=1e-12)
+    if gated:
+        q = cap["q"].reshape(n, SMALL.n_q, SMALL.head_dim)
+        o = _sdpa_ref(q, cap["k"], cap["v"], True).reshape(n, -1)
+        gate = torch.sigmoid(x @ t(W["w_attn_gate"]).T).numpy()
+        assert np.allclose(cap["attn"], o * gate, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("gated", [False, True], ids=["plain", "gated"])
+def test_input_embeddings_match_torch_rms_norm_concat(gated):
+    _check_embed_layer(gated)
+
+
+def test_zero_embedding_columns_reduce_to_the_plain_layer():
+    # with the embedding half of Q/K/V zeroed, the tokens cannot matter and the
+    # layer is the plain one over the hidden half
+    hl, hm, hh = rand_states(8, SMALL.d, 44)
+    W = _embed_model()
+    d = SMALL.d
+    for k in ("w_q", "w_k", "w_v"):
+        W[k][:, :d] = 0.0
+    plain = {k: (v[:, d:] if k in ("w_q", "w_k", "w_v") else v) for k, v in W.items()
+             if k not in ("embed", "gamma_emb")}
+    z1, h1, _ = OracleModel(SMALL, W).prefill_one(hl, hm, hh, tokens=np.arange(8) % VOCAB)
+    z2, h2, _ = OracleModel(SMALL, W).prefill_one(hl, hm, hh, tokens=(np.arange(8) * 7 + 3) % VOCAB)
+    z0, h0, _ = OracleModel(SMALL, plain).prefill_one(hl, hm, hh)
+    assert np.allclose(h1, h0, rtol=1e-12, atol=1e-13) and np.allclose(h2, h0, rtol=1e-12, atol=1e-13)
+    assert abs(z1 - z0) <= 1e-12 * max(1.0, abs(z0))
+
+
+def test_embedding_rows_of_unused_tokens_do_not_matter():
+    hl, hm, hh = rand_states(6, SMALL.d, 45)
+    tok = np.array([1, 4, 4, 9, 1, 2])
+    W = _embed_model()
+    z1, h1, _ = OracleModel(SMALL, W).prefill_one(hl, hm, hh, tokens=tok)
+    W2 = dict(W)
+    W2["embed"] = W["embed"].copy()
+    unused = np.setdiff1d(np.arange(VOCAB), tok)
+    W2["embed"][unused] = 123.0
+    z2, h2, _ = OracleModel(SMALL, W2).prefill_one(hl, hm, hh, tokens=tok)
+    assert np.array_equal(h1, h2) and z1 == z2
+    W2["embed"][4] += 1.0                      # a used row changes the result
+    _, h3, _ = OracleModel(SMALL, W2).prefill_one(hl, hm, hh, tokens=tok)
+    assert not np.allclose(h1, h3)
+
+
+def test_input_embedding_steps_equal_prefill_recompute():
+    n0, n1 = 5, 9
+    hl, hm, hh = rand_states(n1, SMALL.d, 46)
+    tok = np.random.default_rng(47).integers(0, VOCAB, n1)
+    m = OracleModel(SMALL, _embed_model())
+    _, _, st = m.prefill_one(hl[:n0], hm[:n0], hh[:n0], tokens=tok[:n0])
+    for t in range(n0, n1):
+        zs, hs = m.step_one(st, hl[t], hm[t], hh[t], token=int(tok[t]))
+        zf, hf, _ = m.prefill_one(hl[:t + 1], hm[:t + 1], hh[:t + 1], tokens=tok[:t + 1])
+        assert np.allclose(hs, hf[-1], rtol=1e-10, atol=1e-12)
+        assert abs(zs - zf) <= 1e-10 * max(1.0, abs(zf))
+
+
 # ------------------------------------------------------------- MLP probe
 
 def _probe_weights(seed=21):
@@ -490,3 +584,18 @@ def test_planted_gate_mistakes_are_caught(monkeypatch, mistake):
         return o * (1.0 - oracle_model.sigmoid(a @ w.T))
     monkeypatch.setattr(oracle_model, "attention_output_gate", wrong)
     assert _fails(_check_gated_layer)
+
+
+@pytest.mark.parametrize("mistake", ["hidden_first", "no_norm", "no_gain"])
+def test_planted_input_embedding_mistakes_are_caught(monkeypatch, mistake):
+    real = oracle_model.embedded_attention_input
+
+    def wrong(emb_rows, gamma_emb, a, eps):
+        if mistake == "hidden_first":
+            e, _ = real(emb_rows, gamma_emb, a, eps)
+            return e, np.concatenate([a, e], axis=1)
+        if mistake == "no_norm":
+            return emb_rows * gamma_emb, np.concatenate([emb_rows * gamma_emb, a], axis=1)
+        return real(emb_rows, np.ones_like(gamma_emb), a, eps)
+    monkeypatch.setattr(oracle_model, "embedded_attention_input", wrong)
+    assert _fails(_check_embed_layer)
