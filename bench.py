@@ -313,6 +313,74 @@ def bench_probe(a):
     return _emit(out)
 
 
+def bench_sched(a):
+    """The control plane that consumes the static prediction (Section 5
+    system evaluation) on the saturation trace: one step = whole-token
+    predictions from z_hat, the LB + SJF decode-cluster simulation of all
+    1,914 requests, and its serving metrics.  Host code only (no GPU)."""
+    import numpy as np
+    from paper_2609_01068_amd import binding as B
+    from synth.serving import PAPER_TRACE as tr, make_trace, noisy_predictions
+
+    arrival, L = make_trace(tr, a.seed)
+    noisy = noisy_predictions(L, 0.25, a.seed)
+    z = np.log1p(noisy.astype(np.float64)).astype(np.float32)
+    cluster = (tr.instances, tr.max_running)
+    it = (tr.iter_base_us, tr.iter_per_seq_us)
+
+    def one_step():
+        p = B.outlets_pred_tokens(z)
+        _, _, fin = B.outlets_sched_simulate(arrival, L, p, *cluster, B.OUTLETS_ROUTE_LB,
+                                             B.OUTLETS_QUEUE_SJF, *it)
+        return B.outlets_sched_metrics(arrival, L, fin)
+
+    for _ in range(a.warmup):
+        one_step()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        one_step()
+    wall = time.perf_counter() - t0
+    ms = wall * 1e3 / a.steps
+
+    def row(routing, order, pred):
+        _, _, fin = B.outlets_sched_simulate(arrival, L, pred, *cluster, routing, order, *it)
+        m = B.outlets_sched_metrics(arrival, L, fin)
+        return {"tokens_per_s": m[0], "mean_latency_s": m[1], "p99_short_s": m[2], "p99_medium_s": m[3],
+                "p99_long_s": m[4], "makespan_s": m[5]}
+    RR, LB, FCFS, SJF = B.OUTLETS_ROUTE_RR, B.OUTLETS_ROUTE_LB, B.OUTLETS_QUEUE_FCFS, B.OUTLETS_QUEUE_SJF
+    p_tok = B.outlets_pred_tokens(z)
+    serving = {
+        "RR+FCFS": row(RR, FCFS, p_tok),
+        "RR+SJF": row(RR, SJF, p_tok),
+        "LB+SJF": row(LB, SJF, p_tok),
+        "RR+SJF exact lengths": row(RR, SJF, L),
+        "LB+SJF exact lengths": row(LB, SJF, L),
+    }
+    out = {
+        "metric": "control plane: requests predicted-length-converted, routed (LB) and queued (SJF) through "
+                  "a full decode-cluster simulation, per host second",
+        "value": tr.n / (ms / 1e3), "unit": "requests/s (host)", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic (seeded Poisson arrivals at 100/s, lognormal output lengths, median 1,030, "
+                "sigma 0.6, clipped to 2,047; predictions with lognormal error sigma 0.25)",
+        "config": {"workload": "1P3D decode cluster, 3 instances x 256 slots, iteration 12 ms + 0.12 ms per "
+                               "running request, 1,914 requests", "requests": tr.n,
+                   "mean_output_tokens": float(L.mean()),
+                   "prediction_mae_tokens": float(np.abs(p_tok.astype(np.int64) - L).mean())},
+        "roofline": None,
+        "serving": serving,
+    }
+    if not a.no_cpu_baseline:
+        from oracle import sched as S
+        t0 = time.perf_counter()
+        S.simulate([int(x) for x in arrival], [int(x) for x in L], S.pred_tokens(z), *cluster, S.LB, S.SJF, *it)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": tr.n / dt, "unit": "requests/s (host)", "cores": 1, "kind": "oracle",
+                               "sample": f"one LB+SJF simulation of the whole trace in plain Python ({dt:.2f} s)"}
+    return _emit(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -322,12 +390,14 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--workload", default="prefill-8b",
-                    choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3", "probe-8b"],
+                    choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3", "probe-8b",
+                             "sched-1p3d"],
                     help="prefill-8b (default): 32-request 8B prefill + one step; decode-8b: 512 "
                          "in-flight requests with 256..8192 cached tokens, timed decode steps; "
                          "prefill-8b-large: 256 requests (~466k tokens) in one call; "
                          "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests; probe-8b: the "
-                         "MLP-probe baseline on the config-1 batch")
+                         "MLP-probe baseline on the config-1 batch; sched-1p3d: the LB + SJF control "
+                         "plane on the 1,914-request saturation trace (host only)")
     ap.add_argument("--attn-gate", action="store_true",
                     help="draft layer with the Gated Attention output gate (Section 4.1)")
     ap.add_argument("--draft-head", action="store_true",
@@ -348,6 +418,9 @@ def main(argv=None):
     if a.input_embed and a.workload != "prefill-8b":
         print("--input-embed is measured on the prefill-8b workload only", file=sys.stderr)
         return 2
+
+    if a.workload == "sched-1p3d":
+        return bench_sched(a)
 
     import numpy as np
     import torch

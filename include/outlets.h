@@ -384,6 +384,113 @@ int outlets_pager_release(outlets_pager* p, int32_t n, const int32_t* slots);
 /* what: OUTLETS_META_PAGE_TABLE or OUTLETS_META_SEQ_LEN. */
 int outlets_pager_read(outlets_pager* p, int32_t what, int32_t* out, int64_t cap, int64_t* n_out);
 
+/* ------------------------------------------------------------ control plane
+ * The consumer of the static prediction r_hat_0 in disaggregated serving
+ * (Section 5, system-level evaluation): routing of arriving requests over K
+ * decode instances and the admission order of each instance's queue.  Host
+ * code only (no GPU), thread-compatible.
+ *   routing OUTLETS_ROUTE_RR: the i-th submitted request goes to instance
+ *     i mod K.  OUTLETS_ROUTE_LB: to the instance with the lowest estimated
+ *     remaining work, the sum of predicted remaining lengths of its waiting
+ *     (pred) and running (max(pred - generated, 0)) requests; ties go to the
+ *     lowest instance index.
+ *   queue OUTLETS_QUEUE_FCFS: admission in submission order.
+ *     OUTLETS_QUEUE_SJF: shortest predicted length first, ties in
+ *     submission order.  Admission is non-preemptive.
+ * Predicted lengths are whole tokens (outlets_pred_tokens converts the
+ * length head's z_hat).
+ */
+enum { OUTLETS_ROUTE_RR = 0, OUTLETS_ROUTE_LB = 1 };
+enum { OUTLETS_QUEUE_FCFS = 0, OUTLETS_QUEUE_SJF = 1 };
+
+typedef struct outlets_sched outlets_sched;
+
+/*
+ * z_hat (host float [n], the length head's log(1 + length) estimates) ->
+ * tokens_out (host int32 [n]): floor(max(0, expm1(z)) + 0.5), NaN -> 0,
+ * capped at 2^31 - 1.
+ */
+int outlets_pred_tokens(int32_t n, const float* z_hat, int32_t* tokens_out);
+
+/*
+ * An online control plane for K = n_instances decode instances running at
+ * most max_running requests each; request ids are the caller's, in
+ * [0, max_requests), and may be reused once finished.
+ */
+int outlets_sched_create(int32_t n_instances, int32_t max_running, int32_t routing,
+                         int32_t queue_order, int32_t max_requests, outlets_sched** out);
+int outlets_sched_destroy(outlets_sched* s);
+
+/*
+ * Route n arriving requests in argument order; instance_out [n] receives
+ * each one's instance, and each joins that instance's queue.  All checks
+ * come first (ids in range and idle, no repeats, pred_tokens >= 0: else
+ * INVALID_ARG, or SLOT_BUSY for an id still waiting or running) and a failed
+ * call changes nothing.
+ */
+int outlets_sched_submit(outlets_sched* s, int32_t n, const int32_t* ids, const int32_t* pred_tokens,
+                         int32_t* instance_out);
+
+/*
+ * Admit up to min(cap, max_running - running) waiting requests of
+ * `instance` in queue order: ids_out [cap] receives them, *n_out the count.
+ * Call it when the instance starts a decode iteration.
+ */
+int outlets_sched_admit(outlets_sched* s, int32_t instance, int32_t cap, int32_t* ids_out, int32_t* n_out);
+
+/* One decode iteration of `instance` finished: each running request there
+ * generated one token (its predicted remaining length drops by one while
+ * positive). */
+int outlets_sched_iteration(outlets_sched* s, int32_t instance);
+
+/* Requests that finished; each must be running (else INVALID_ARG, no change). */
+int outlets_sched_finish(outlets_sched* s, int32_t n, const int32_t* ids);
+
+/* Estimated remaining work (predicted tokens), queue length and running
+ * count of `instance`; any output may be NULL. */
+int outlets_sched_read(outlets_sched* s, int32_t instance, int64_t* load, int32_t* n_waiting,
+                       int32_t* n_running);
+
+/*
+ * Discrete-event run of the decode cluster (the setting of the paper's
+ * saturation experiment: one prefill instance feeding K decode instances)
+ * over a request trace, using the control plane above.  Each instance runs
+ * continuous-batching iterations back to back while it has running
+ * requests; an iteration with b running requests lasts iter_base_us +
+ * iter_per_seq_us * b microseconds and gives each one token; waiting
+ * requests are admitted only when an iteration starts (or on arrival at an
+ * idle instance); a request finishes at the end of the iteration that makes
+ * its out_len-th token.  Events at one instant: iteration ends (instance
+ * order), then arrivals (trace order), then admissions and iteration starts.
+ *   arrival_us [n] (host, >= 0, nondecreasing), out_len [n] (true output
+ *   lengths >= 1), pred_tokens [n] (>= 0).
+ *   instance_out [n], start_us_out [n] (admission time), finish_us_out [n].
+ * Errors: bad config or inputs (INVALID_ARG, nothing written).
+ */
+typedef struct outlets_sim_config {
+    int32_t n_instances;
+    int32_t max_running;
+    int32_t routing;
+    int32_t queue_order;
+    int64_t iter_base_us;
+    int64_t iter_per_seq_us;
+} outlets_sim_config;
+
+int outlets_sched_simulate(const outlets_sim_config* cfg, int32_t n, const int64_t* arrival_us,
+                           const int32_t* out_len, const int32_t* pred_tokens, int32_t* instance_out,
+                           int64_t* start_us_out, int64_t* finish_us_out);
+
+/*
+ * Serving metrics of a run: out [6] = throughput (generated tokens / (last
+ * finish - first arrival), tokens/s), mean latency (s), P99 latency (s,
+ * nearest rank: the ceil(0.99 m)-th smallest of m) of requests with out_len
+ * < short_below, in [short_below, long_from), and >= long_from (NaN for an
+ * empty class), and the makespan (s).  Latency = finish - arrival.
+ */
+int outlets_sched_metrics(int32_t n, const int64_t* arrival_us, const int32_t* out_len,
+                          const int64_t* finish_us, int32_t short_below, int32_t long_from,
+                          double* out);
+
 #ifdef __cplusplus
 }
 #endif

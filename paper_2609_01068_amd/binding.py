@@ -72,6 +72,15 @@ class outlets_weights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in WEIGHT_FIELDS]
 
 
+OUTLETS_ROUTE_RR, OUTLETS_ROUTE_LB = 0, 1
+OUTLETS_QUEUE_FCFS, OUTLETS_QUEUE_SJF = 0, 1
+
+
+class outlets_sim_config(C.Structure):
+    _fields_ = [("n_instances", C.c_int32), ("max_running", C.c_int32), ("routing", C.c_int32),
+                ("queue_order", C.c_int32), ("iter_base_us", C.c_int64), ("iter_per_seq_us", C.c_int64)]
+
+
 _lib: Optional[C.CDLL] = None
 
 _P = C.c_void_p
@@ -98,6 +107,16 @@ _SIGS = {
     "outlets_pager_step": (C.c_int, [_P, C.c_int32, _I32P]),
     "outlets_pager_release": (C.c_int, [_P, C.c_int32, _I32P]),
     "outlets_pager_read": (C.c_int, [_P, C.c_int32, _I32P, C.c_int64, C.POINTER(C.c_int64)]),
+    "outlets_pred_tokens": (C.c_int, [C.c_int32, _P, _P]),
+    "outlets_sched_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(_P)]),
+    "outlets_sched_destroy": (C.c_int, [_P]),
+    "outlets_sched_submit": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _I32P]),
+    "outlets_sched_admit": (C.c_int, [_P, C.c_int32, C.c_int32, _I32P, _I32P]),
+    "outlets_sched_iteration": (C.c_int, [_P, C.c_int32]),
+    "outlets_sched_finish": (C.c_int, [_P, C.c_int32, _I32P]),
+    "outlets_sched_read": (C.c_int, [_P, C.c_int32, C.POINTER(C.c_int64), _I32P, _I32P]),
+    "outlets_sched_simulate": (C.c_int, [C.POINTER(outlets_sim_config), C.c_int32, _P, _P, _P, _P, _P, _P]),
+    "outlets_sched_metrics": (C.c_int, [C.c_int32, _P, _P, _P, C.c_int32, C.c_int32, _P]),
 }
 
 
@@ -251,6 +270,96 @@ class Pager:
     def close(self):
         if self.h:
             lib().outlets_pager_destroy(self.h)
+            self.h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------------ control plane (host only)
+
+def _np(a, dtype):
+    import numpy as np
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def outlets_pred_tokens(z_hat):
+    """Whole-token predicted lengths from z_hat (host floats)."""
+    import numpy as np
+    z = _np(z_hat, np.float32)
+    out = np.empty(len(z), dtype=np.int32)
+    check(lib().outlets_pred_tokens(len(z), z.ctypes.data, out.ctypes.data), "outlets_pred_tokens")
+    return out
+
+
+def outlets_sched_simulate(arrival_us, out_len, pred_tokens, n_instances: int, max_running: int,
+                           routing: int, queue_order: int, iter_base_us: int, iter_per_seq_us: int):
+    """Run the decode-cluster simulation; returns (instance, start_us, finish_us) arrays."""
+    import numpy as np
+    a, L, p = _np(arrival_us, np.int64), _np(out_len, np.int32), _np(pred_tokens, np.int32)
+    n = len(a)
+    if len(L) != n or len(p) != n:
+        raise ValueError("trace arrays differ in length")
+    cfg = outlets_sim_config(n_instances, max_running, routing, queue_order, iter_base_us, iter_per_seq_us)
+    inst = np.full(n, -1, dtype=np.int32)
+    start = np.full(n, -1, dtype=np.int64)
+    finish = np.full(n, -1, dtype=np.int64)
+    check(lib().outlets_sched_simulate(C.byref(cfg), n, a.ctypes.data, L.ctypes.data, p.ctypes.data,
+                                       inst.ctypes.data, start.ctypes.data, finish.ctypes.data),
+          "outlets_sched_simulate")
+    return inst, start, finish
+
+
+def outlets_sched_metrics(arrival_us, out_len, finish_us, short_below: int = 800, long_from: int = 1300):
+    """(tokens/s, mean latency s, P99 short, P99 medium, P99 long, makespan s)."""
+    import numpy as np
+    a, L, f = _np(arrival_us, np.int64), _np(out_len, np.int32), _np(finish_us, np.int64)
+    out = np.empty(6, dtype=np.float64)
+    check(lib().outlets_sched_metrics(len(a), a.ctypes.data, L.ctypes.data, f.ctypes.data, short_below,
+                                      long_from, out.ctypes.data), "outlets_sched_metrics")
+    return tuple(float(x) for x in out)
+
+
+class ControlPlane:
+    """The library's online control plane (host only)."""
+
+    def __init__(self, n_instances: int, max_running: int, routing: int, queue_order: int, max_requests: int):
+        self.h = C.c_void_p()
+        check(lib().outlets_sched_create(n_instances, max_running, routing, queue_order, max_requests,
+                                         C.byref(self.h)), "outlets_sched_create")
+        self.max_running = max_running
+
+    def submit(self, ids, preds):
+        out = (C.c_int32 * max(1, len(ids)))()
+        check(lib().outlets_sched_submit(self.h, len(ids), i32_array(ids), i32_array(preds), out),
+              "outlets_sched_submit")
+        return list(out[:len(ids)])
+
+    def admit(self, instance: int, cap: Optional[int] = None):
+        cap = self.max_running if cap is None else cap
+        out = (C.c_int32 * max(1, cap))()
+        n = C.c_int32()
+        check(lib().outlets_sched_admit(self.h, instance, cap, out, C.byref(n)), "outlets_sched_admit")
+        return list(out[:n.value])
+
+    def iteration(self, instance: int) -> None:
+        check(lib().outlets_sched_iteration(self.h, instance), "outlets_sched_iteration")
+
+    def finish(self, ids) -> None:
+        check(lib().outlets_sched_finish(self.h, len(ids), i32_array(ids)), "outlets_sched_finish")
+
+    def read(self, instance: int):
+        load, w, r = C.c_int64(), C.c_int32(), C.c_int32()
+        check(lib().outlets_sched_read(self.h, instance, C.byref(load), C.byref(w), C.byref(r)),
+              "outlets_sched_read")
+        return load.value, w.value, r.value
+
+    def close(self):
+        if self.h:
+            lib().outlets_sched_destroy(self.h)
             self.h = C.c_void_p()
 
     def __del__(self):

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "liboutlets.so")
 
-SOURCES = ["pager.cpp", "gemm.hip", "rows.hip", "attn.hip", "api.hip"]
+SOURCES = ["pager.cpp", "sched.cpp", "gemm.hip", "rows.hip", "attn.hip", "api.hip"]
 ARCH = "gfx950"
 
 

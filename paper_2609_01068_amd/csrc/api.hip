@@ -16,6 +16,7 @@
 #include "kernels.hpp"
 #include "outlets.h"
 #include "pager.hpp"
+#include "sched.hpp"
 
 using namespace outlets;
 
@@ -1032,6 +1033,166 @@ int outlets_pager_read(outlets_pager* p, int32_t what, int32_t* out, int64_t cap
     *n_out = static_cast<int64_t>(v->size());
     if (cap < *n_out) return fail(OUTLETS_ERR_INVALID_ARG, "output capacity too small");
     std::memcpy(out, v->data(), sizeof(int32_t) * v->size());
+    return OUTLETS_OK;
+}
+
+
+// ---------------------------------------------------------------- control plane
+
+struct outlets_sched {
+    ControlPlane cp;
+    outlets_sched(const SchedPolicy& p, int32_t cap) : cp(p, cap) {}
+};
+
+namespace {
+
+int check_policy(int32_t k, int32_t s, int32_t routing, int32_t order) {
+    if (k <= 0 || s <= 0) return fail(OUTLETS_ERR_INVALID_ARG, "instances and max_running must be positive");
+    if ((routing != OUTLETS_ROUTE_RR && routing != OUTLETS_ROUTE_LB) ||
+        (order != OUTLETS_QUEUE_FCFS && order != OUTLETS_QUEUE_SJF))
+        return fail(OUTLETS_ERR_INVALID_ARG, "unknown routing or queue order");
+    return OUTLETS_OK;
+}
+
+}  // namespace
+
+int outlets_pred_tokens(int32_t n, const float* z_hat, int32_t* tokens_out) {
+    if (n < 0 || (n > 0 && (!z_hat || !tokens_out))) return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    for (int32_t i = 0; i < n; ++i) tokens_out[i] = pred_tokens_from_z(z_hat[i]);
+    return OUTLETS_OK;
+}
+
+int outlets_sched_create(int32_t n_instances, int32_t max_running, int32_t routing, int32_t queue_order,
+                         int32_t max_requests, outlets_sched** out) {
+    if (!out) return fail(OUTLETS_ERR_INVALID_ARG, "out is null");
+    *out = nullptr;
+    int rc = check_policy(n_instances, max_running, routing, queue_order);
+    if (rc) return rc;
+    if (max_requests <= 0) return fail(OUTLETS_ERR_INVALID_ARG, "max_requests must be positive");
+    SchedPolicy p;
+    p.instances = n_instances;
+    p.max_running = max_running;
+    p.routing = routing;
+    p.order = queue_order;
+    try {
+        *out = new outlets_sched(p, max_requests);
+    } catch (const std::bad_alloc&) {
+        return fail(OUTLETS_ERR_NOMEM, "host allocation failed");
+    }
+    return OUTLETS_OK;
+}
+
+int outlets_sched_destroy(outlets_sched* s) {
+    delete s;
+    return OUTLETS_OK;
+}
+
+int outlets_sched_submit(outlets_sched* s, int32_t n, const int32_t* ids, const int32_t* pred_tokens,
+                         int32_t* instance_out) {
+    if (!s || n < 0 || (n > 0 && (!ids || !pred_tokens || !instance_out)))
+        return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    const char* why = "";
+    int rc = s->cp.check_submit(n, ids, pred_tokens, &why);
+    if (rc) return fail(rc, why);
+    for (int32_t i = 0; i < n; ++i) instance_out[i] = s->cp.submit(ids[i], pred_tokens[i]);
+    return OUTLETS_OK;
+}
+
+int outlets_sched_admit(outlets_sched* s, int32_t instance, int32_t cap, int32_t* ids_out, int32_t* n_out) {
+    if (!s || !n_out || cap < 0 || (cap > 0 && !ids_out)) return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    if (instance < 0 || instance >= s->cp.instances()) return fail(OUTLETS_ERR_INVALID_ARG, "instance out of range");
+    *n_out = s->cp.admit(instance, cap, ids_out);
+    return OUTLETS_OK;
+}
+
+int outlets_sched_iteration(outlets_sched* s, int32_t instance) {
+    if (!s) return fail(OUTLETS_ERR_INVALID_ARG, "null control plane");
+    if (instance < 0 || instance >= s->cp.instances()) return fail(OUTLETS_ERR_INVALID_ARG, "instance out of range");
+    s->cp.iteration(instance);
+    return OUTLETS_OK;
+}
+
+int outlets_sched_finish(outlets_sched* s, int32_t n, const int32_t* ids) {
+    if (!s || n < 0 || (n > 0 && !ids)) return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    std::vector<char> seen(static_cast<size_t>(s->cp.capacity()), 0);
+    for (int32_t i = 0; i < n; ++i) {
+        if (ids[i] < 0 || ids[i] >= s->cp.capacity()) return fail(OUTLETS_ERR_INVALID_ARG, "request id out of range");
+        if (!s->cp.is_running(ids[i])) return fail(OUTLETS_ERR_INVALID_ARG, "request is not running");
+        if (seen[ids[i]]) return fail(OUTLETS_ERR_INVALID_ARG, "repeated request id");
+        seen[ids[i]] = 1;
+    }
+    for (int32_t i = 0; i < n; ++i) s->cp.finish(ids[i]);
+    return OUTLETS_OK;
+}
+
+int outlets_sched_read(outlets_sched* s, int32_t instance, int64_t* load, int32_t* n_waiting,
+                       int32_t* n_running) {
+    if (!s) return fail(OUTLETS_ERR_INVALID_ARG, "null control plane");
+    if (instance < 0 || instance >= s->cp.instances()) return fail(OUTLETS_ERR_INVALID_ARG, "instance out of range");
+    if (load) *load = s->cp.load(instance);
+    if (n_waiting) *n_waiting = s->cp.n_waiting(instance);
+    if (n_running) *n_running = static_cast<int32_t>(s->cp.running(instance).size());
+    return OUTLETS_OK;
+}
+
+int outlets_sched_simulate(const outlets_sim_config* cfg, int32_t n, const int64_t* arrival_us,
+                           const int32_t* out_len, const int32_t* pred_tokens, int32_t* instance_out,
+                           int64_t* start_us_out, int64_t* finish_us_out) {
+    if (!cfg || n < 0) return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    int rc = check_policy(cfg->n_instances, cfg->max_running, cfg->routing, cfg->queue_order);
+    if (rc) return rc;
+    if (cfg->iter_base_us < 0 || cfg->iter_per_seq_us < 0)
+        return fail(OUTLETS_ERR_INVALID_ARG, "iteration times must be >= 0");
+    if (n == 0) return OUTLETS_OK;
+    if (!arrival_us || !out_len || !pred_tokens || !instance_out || !start_us_out || !finish_us_out)
+        return fail(OUTLETS_ERR_INVALID_ARG, "null array");
+    if (arrival_us[0] < 0) return fail(OUTLETS_ERR_INVALID_ARG, "arrival times must be >= 0");
+    SimConfig sc;
+    sc.policy.instances = cfg->n_instances;
+    sc.policy.max_running = cfg->max_running;
+    sc.policy.routing = cfg->routing;
+    sc.policy.order = cfg->queue_order;
+    sc.iter_base_us = cfg->iter_base_us;
+    sc.iter_per_seq_us = cfg->iter_per_seq_us;
+    const char* why = "";
+    try {
+        rc = simulate(sc, n, arrival_us, out_len, pred_tokens, instance_out, start_us_out, finish_us_out, &why);
+    } catch (const std::bad_alloc&) {
+        return fail(OUTLETS_ERR_NOMEM, "host allocation failed");
+    }
+    return rc ? fail(rc, why) : OUTLETS_OK;
+}
+
+int outlets_sched_metrics(int32_t n, const int64_t* arrival_us, const int32_t* out_len,
+                          const int64_t* finish_us, int32_t short_below, int32_t long_from,
+                          double* out) {
+    if (n < 0 || !out || (n > 0 && (!arrival_us || !out_len || !finish_us)))
+        return fail(OUTLETS_ERR_INVALID_ARG, "bad arguments");
+    const double nan = std::nan("");
+    for (int i = 0; i < 6; ++i) out[i] = nan;
+    if (n == 0) return OUTLETS_OK;
+    std::vector<double> cls[3];
+    double lat_sum = 0.0;
+    int64_t tokens = 0, t0 = arrival_us[0], t1 = finish_us[0];
+    for (int32_t i = 0; i < n; ++i) {
+        const double lat = static_cast<double>(finish_us[i] - arrival_us[i]) / 1e6;
+        lat_sum += lat;
+        tokens += out_len[i];
+        t0 = std::min(t0, arrival_us[i]);
+        t1 = std::max(t1, finish_us[i]);
+        cls[out_len[i] < short_below ? 0 : (out_len[i] < long_from ? 1 : 2)].push_back(lat);
+    }
+    const double span = static_cast<double>(t1 - t0) / 1e6;
+    out[0] = span > 0 ? static_cast<double>(tokens) / span : INFINITY;
+    out[1] = lat_sum / n;
+    for (int c = 0; c < 3; ++c) {
+        std::vector<double>& v = cls[c];
+        if (v.empty()) continue;
+        std::sort(v.begin(), v.end());
+        const size_t m = v.size();
+        out[2 + c] = v[(99 * m + 99) / 100 - 1];
+    }
+    out[5] = span;
     return OUTLETS_OK;
 }
 
