@@ -44,9 +44,6 @@ namespace {
 #ifndef OUTLETS_GEMM_DMAW
 #define OUTLETS_GEMM_DMAW 4   // waves that issue the LDS copies (0 = all)
 #endif
-#ifndef OUTLETS_GEMM_GM
-#define OUTLETS_GEMM_GM 8     // row tiles walked per column step within an XCD
-#endif
 constexpr int BK = OUTLETS_GEMM_BK;
 
 __device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
@@ -66,9 +63,11 @@ __device__ __forceinline__ void b_row(const GemmB& B, int n, int& s, int& r) {
 __device__ __forceinline__ float silu_f(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // Tile order: pid walks GM row-tiles before moving along N, so A rows and
-// B columns are reused from L2.
+// B columns are reused from L2.  GM = 3 for wide outputs (>= 64 column
+// tiles) and 2 otherwise (measured best among 1-16 on the draft layer's
+// shapes).
 __host__ __device__ __forceinline__ void tile_coords(int pid, int mt, int nt, int& tm, int& tn) {
-    constexpr int GM = OUTLETS_GEMM_GM;
+    const int GM = nt >= 64 ? 3 : 2;
     const int group = pid / (GM * nt);
     const int first = group * GM;
     const int gsize = (mt - first < GM) ? mt - first : GM;
@@ -224,6 +223,7 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             dma16(rb[j], b_voff[j] + static_cast<uint32_t>(k0 * ESZ), base + A_BYTES + (dwave * BCP + j) * 1024);
     };
 
+    const int grp = lane >> 4, l16 = lane & 15;
     f32x4 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -232,7 +232,6 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.f;
 
-    const int grp = lane >> 4, l16 = lane & 15;
     auto load_a = [&](const char* base, int st, bf16x8* af) {
         const int c = 4 * st + grp;
 #pragma unroll
@@ -314,7 +313,6 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     constexpr int OSZ = F32OUT ? 4 : static_cast<int>(sizeof(OutT));
     const int rows_valid = EPI == EPI_PARTIAL_TILE ? BM : min(BM, M - m0);
     const int ldc = EPI == EPI_PARTIAL_TILE ? BN : static_cast<int>(C.ldc);   // tile offsets fit 32 bits
-    const int ldr = static_cast<int>(C.ldr);
     const int ncol0 = EPI == EPI_PARTIAL_TILE ? n0 : 0;       // column origin of the output block
     char* cbase =
         EPI == EPI_PARTIAL_TILE
@@ -322,6 +320,7 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             : static_cast<char*>(C.c) +
                   ((EPI == EPI_PARTIAL ? (int64_t)blockIdx.y * C.split_stride : 0) + (int64_t)m0 * C.ldc) * OSZ;
     const __amdgpu_buffer_rsrc_t rc = buf_rsrc(cbase, (int64_t)rows_valid * ldc * OSZ);
+    const int ldr = static_cast<int>(C.ldr);
     const __amdgpu_buffer_rsrc_t rr =
         EPI == EPI_RESID_F32 ? buf_rsrc(C.resid + (int64_t)m0 * C.ldr, (int64_t)rows_valid * C.ldr * 4) : rc;
     auto put = [&](uint32_t off, float v) {
@@ -340,17 +339,16 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     for (int j0 = 0; j0 < FN; j0 += JB) {
         float rv[JB][EPI == EPI_RESID_F32 ? FM : 1][4];
         if (EPI == EPI_RESID_F32) {
+            // one lane offset; the row step goes in the scalar offset
+            const uint32_t vb = static_cast<uint32_t>(((wm * TM + 4 * grp) * ldr + n0 + wn * TN + l16) * 4);
 #pragma unroll
             for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int n = n0 + wn * TN + (j0 + jj) * 16 + l16;
-                        const int row = wm * TM + i * 16 + 4 * grp + q;
+                    for (int q = 0; q < 4; ++q)
                         rv[jj][i][q] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                            rr, static_cast<uint32_t>((row * ldr + n) * 4), 0, 0));
-                    }
+                            rr, vb + (j0 + jj) * 64, (i * 16 + q) * ldr * 4, 0));
         }
 #pragma unroll
         for (int jj = 0; jj < JB; ++jj) {
