@@ -352,6 +352,15 @@ enum {
 int outlets_profile_enable(outlets_ctx* ctx, int32_t enable);
 
 /*
+ * Like outlets_profile_enable, but records event pairs only around the
+ * kernel groups whose bit is set in `groups` (bit k = group OUTLETS_K_k;
+ * bits at or above OUTLETS_K_COUNT are ignored); 0 stops.  Timing one group
+ * (e.g. the dominant kernel) perturbs the calls far less than timing all of
+ * them.  Clears the totals.
+ */
+int outlets_profile_enable_groups(outlets_ctx* ctx, uint32_t groups);
+
+/*
  * Total milliseconds and launch count recorded for kernel group `which`
  * (OUTLETS_K_*) inside prefill calls (call = 0) or step calls (call = 1)
  * since profiling was enabled.  Synchronises on the recorded events.

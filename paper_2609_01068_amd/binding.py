@@ -99,6 +99,7 @@ _SIGS = {
     "outlets_get_buffer": (C.c_int, [_P, C.c_int32, _P, C.c_int64, C.POINTER(C.c_int64), _P]),
     "outlets_last_error": (C.c_char_p, []),
     "outlets_profile_enable": (C.c_int, [_P, C.c_int32]),
+    "outlets_profile_enable_groups": (C.c_int, [_P, C.c_uint32]),
     "outlets_profile_read": (C.c_int, [_P, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "outlets_varlen_meta": (C.c_int, [C.c_int32, _I32P, _I32P, _I32P, _I32P]),
     "outlets_pager_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(_P)]),
@@ -225,6 +226,10 @@ def outlets_buffer_size(ctx, which: int) -> int:
 
 def outlets_profile_enable(ctx, enable: bool) -> None:
     check(lib().outlets_profile_enable(ctx, int(bool(enable))), "outlets_profile_enable")
+
+
+def outlets_profile_enable_groups(ctx, groups: int) -> None:
+    check(lib().outlets_profile_enable_groups(ctx, int(groups) & 0xFFFFFFFF), "outlets_profile_enable_groups")
 
 
 def outlets_profile_read(ctx, call: int, which: int):

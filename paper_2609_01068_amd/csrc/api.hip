@@ -106,6 +106,7 @@ struct outlets_ctx {
 
     // per-kernel timing (outlets_profile_enable)
     bool prof_on = false;
+    uint32_t prof_mask = 0;   // kernel groups timed while prof_on
     struct Mark { int phase, which; hipEvent_t a, b; };
     std::vector<Mark> marks;
     std::vector<hipEvent_t> spare;
@@ -155,7 +156,7 @@ struct KTimer {
     hipStream_t st;
     hipEvent_t a = nullptr;
     KTimer(outlets_ctx* c_, int w, hipStream_t s) : c(c_), which(w), st(s) {
-        if (c->prof_on && (a = c->take_event())) (void)hipEventRecord(a, st);
+        if (c->prof_on && ((c->prof_mask >> which) & 1u) && (a = c->take_event())) (void)hipEventRecord(a, st);
     }
     ~KTimer() {
         if (!a) return;
@@ -951,14 +952,19 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
     return OUTLETS_OK;
 }
 
-int outlets_profile_enable(outlets_ctx* ctx, int32_t enable) {
+int outlets_profile_enable_groups(outlets_ctx* ctx, uint32_t groups) {
     if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
     (void)hipSetDevice(ctx->device);
     collect_marks(ctx);
     for (int p = 0; p < 2; ++p)
         for (int i = 0; i < OUTLETS_K_COUNT; ++i) { ctx->prof_ms[p][i] = 0.0; ctx->prof_n[p][i] = 0; }
-    ctx->prof_on = enable != 0;
+    ctx->prof_mask = groups & ((1u << OUTLETS_K_COUNT) - 1u);
+    ctx->prof_on = ctx->prof_mask != 0;
     return OUTLETS_OK;
+}
+
+int outlets_profile_enable(outlets_ctx* ctx, int32_t enable) {
+    return outlets_profile_enable_groups(ctx, enable ? (1u << OUTLETS_K_COUNT) - 1u : 0u);
 }
 
 int outlets_profile_read(outlets_ctx* ctx, int32_t call, int32_t which, double* total_ms,

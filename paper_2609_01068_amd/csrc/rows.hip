@@ -341,6 +341,41 @@ head_finish_kernel(int h1, int splits, int n_req, int rows, const float* partial
     if (threadIdx.x == 0) z[i] = acc + load_act<TW>(b2);
 }
 
+// Same result for the fixed split count S and h1 a multiple of 4: each thread
+// takes four consecutive hidden units and issues all 2 S of its partial loads
+// (16-byte) before summing them in split order, so the block waits out one
+// memory latency instead of one per split.
+template <typename TW, int S>
+__global__ void __launch_bounds__(256)
+head_finish_vec_kernel(int h1, int n_req, int rows, const float* partial, const TW* b1, const TW* w2,
+                       const TW* b2, float* z) {
+    __shared__ float red[4];
+    const int i = blockIdx.x;
+    const bool lo = rows > n_req;
+    float acc = 0.f;
+    for (int j = threadIdx.x * 4; j < h1; j += 1024) {
+        float4 ph[S], pl[S];
+#pragma unroll
+        for (int sp = 0; sp < S; ++sp) {
+            ph[sp] = *reinterpret_cast<const float4*>(partial + ((int64_t)sp * rows + i) * h1 + j);
+            pl[sp] = lo ? *reinterpret_cast<const float4*>(partial + ((int64_t)sp * rows + n_req + i) * h1 + j)
+                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = load_act<TW>(b1 + j + e);
+#pragma unroll
+        for (int sp = 0; sp < S; ++sp) {
+            v[0] += ph[sp].x; v[1] += ph[sp].y; v[2] += ph[sp].z; v[3] += ph[sp].w;
+            if (lo) { v[0] += pl[sp].x; v[1] += pl[sp].y; v[2] += pl[sp].z; v[3] += pl[sp].w; }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = fmaf(fmaxf(v[e], 0.f), load_act<TW>(w2 + j + e), acc);
+    }
+    acc = block_sum<256>(acc, red);
+    if (threadIdx.x == 0) z[i] = acc + load_act<TW>(b2);
+}
+
 template <typename T>
 __global__ void copy_rows_kernel(int d, const float* src, int64_t lds, T* dst, int64_t ldd) {
     const int64_t r = blockIdx.x;
@@ -531,6 +566,17 @@ void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* 
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
                         const void* b1, const void* w2, const void* b2, float* z, hipStream_t st) {
     if (n_req <= 0) return;
+    if (splits == 8 && h1 % 4 == 0) {
+        if (w_fmt == FMT_F32)
+            hipLaunchKernelGGL((head_finish_vec_kernel<float, 8>), dim3(n_req), dim3(256), 0, st, h1, n_req,
+                               n_req, partial, static_cast<const float*>(b1), static_cast<const float*>(w2),
+                               static_cast<const float*>(b2), z);
+        else
+            hipLaunchKernelGGL((head_finish_vec_kernel<bf16_t, 8>), dim3(n_req), dim3(256), 0, st, h1, n_req,
+                               2 * n_req, partial, static_cast<const bf16_t*>(b1),
+                               static_cast<const bf16_t*>(w2), static_cast<const bf16_t*>(b2), z);
+        return;
+    }
     if (w_fmt == FMT_F32)
         hipLaunchKernelGGL((head_finish_kernel<float>), dim3(n_req), dim3(256), 0, st, h1, splits,
                            n_req, n_req, partial, static_cast<const float*>(b1),

@@ -197,8 +197,14 @@ class OutletsPredictor:
         return p_out[:n_req]
 
     # ------------------------------------------------------------ inspection
-    def profile(self, enable: bool) -> None:
-        B.outlets_profile_enable(self.ctx, enable)
+    def profile(self, enable: bool, groups=None) -> None:
+        """Time every kernel group (or only the named ones, e.g. ["ATTN"]) of
+        later calls; enable=False stops."""
+        if groups is None:
+            B.outlets_profile_enable(self.ctx, enable)
+        else:
+            mask = sum(1 << B.KERNELS.index(g) for g in groups) if enable else 0
+            B.outlets_profile_enable_groups(self.ctx, mask)
 
     def profile_read(self, call: str = "prefill"):
         """{kernel group: (total ms, launches)} of prefill or step calls since
