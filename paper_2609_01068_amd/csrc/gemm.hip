@@ -277,8 +277,11 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
         wait_dma<(STAGES - 2) * OPS>();
         barrier_no_fence();   // every wave's copies of slice `it` are in LDS; slice it-1 is consumed
         // past the end, re-copy the last slice into a stage nobody reads again:
-        // the loop body stays one basic block, which the scheduler needs
-        issue(kb + min(it + STAGES - 1, nk_loop - 1) * BK, (it + STAGES - 1) % STAGES);
+        // the loop body stays one basic block, which the scheduler needs.
+        // With bf16 weights the copies go out first; with e4m3 weights after
+        // the first 32-deep step's MFMAs (measured: the other order is 10%
+        // slower for bf16 and 3-5% slower for e4m3)
+        if (!E4M3) issue(kb + min(it + STAGES - 1, nk_loop - 1) * BK, (it + STAGES - 1) % STAGES);
         const char* base = lds + (it % STAGES) * STAGE;
         bf16x8 af[2][FM], bfr[2][FN];
         load_a(base, 0, af[0]);
@@ -294,6 +297,7 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[st & 1][i], bfr[st & 1][j], acc[i][j], 0, 0, 0);
+            if (E4M3 && st == 0) issue(kb + min(it + STAGES - 1, nk_loop - 1) * BK, (it + STAGES - 1) % STAGES);
         }
 #if OUTLETS_GEMM_IGLP >= 0
         __builtin_amdgcn_iglp_opt(OUTLETS_GEMM_IGLP);   // interleave LDS reads with MFMAs
