@@ -322,7 +322,8 @@ enum {
  * Copy an activation of the last call (rows of that call only) or a KV pool
  * into caller device memory `dst` (`nbytes` capacity) on `stream`;
  * *n_bytes receives the size.  Buffers 0..8 and 12 need keep_intermediates
- * (HDRAFT, POOLED and the pools are always kept); NORM_EMB needs input
+ * (POOLED and the pools are always kept; h_draft of every row is otherwise
+ * available through the predict calls' hdraft_out); NORM_EMB needs input
  * embeddings.
  */
 int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbytes,
@@ -339,7 +340,7 @@ enum {
     OUTLETS_K_O_GEMM = 6,
     OUTLETS_K_GATE_UP_GEMM = 7, /* gate/up projection with the SwiGLU epilogue */
     OUTLETS_K_DOWN_GEMM = 8,
-    OUTLETS_K_POOL = 9,
+    OUTLETS_K_POOL = 9,         /* pooling (in prefill calls with the final RMSNorm, fused) */
     OUTLETS_K_HEAD = 10,        /* length head (both layers) */
     OUTLETS_K_COUNT = 11
 };

@@ -369,15 +369,28 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
       gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(c->mlp, c->F), 1, st, c->splitk_ws, c->splitk_bytes); }
     { KTimer t(c, OUTLETS_K_DOWN_GEMM, st);
       gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(c->r_x2, d, c->r_x1, d), 1, st, c->splitk_ws, c->splitk_bytes); }
-    { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d, st); }
     uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
-    { KTimer t(c, OUTLETS_K_POOL, st);
-      if (prefill)
-          launch_pool_prefill(n, c->n_tiles, d, FMT_F32, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
-                              c->pool_part, c->pool_sum, c->pooled, pb, st);
-      else
-          launch_pool_step(n, d, FMT_F32, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
+    // prefill: final RMSNorm + pooling in one pass over x2 (h_draft rows are
+    // stored only when the caller wants them or intermediates are kept; the
+    // pooling needs only each request's last row)
+    bool fused_pool = false;
+    if (prefill) {
+        KTimer t(c, OUTLETS_K_POOL, st);
+        fused_pool = launch_norm_pool_prefill(
+            af, c->small_fmt, n, c->n_tiles, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d,
+            hdraft_out != nullptr || c->cfg.keep_intermediates != 0, req_off, req_slot, c->d_meta + c->tiles_off,
+            c->pool_part, c->pool_sum, c->pooled, pb, st);
+    }
+    if (!fused_pool) {
+        { KTimer t(c, OUTLETS_K_NORM, st);
+          launch_rmsnorm(af, c->small_fmt, T, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d, st); }
+        { KTimer t(c, OUTLETS_K_POOL, st);
+          if (prefill)
+              launch_pool_prefill(n, c->n_tiles, d, FMT_F32, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
+                                  c->pool_part, c->pool_sum, c->pooled, pb, st);
+          else
+              launch_pool_step(n, d, FMT_F32, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
+    }
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
     // bf16 heads read the hi/lo split of the pooled vector: 2n rows
     const int head_rows = (wf == FMT_F32) ? n : 2 * n;
@@ -924,7 +937,7 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
         case OUTLETS_BUF_NORM_MLP: src = ctx->b_norm; size = ab * T * d; break;
         case OUTLETS_BUF_MLP_ACT: src = ctx->mlp; size = ab * T * ctx->F; break;
         case OUTLETS_BUF_X2: src = ctx->r_x2; size = 4 * T * d; break;
-        case OUTLETS_BUF_HDRAFT: src = ctx->r_h; size = 4 * T * d; needs_keep = false; break;
+        case OUTLETS_BUF_HDRAFT: src = ctx->r_h; size = 4 * T * d; needs_keep = true; break;
         case OUTLETS_BUF_POOLED: src = ctx->pooled; size = 4 * n * 2 * d; needs_keep = false; break;
         case OUTLETS_BUF_NORM_EMB:
             if (!ctx->embed_in) return fail(OUTLETS_ERR_INVALID_ARG, "the context has no input embeddings");

@@ -134,6 +134,16 @@ void launch_pool_prefill(int n_req, int n_tiles, int d, int h_fmt, const void* h
                          const int32_t* req_off, const int32_t* req_slot, const int32_t* cu_tiles,
                          float* part, float* pool_sum, float* pooled, uint16_t* pooled_bf16,
                          hipStream_t st);
+// The final RMSNorm (x -> y2 fp32 and, if y is set, y in act format) fused
+// with launch_pool_prefill on the normalised rows.  Rows are stored only
+// when full_rows; otherwise only each request's last row of y2 is (all the
+// pooling needs).  Returns false, launching nothing, for shapes the fused
+// kernel does not take (d not 1024, 2048, 4096 or 8192, or misaligned).
+bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles, int d, const float* x,
+                              int64_t ldx, const void* gamma, float eps, void* y, int64_t ldy, float* y2,
+                              int64_t ldy2, bool full_rows, const int32_t* req_off, const int32_t* req_slot,
+                              const int32_t* cu_tiles, float* part, float* pool_sum, float* pooled,
+                              uint16_t* pooled_bf16, hipStream_t st);
 // Step pooling: pool_sum[slot] += h[i]; pooled[i] = [pool_sum / (start + 1) ; h[i]].
 void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,

@@ -280,6 +280,87 @@ pool_tiles_kernel(int d, int n_req, const TH* h, int64_t ldh, const int32_t* req
     part[(int64_t)t * d + c] = s;
 }
 
+// The final RMSNorm fused with stage 1 of the prefill pooling (d = 1024 V):
+// tile t (as in pool_tiles_kernel) normalises its rows in order with the
+// arithmetic of rmsnorm_vec_kernel and sums them in row order into part[t],
+// so the sums are those of the unfused pair, bit for bit.  Normalised rows
+// are stored (y2 fp32, y in the act format) only when full_rows; otherwise
+// only each request's last row, which the head input also needs.  The next
+// row's loads are issued before the current row's reduction.
+template <typename TY, typename TG, int V>
+__global__ void __launch_bounds__(256)
+norm_pool_tiles_kernel(int d, int n_req, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
+                       int64_t ldy, float* y2, int64_t ldy2, int full_rows, const int32_t* req_off,
+                       const int32_t* cu_tiles, float* part) {
+    __shared__ float red[4];
+    const int t = blockIdx.x, th = threadIdx.x;
+    int lo = 0, hi = n_req - 1;        // request lo with cu_tiles[lo] <= t < cu_tiles[lo + 1]
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (cu_tiles[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const int b = req_off[lo] + (t - cu_tiles[lo]) * 32;
+    const int e = min(b + 32, req_off[lo + 1]);
+    const int last = req_off[lo + 1] - 1;
+    float g[V][4];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        const int c = (j * 256 + th) * 4;
+        if constexpr (sizeof(TG) == 4) {
+            const float4 gv = *reinterpret_cast<const float4*>(gamma + c);
+            g[j][0] = gv.x; g[j][1] = gv.y; g[j][2] = gv.z; g[j][3] = gv.w;
+        } else {
+            const uint2 gv = *reinterpret_cast<const uint2*>(gamma + c);
+            g[j][0] = __uint_as_float(gv.x << 16); g[j][1] = __uint_as_float(gv.x & 0xffff0000u);
+            g[j][2] = __uint_as_float(gv.y << 16); g[j][3] = __uint_as_float(gv.y & 0xffff0000u);
+        }
+    }
+    float4 acc[V], vn[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        vn[j] = reinterpret_cast<const float4*>(x + (int64_t)b * ldx)[j * 256 + th];
+    }
+    for (int r = b; r < e; ++r) {
+        float4 v[V];
+        float ss = 0.f;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            v[j] = vn[j];
+            ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
+        }
+        if (r + 1 < e) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) vn[j] = reinterpret_cast<const float4*>(x + (int64_t)(r + 1) * ldx)[j * 256 + th];
+        }
+        ss = block_sum<256>(ss, red);
+        const float inv = 1.0f / sqrtf(ss / d + eps);
+        const bool store = full_rows || r == last;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            const int c = (j * 256 + th) * 4;
+            const float o0 = v[j].x * inv * g[j][0], o1 = v[j].y * inv * g[j][1];
+            const float o2 = v[j].z * inv * g[j][2], o3 = v[j].w * inv * g[j][3];
+            acc[j].x += o0; acc[j].y += o1; acc[j].z += o2; acc[j].w += o3;
+            if (store) {
+                if (y) {
+                    if constexpr (sizeof(TY) == 4) {
+                        *reinterpret_cast<float4*>(y + (int64_t)r * ldy + c) = make_float4(o0, o1, o2, o3);
+                    } else {
+                        uint2 pk;
+                        pk.x = f32_to_bf16(o0) | (uint32_t(f32_to_bf16(o1)) << 16);
+                        pk.y = f32_to_bf16(o2) | (uint32_t(f32_to_bf16(o3)) << 16);
+                        *reinterpret_cast<uint2*>(y + (int64_t)r * ldy + c) = pk;
+                    }
+                }
+                *reinterpret_cast<float4*>(y2 + (int64_t)r * ldy2 + c) = make_float4(o0, o1, o2, o3);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) reinterpret_cast<float4*>(part + (int64_t)t * d)[j * 256 + th] = acc[j];
+}
+
 template <typename TH>
 __global__ void __launch_bounds__(256)
 pool_prefill_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_off,
@@ -513,6 +594,37 @@ void launch_pool_prefill(int n_req, int n_tiles, int d, int h_fmt, const void* h
         hipLaunchKernelGGL(pool_prefill_kernel<bf16_t>, gr, dim3(256), 0, st, d, hh, ldh, req_off, req_slot,
                            cu_tiles, part, pool_sum, pooled, pooled_bf16);
     }
+}
+
+bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles, int d, const float* x,
+                              int64_t ldx, const void* gamma, float eps, void* y, int64_t ldy, float* y2,
+                              int64_t ldy2, bool full_rows, const int32_t* req_off, const int32_t* req_slot,
+                              const int32_t* cu_tiles, float* part, float* pool_sum, float* pooled,
+                              uint16_t* pooled_bf16, hipStream_t st) {
+    const bool vec = d % 1024 == 0 && d <= 8192 && ldx % 4 == 0 && (!y || ldy % 4 == 0) && ldy2 % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(y2) % 16 == 0 && reinterpret_cast<uintptr_t>(gamma) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(part) % 16 == 0 && (d / 1024 & (d / 1024 - 1)) == 0;
+    if (!vec) return false;
+    if (n_req <= 0) return true;
+    const int V = d / 1024, fr = full_rows ? 1 : 0;
+#define OUTLETS_NP_V(TY, TG, VV)                                                                        \
+    case VV:                                                                                            \
+        hipLaunchKernelGGL((norm_pool_tiles_kernel<TY, TG, VV>), dim3(n_tiles), dim3(256), 0, st, d, n_req, x, \
+                           ldx, static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2, fr,  \
+                           req_off, cu_tiles, part);                                                    \
+        break;
+#define OUTLETS_NP(TY, TG)                                                                              \
+    switch (V) { OUTLETS_NP_V(TY, TG, 1) OUTLETS_NP_V(TY, TG, 2) OUTLETS_NP_V(TY, TG, 4) OUTLETS_NP_V(TY, TG, 8) }
+    if (act_fmt == FMT_F32) { OUTLETS_NP(float, float) }
+    else if (gamma_fmt == FMT_F32) { OUTLETS_NP(bf16_t, float) }
+    else { OUTLETS_NP(bf16_t, bf16_t) }
+#undef OUTLETS_NP
+#undef OUTLETS_NP_V
+    const dim3 gr(n_req, (d + 255) / 256);
+    hipLaunchKernelGGL(pool_prefill_kernel<float>, gr, dim3(256), 0, st, d, static_cast<const float*>(y2), ldy2,
+                       req_off, req_slot, cu_tiles, part, pool_sum, pooled, pooled_bf16);
+    return true;
 }
 
 void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,

@@ -173,6 +173,36 @@ def test_config1_full_shape_sampled_requests(variant):
     pred.close()
 
 
+def test_fused_final_norm_pooling_with_and_without_hdraft():
+    """8B shape (d = 4096, the fused final-RMSNorm + pooling path): ragged
+    32-row tiles and a 1-token request.  z must not depend on whether the
+    caller asks for h_draft (only the requests' last rows are stored then),
+    and matches the oracle."""
+    lens = [40, 1, 33, 100, 64]
+    case = make_case(1, lens=lens, n_req=len(lens))
+    say(f"case: 8B bf16, lens {lens}, prefill with and without h_draft")
+    pred = make_predictor(case, max_slots=16)
+    H = device_states(case)
+    z1, hd = pred.prefill(list(range(5)), case.lens, *H, want_hdraft=True)
+    z1, hd = tensor_to_f64(z1), tensor_to_f64(hd)
+    pred.release(list(range(5)))
+    z2, none = pred.prefill(list(range(5, 10)), case.lens, *H)
+    assert none is None
+    assert np.array_equal(tensor_to_f64(z2), z1)
+    orc = oracle_for(case)
+    O = oracle_states(case)
+    off = np.concatenate([[0], np.cumsum(case.lens)])
+    z_ref = []
+    for i in range(5):
+        zi, hi, _ = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O))
+        z_ref.append(zi)
+        assert rel_fro(hd[off[i]:off[i + 1]], hi) <= TOL_HDRAFT["bf16"], i
+    ez = z_errors(z1, z_ref)
+    say(f"  z max rel err {ez.max():.3e}")
+    assert ez.max() <= TOL_Z["bf16"], ez
+    pred.close()
+
+
 def test_packing_and_permutation_invariance():
     say("case: bf16 reduced shape, packed batch vs one-by-one vs permuted")
     case = make_case(1, lens=[7, 130, 1, 64], shape=reduced_shape(), n_req=4)
