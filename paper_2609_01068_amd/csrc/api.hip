@@ -339,12 +339,25 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
       if (c->embed_in)
           launch_embed_norm(af, c->small_fmt, T, static_cast<int>(d), c->cfg.vocab, tokens, c->w.embed,
                             c->w.gamma_emb, eps, c->e_norm, d, st); }
-    { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
-    { KTimer t(c, OUTLETS_K_ROPE_KV, st);
-      launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
-                     c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
-                     c->cfg.head_dim, st); }
+    // QKV projection; where it runs as one kernel without a K split, RoPE and
+    // the paged K/V write happen in its epilogue
+    if (gemm_qkv_rope_fusable(af, wf, T, static_cast<int>(c->qkv_dim), static_cast<int>(c->k_attn),
+                              c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim)) {
+        KTimer t(c, OUTLETS_K_QKV_GEMM, st);
+        GemmC qc = gemm_c(c->qkv, c->qkv_dim);
+        qc.rope = RopeKV{c->tok_pos, c->tok_slot, c->page_table, static_cast<int32_t>(c->max_pages),
+                         c->cfg.n_q_heads, c->cfg.n_kv_heads, static_cast<uint16_t*>(c->kpool),
+                         static_cast<uint16_t*>(c->vpool), c->cos_t, c->sin_t};
+        gemm_launch(af, wf, EPI_QKV_ROPE, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, qc, 1, st,
+                    c->splitk_ws, c->splitk_bytes);
+    } else {
+        { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
+          gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
+        { KTimer t(c, OUTLETS_K_ROPE_KV, st);
+          launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
+                         c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
+                         c->cfg.head_dim, st); }
+    }
     { KTimer t(c, OUTLETS_K_ATTN, st);
       const void* gate = c->gated ? static_cast<const char*>(c->qkv) + (c->qdim + 2 * c->kvdim) * fmt_bytes(af)
                                   : nullptr;

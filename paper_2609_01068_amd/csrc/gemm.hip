@@ -334,6 +334,109 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
             __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), rc, off, 0, 0);
         }
     };
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        // A wave's 128 columns are one head (head dim 128): q, k, v or gate.
+        // Rotate-half pairs (c, c + 64) are blocks j and j + 4 of the same
+        // lane, so the rotation is applied to the fp32 accumulators.  q and
+        // gate go to C; k (rotated) and v go straight into the KV pages
+        // (K [page][kv head][16 tokens][128], V [page][kv head][128][16]).
+        static_assert(TN == 128 && FN == 8, "one 128-wide head per wave");
+        const RopeKV& R = C.rope;
+        const int hcol0 = n0 + wn * TN, head = hcol0 / 128;
+        const int region = head < R.n_q ? 0 : (head < R.n_q + R.n_kv ? 1 : (head < R.n_q + 2 * R.n_kv ? 2 : 3));
+        const int kvh = region == 1 ? head - R.n_q : head - R.n_q - R.n_kv;
+        float sc[FN];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            sc[j] = 1.f;
+            if (E4M3) {
+                int sg, r;
+                b_row(B, hcol0 + j * 16 + l16, sg, r);
+                sc[j] = bf16_to_f32(B.scale[sg][r]);
+            }
+        }
+        bf16_t* cq = static_cast<bf16_t*>(C.c);
+        if (region == 2) {
+            // V pages hold each channel's 16 tokens contiguously: a lane's 4
+            // consecutive rows go out as one 8-byte (or two 4-byte) store per
+            // channel when they are consecutive positions on one page
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int t0 = m0 + wm * TM + i * 16 + 4 * grp;
+                int pos[4], page[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int t = min(t0 + q, M - 1);
+                    pos[q] = R.tok_pos[t];
+                    page[q] = R.page_table[(int64_t)R.tok_slot[t] * R.max_pages + (pos[q] >> 4)];
+                }
+                const bool run4 = t0 + 3 < M && page[3] == page[0] && pos[3] == pos[0] + 3 &&
+                                  page[1] == page[0] && page[2] == page[0] && pos[1] == pos[0] + 1 &&
+                                  pos[2] == pos[0] + 2;
+                const int off0 = pos[0] & 15;
+                if (run4 && (off0 & 3) == 0) {
+                    bf16_t* vb = R.vpool + ((int64_t)page[0] * R.n_kv + kvh) * 128 * 16 + off0;
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) {
+                        const float s = sc[j];
+                        uint2 pk;
+                        pk.x = f32_to_bf16(acc[i][j][0] * s) | (uint32_t(f32_to_bf16(acc[i][j][1] * s)) << 16);
+                        pk.y = f32_to_bf16(acc[i][j][2] * s) | (uint32_t(f32_to_bf16(acc[i][j][3] * s)) << 16);
+                        *reinterpret_cast<uint2*>(vb + (j * 16 + l16) * 16) = pk;
+                    }
+                } else if (run4 && (off0 & 1) == 0) {
+                    bf16_t* vb = R.vpool + ((int64_t)page[0] * R.n_kv + kvh) * 128 * 16 + off0;
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) {
+                        const float s = sc[j];
+                        uint32_t* d = reinterpret_cast<uint32_t*>(vb + (j * 16 + l16) * 16);
+                        d[0] = f32_to_bf16(acc[i][j][0] * s) | (uint32_t(f32_to_bf16(acc[i][j][1] * s)) << 16);
+                        d[1] = f32_to_bf16(acc[i][j][2] * s) | (uint32_t(f32_to_bf16(acc[i][j][3] * s)) << 16);
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (t0 + q >= M) continue;
+                        bf16_t* vb = R.vpool + ((int64_t)page[q] * R.n_kv + kvh) * 128 * 16 + (pos[q] & 15);
+#pragma unroll
+                        for (int j = 0; j < FN; ++j) vb[(j * 16 + l16) * 16] = f32_to_bf16(acc[i][j][q] * sc[j]);
+                    }
+                }
+            }
+            return;
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int t = m0 + wm * TM + i * 16 + 4 * grp + q;
+                if (t >= M) continue;
+                bf16_t* crow = cq + (int64_t)t * C.ldc + hcol0;
+                if (region == 3) {
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) crow[j * 16 + l16] = f32_to_bf16(acc[i][j][q] * sc[j]);
+                    continue;
+                }
+                const int pos = R.tok_pos[t];
+                const float* cr = R.cos_t + (int64_t)pos * 64;
+                const float* sr = R.sin_t + (int64_t)pos * 64;
+                bf16_t* dst = crow;
+                if (region == 1) {
+                    const int page = R.page_table[(int64_t)R.tok_slot[t] * R.max_pages + (pos >> 4)];
+                    dst = R.kpool + (((int64_t)page * R.n_kv + kvh) * 16 + (pos & 15)) * 128;
+                }
+#pragma unroll
+                for (int j = 0; j < FN / 2; ++j) {
+                    const int c = j * 16 + l16;
+                    const float x1 = acc[i][j][q] * sc[j], x2 = acc[i][j + 4][q] * sc[j + 4];
+                    const float cs = cr[c], sn = sr[c];
+                    dst[c] = f32_to_bf16(x1 * cs - x2 * sn);
+                    dst[c + 64] = f32_to_bf16(x2 * cs + x1 * sn);
+                }
+            }
+        }
+        return;
+    }
     // The residual may alias the output (in-place update): the residuals of
     // JB column blocks are loaded before any of their stores, so the loads
     // overlap instead of each block waiting out a full memory latency.
@@ -569,7 +672,7 @@ void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& 
     const int W = device_cus();
     const int full = T / W, tail = T % W;
     int S = 1;
-    if (splits == 1 && EPI != EPI_PARTIAL && full >= 1 && full <= 64 && tail > 0 && ws) {
+    if (splits == 1 && EPI != EPI_PARTIAL && EPI != EPI_QKV_ROPE && full >= 1 && full <= 64 && tail > 0 && ws) {
         S = std::min({16, W / tail, (K / BK) / 4});
         if ((size_t)S * tail * 65536 * sizeof(float) > ws_bytes) S = 1;
     }
@@ -615,6 +718,11 @@ int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
     return best;
 }
 
+bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int M, int N, int K, int n_q, int n_kv, int hd) {
+    return act_fmt == FMT_BF16 && w_fmt != FMT_F32 && hd == 128 && N % 256 == 0 && (n_q * hd) % 256 == 0 &&
+           (n_kv * hd) % 128 == 0 && gemm_splitk_plan(w_fmt, EPI_STORE_ACT, M, N, K) == 1;
+}
+
 int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
                const GemmB& b, int splits, const char** why) {
     if (M <= 0 || N <= 0 || K <= 0 || splits <= 0) { *why = "gemm: empty shape"; return OUTLETS_ERR_INVALID_ARG; }
@@ -645,7 +753,7 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  size_t ws_bytes) {
     // Small M: split K over more workgroups into fp32 partials, then reduce in
     // a fixed order and apply the epilogue (deterministic).
-    const int sk = (splits == 1) ? gemm_splitk_plan(w_fmt, epi, M, N, K) : 1;
+    const int sk = (splits == 1 && epi != EPI_QKV_ROPE) ? gemm_splitk_plan(w_fmt, epi, M, N, K) : 1;
     if (sk > 1 && ws && (size_t)sk * M * N * sizeof(float) <= ws_bytes) {
         GemmC pc{};
         pc.c = ws;
@@ -684,6 +792,7 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
         OUTLETS_GEMM_CASE(EPI_RESID_F32)
         OUTLETS_GEMM_CASE(EPI_SWIGLU)
         OUTLETS_GEMM_CASE(EPI_PARTIAL)
+        OUTLETS_GEMM_CASE(EPI_QKV_ROPE)
     }
 #undef OUTLETS_GEMM_CASE
 }

@@ -37,7 +37,22 @@ enum Epilogue : int {
     EPI_RESID_F32 = 2,  // C (f32) = resid + acc   (C may alias resid)
     EPI_SWIGLU = 3,     // C (act) [M, N/2] = silu(gate) * up   (requires paired B)
     EPI_PARTIAL = 4,    // C (f32) + split * split_stride = acc over the split's K range
-    EPI_PARTIAL_TILE = 5  // internal: per-tile fp32 blocks of the K-split tail of a large GEMM
+    EPI_PARTIAL_TILE = 5, // internal: per-tile fp32 blocks of the K-split tail of a large GEMM
+    EPI_QKV_ROPE = 6    // q|k|v|gate columns (bf16, head dim 128): q rotated and stored to C,
+                        // k rotated and v written into their KV pages, gate stored to C
+};
+
+// Rotary embedding and paged K/V write of EPI_QKV_ROPE (rows are tokens):
+// the layout of launch_rope_kv.
+struct RopeKV {
+    const int32_t* tok_pos;
+    const int32_t* tok_slot;
+    const int32_t* page_table;
+    int32_t max_pages, n_q, n_kv;
+    uint16_t* kpool;
+    uint16_t* vpool;
+    const float* cos_t;
+    const float* sin_t;
 };
 
 struct GemmC {
@@ -46,6 +61,7 @@ struct GemmC {
     const float* resid;
     int64_t ldr;
     int64_t split_stride;
+    RopeKV rope;
 };
 
 enum Fmt : int { FMT_F32 = 0, FMT_BF16 = 1, FMT_E4M3 = 2 };
@@ -62,6 +78,9 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st,
                  float* ws = nullptr, size_t ws_bytes = 0);
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
+// Whether gemm_launch takes EPI_QKV_ROPE for this shape (one kernel, no K
+// split); otherwise store with EPI_STORE_ACT and run launch_rope_kv.
+bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int M, int N, int K, int n_q, int n_kv, int hd);
 
 // ---------------------------------------------------------------- elementwise / rows
 // Per-call token metadata from per-request arrays:

@@ -203,6 +203,44 @@ def test_fused_final_norm_pooling_with_and_without_hdraft():
     pred.close()
 
 
+def test_qkv_rope_epilogue_matches_separate_rope_kernel():
+    """8B shape: a 100-token request prefilled inside a 3,100-token batch
+    (the QKV GEMM has >= 256 tiles: RoPE and the K/V page writes run in its
+    epilogue) and alone (split-K QKV GEMM, then the separate RoPE/KV
+    kernel).  Its z, h_draft and its K/V page contents agree; rounding
+    differs (the fused path rounds q and k once, after the rotation)."""
+    import torch
+    from paper_2609_01068_amd import binding as B
+    lens = [100, 1500, 1500]
+    case = make_case(1, lens=lens, n_req=len(lens))
+    say(f"case: 8B bf16, lens {lens} (fused QKV epilogue) vs request 0 alone")
+    pred = make_predictor(case, max_slots=4, num_pages=4 * (1600 // 16 + 8))
+    H = device_states(case)
+    z_all, hd_all = pred.prefill([0, 1, 2], case.lens, *H, want_hdraft=True)
+    z_all, hd_all = tensor_to_f64(z_all), tensor_to_f64(hd_all)
+
+    def pages_of(slot, n):
+        table = pred.meta(B.OUTLETS_META_PAGE_TABLE).reshape(pred.cfg.max_slots, -1)
+        ids = table[slot, :(n + 15) // 16]
+        assert np.all(ids >= 0)
+        kp = pred.buffer("K_POOL", torch.bfloat16).float().cpu().numpy().reshape(-1, 8, 16, 128)
+        vp = pred.buffer("V_POOL", torch.bfloat16).float().cpu().numpy().reshape(-1, 8, 128, 16)
+        k = kp[ids].transpose(0, 2, 1, 3).reshape(-1, 8, 128)[:n]          # [token, kv head, ch]
+        v = vp[ids].transpose(0, 3, 1, 2).reshape(-1, 8, 128)[:n]
+        return k.astype(np.float64), v.astype(np.float64)
+
+    k_all, v_all = pages_of(0, 100)
+    z1, hd1 = pred.prefill([3], case.lens[:1], *[x[:100].contiguous() for x in H], want_hdraft=True)
+    z1, hd1 = tensor_to_f64(z1), tensor_to_f64(hd1)
+    k1, v1 = pages_of(3, 100)
+    ek, ev = rel_fro(k_all, k1), rel_fro(v_all, v1)
+    eh = rel_fro(hd_all[:100], hd1)
+    say(f"  K pages rel err {ek:.2e}, V pages {ev:.2e}, h_draft {eh:.2e}, z {z_all[0]:.6f} vs {z1[0]:.6f}")
+    assert ek <= 1e-2 and ev <= 1e-2 and eh <= 1e-2
+    assert abs(z_all[0] - z1[0]) <= 1e-2 * max(abs(z1[0]), float(np.sqrt(np.mean(z_all ** 2))))
+    pred.close()
+
+
 def test_packing_and_permutation_invariance():
     say("case: bf16 reduced shape, packed batch vs one-by-one vs permuted")
     case = make_case(1, lens=[7, 130, 1, 64], shape=reduced_shape(), n_req=4)
