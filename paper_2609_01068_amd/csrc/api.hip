@@ -339,10 +339,10 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
       if (c->embed_in)
           launch_embed_norm(af, c->small_fmt, T, static_cast<int>(d), c->cfg.vocab, tokens, c->w.embed,
                             c->w.gamma_emb, eps, c->e_norm, d, st); }
-    // QKV projection; where it runs as one kernel without a K split, RoPE and
-    // the paged K/V write happen in its epilogue
-    if (gemm_qkv_rope_fusable(af, wf, T, static_cast<int>(c->qkv_dim), static_cast<int>(c->k_attn),
-                              c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim)) {
+    // QKV projection; with bf16 activations and head dim 128, RoPE and the
+    // paged K/V write happen in its epilogue (or in its split-K reduce)
+    if (gemm_qkv_rope_fusable(af, wf, c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim,
+                              static_cast<int>(c->qkv_dim))) {
         KTimer t(c, OUTLETS_K_QKV_GEMM, st);
         GemmC qc = gemm_c(c->qkv, c->qkv_dim);
         qc.rope = RopeKV{c->tok_pos, c->tok_slot, c->page_table, static_cast<int32_t>(c->max_pages),
@@ -585,7 +585,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     const int64_t max_chunks = Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages());
     c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
     if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
-        ALLOC(c->decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * (cfg->head_dim + 2));
+        ALLOC(c->decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
     ALLOC(c->pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
     {
         // split-K scratch: the largest plan over the layer's GEMMs for M up to 1024

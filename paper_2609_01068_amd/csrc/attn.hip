@@ -407,6 +407,7 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
 #define OUTLETS_DECODE_PPI 2
 #endif
 constexpr int kDecodeChunk = OUTLETS_DECODE_CHUNK;
+constexpr int kDecodeRec = 128 + 4;   // floats per partial record: m, l, 2 pad, o[128]
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -524,38 +525,53 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
             }
         }
     }
-    // partial record: [m, l, o[0..HD)] per (work item, KV head, query head)
+    // partial record [m, l, -, -, o[0..HD)] per (work item, query head
+    // g G + col); o starts 16-byte aligned
     if (col < G) {
-        float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * (HD + 2);
+        float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * kDecodeRec;
         if (grp == 0) { rec[0] = m; rec[1] = l; }
 #pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) rec[2 + 16 * cb + 4 * grp + i] = o[cb][i];
+        for (int cb = 0; cb < HD / 16; ++cb) *reinterpret_cast<f32x4*>(rec + 4 + 16 * cb + 4 * grp) = o[cb];
     }
 }
 
-// grid (n_req, n_q), 128 threads: merge the request's chunk partials in order.
-template <int G>
-__global__ void __launch_bounds__(128)
-attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_kv, bf16_t* out, int64_t ldo,
+// Merge of a request's chunk partials, in chunk order (deterministic).
+// Grid (n_req, ceil(n_q / 8)), 256 threads: 32 threads per query head, 4
+// channels each.  The chunks' maxima give the common reference M; chunk c's
+// o and l enter with weight 2^(m_c - M).
+__global__ void __launch_bounds__(256)
+attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_q, bf16_t* out, int64_t ldo,
                     const bf16_t* gate, int64_t ldg) {
     constexpr int HD = 128;
-    const int r = blockIdx.x, h = blockIdx.y, ch = threadIdx.x;
-    const int g = h / G, col = h % G;
+    const int r = blockIdx.x, h = blockIdx.y * 8 + (threadIdx.x >> 5), ch = (threadIdx.x & 31) * 4;
+    if (h >= n_q) return;
     const int c0 = cu_chunks[r], c1 = cu_chunks[r + 1];
     float M = -INFINITY;
-    for (int c = c0; c < c1; ++c) M = fmaxf(M, part[(((int64_t)c * n_kv + g) * G + col) * (HD + 2)]);
-    float L = 0.f, O = 0.f;
+    for (int c = c0; c < c1; ++c) M = fmaxf(M, part[((int64_t)c * n_q + h) * kDecodeRec]);
+    float L = 0.f;
+    f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
     for (int c = c0; c < c1; ++c) {
-        const float* rec = part + (((int64_t)c * n_kv + g) * G + col) * (HD + 2);
-        const float f = fast_exp2(rec[0] - M);
-        L = fmaf(rec[1], f, L);
-        O = fmaf(rec[2 + ch], f, O);
+        const float* rec = part + ((int64_t)c * n_q + h) * kDecodeRec;
+        const float2 ml = *reinterpret_cast<const float2*>(rec);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(rec + 4 + ch);
+        const float f = fast_exp2(ml.x - M);
+        L = fmaf(ml.y, f, L);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) O[j] = fmaf(v[j], f, O[j]);
     }
-    float y = O / L;
-    if (gate) y *= sigmoid_f(bf16_to_f32(gate[(int64_t)r * ldg + (int64_t)h * HD + ch]));
-    out[(int64_t)r * ldo + (int64_t)h * HD + ch] = f32_to_bf16(y);
+    float y[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = O[j] / L;
+    const int64_t col0 = (int64_t)h * HD + ch;
+    if (gate) {
+        const bf16_t* gr = gate + (int64_t)r * ldg + col0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) y[j] *= sigmoid_f(bf16_to_f32(gr[j]));
+    }
+    *reinterpret_cast<uint2*>(out + (int64_t)r * ldo + col0) =
+        make_uint2(f32_to_bf16(y[0]) | (uint32_t(f32_to_bf16(y[1])) << 16),
+                   f32_to_bf16(y[2]) | (uint32_t(f32_to_bf16(y[3])) << 16));
 }
 
 template <typename T, int HD>
@@ -617,6 +633,7 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
 }
 
 int attn_decode_chunk_pages() { return kDecodeChunk; }
+int attn_decode_record_floats() { return kDecodeRec; }
 
 void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
@@ -632,9 +649,6 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
                            static_cast<const bf16_t*>(q), ldq, work, req_slot, req_start,          \
                            page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
                            static_cast<const bf16_t*>(vpool), n_kv, qscale, part);                 \
-        hipLaunchKernelGGL((attn_decode_combine<GG>), dim3(n_req, n_q), dim3(128), 0, st,          \
-                           cu_chunks, part, n_kv, static_cast<bf16_t*>(out), ldo,                  \
-                           static_cast<const bf16_t*>(gate), ldq);                                 \
         break;
     switch (G) {
         OUTLETS_DEC_G(1)
@@ -643,6 +657,8 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
         OUTLETS_DEC_G(8)
     }
 #undef OUTLETS_DEC_G
+    hipLaunchKernelGGL(attn_decode_combine, dim3(n_req, (n_q + 7) / 8), dim3(256), 0, st, cu_chunks, part, n_q,
+                       static_cast<bf16_t*>(out), ldo, static_cast<const bf16_t*>(gate), ldq);
 }
 
 bool attn_supported(int n_q, int n_kv, int hd) {

@@ -579,6 +579,48 @@ splitk_reduce(int M, int N, int S, const float* part, GemmC C) {
         static_cast<float*>(C.c)[(int64_t)m * C.ldc + n] = C.resid[(int64_t)m * C.ldr + n] + v;
 }
 
+// Split-K reduce of the QKV GEMM with the EPI_QKV_ROPE epilogue: one thread
+// per (token, 128-wide head, channel pair c, c + 64); the pair is summed over
+// the splits in order, then rotated (q, k) and stored like the epilogue does.
+__global__ void __launch_bounds__(256)
+splitk_reduce_qkv_rope(int M, int N, int S, const float* part, GemmC C) {
+    const RopeKV& R = C.rope;
+    const int heads = N / 128;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)M * heads * 64) return;
+    const int c = static_cast<int>(idx & 63);
+    const int64_t th = idx >> 6;
+    const int head = static_cast<int>(th % heads), t = static_cast<int>(th / heads);
+    const int64_t plane = (int64_t)M * N, e = (int64_t)t * N + head * 128 + c;
+    float x1 = 0.f, x2 = 0.f;
+    for (int sp = 0; sp < S; ++sp) {
+        x1 += part[sp * plane + e];
+        x2 += part[sp * plane + e + 64];
+    }
+    const int region = head < R.n_q ? 0 : (head < R.n_q + R.n_kv ? 1 : (head < R.n_q + 2 * R.n_kv ? 2 : 3));
+    bf16_t* dst = static_cast<bf16_t*>(C.c) + (int64_t)t * C.ldc + head * 128;
+    if (region == 3) {
+        dst[c] = f32_to_bf16(x1);
+        dst[c + 64] = f32_to_bf16(x2);
+        return;
+    }
+    const int pos = R.tok_pos[t];
+    const int kvh = region == 1 ? head - R.n_q : head - R.n_q - R.n_kv;
+    if (region > 0) {
+        const int page = R.page_table[(int64_t)R.tok_slot[t] * R.max_pages + (pos >> 4)];
+        if (region == 2) {
+            bf16_t* vb = R.vpool + ((int64_t)page * R.n_kv + kvh) * 128 * 16 + (pos & 15);
+            vb[c * 16] = f32_to_bf16(x1);
+            vb[(c + 64) * 16] = f32_to_bf16(x2);
+            return;
+        }
+        dst = R.kpool + (((int64_t)page * R.n_kv + kvh) * 16 + (pos & 15)) * 128;
+    }
+    const float cs = R.cos_t[(int64_t)pos * 64 + c], sn = R.sin_t[(int64_t)pos * 64 + c];
+    dst[c] = f32_to_bf16(x1 * cs - x2 * sn);
+    dst[c + 64] = f32_to_bf16(x2 * cs + x1 * sn);
+}
+
 // ---------------------------------------------------------------- fp32 VALU path
 template <int EPI>
 __global__ void __launch_bounds__(256)
@@ -746,9 +788,9 @@ int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
     return best;
 }
 
-bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int M, int N, int K, int n_q, int n_kv, int hd) {
+bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int n_q, int n_kv, int hd, int N) {
     return act_fmt == FMT_BF16 && w_fmt != FMT_F32 && hd == 128 && N % 256 == 0 && (n_q * hd) % 256 == 0 &&
-           (n_kv * hd) % 128 == 0 && gemm_splitk_plan(w_fmt, EPI_STORE_ACT, M, N, K) == 1;
+           (n_kv * hd) % 128 == 0;
 }
 
 int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
@@ -781,7 +823,7 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  size_t ws_bytes) {
     // Small M: split K over more workgroups into fp32 partials, then reduce in
     // a fixed order and apply the epilogue (deterministic).
-    const int sk = (splits == 1 && epi != EPI_QKV_ROPE) ? gemm_splitk_plan(w_fmt, epi, M, N, K) : 1;
+    const int sk = splits == 1 ? gemm_splitk_plan(w_fmt, epi == EPI_QKV_ROPE ? EPI_STORE_ACT : epi, M, N, K) : 1;
     if (sk > 1 && ws && (size_t)sk * M * N * sizeof(float) <= ws_bytes) {
         GemmC pc{};
         pc.c = ws;
@@ -796,6 +838,10 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
             case EPI_STORE_ACT: hipLaunchKernelGGL((splitk_reduce<EPI_STORE_ACT, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
             case EPI_RESID_F32: hipLaunchKernelGGL((splitk_reduce<EPI_RESID_F32, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
             case EPI_SWIGLU: hipLaunchKernelGGL((splitk_reduce<EPI_SWIGLU, bf16_t>), grid, dim3(256), 0, st, M, N, sk, ws, c); break;
+            case EPI_QKV_ROPE:
+                hipLaunchKernelGGL(splitk_reduce_qkv_rope, dim3((unsigned)(((int64_t)M * (N / 2) + 255) / 256)), dim3(256),
+                                   0, st, M, N, sk, ws, c);
+                break;
         }
         return;
     }

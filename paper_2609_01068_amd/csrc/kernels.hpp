@@ -78,9 +78,11 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st,
                  float* ws = nullptr, size_t ws_bytes = 0);
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
-// Whether gemm_launch takes EPI_QKV_ROPE for this shape (one kernel, no K
-// split); otherwise store with EPI_STORE_ACT and run launch_rope_kv.
-bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int M, int N, int K, int n_q, int n_kv, int hd);
+// Whether gemm_launch takes EPI_QKV_ROPE for this layout (bf16 activations,
+// head dim 128; N = q|k|v[|gate] columns); otherwise store with
+// EPI_STORE_ACT and run launch_rope_kv.  With a K split the reduce kernel
+// applies the same epilogue.
+bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int n_q, int n_kv, int hd, int N);
 
 // ---------------------------------------------------------------- elementwise / rows
 // Per-call token metadata from per-request arrays:
@@ -130,8 +132,10 @@ void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64
 // Decode attention (bf16, hd 128, one query per request, split over chunks of
 // attn_decode_chunk_pages() pages): work[2 i], work[2 i + 1] = (request, chunk);
 // cu_chunks[n_req + 1] = first work item of each request; part = fp32 scratch
-// [n_work, n_kv, G, 130].  Queries are row r of q for request r.
+// [n_work, n_q, attn_decode_record_floats()].  Queries are row r of q for
+// request r.
 int attn_decode_chunk_pages();
+int attn_decode_record_floats();
 void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,

@@ -203,17 +203,17 @@ def test_fused_final_norm_pooling_with_and_without_hdraft():
     pred.close()
 
 
-def test_qkv_rope_epilogue_matches_separate_rope_kernel():
+def test_qkv_rope_epilogue_matches_split_k_reduce():
     """8B shape: a 100-token request prefilled inside a 3,100-token batch
     (the QKV GEMM has >= 256 tiles: RoPE and the K/V page writes run in its
-    epilogue) and alone (split-K QKV GEMM, then the separate RoPE/KV
-    kernel).  Its z, h_draft and its K/V page contents agree; rounding
-    differs (the fused path rounds q and k once, after the rotation)."""
+    epilogue) and alone (the QKV GEMM splits K; its reduce kernel sums the
+    fp32 partials and applies RoPE and the page writes).  Its z, h_draft and
+    its K/V page contents agree up to the split's summation order."""
     import torch
     from paper_2609_01068_amd import binding as B
     lens = [100, 1500, 1500]
     case = make_case(1, lens=lens, n_req=len(lens))
-    say(f"case: 8B bf16, lens {lens} (fused QKV epilogue) vs request 0 alone")
+    say(f"case: 8B bf16, lens {lens} (QKV epilogue) vs request 0 alone (split-K reduce)")
     pred = make_predictor(case, max_slots=4, num_pages=4 * (1600 // 16 + 8))
     H = device_states(case)
     z_all, hd_all = pred.prefill([0, 1, 2], case.lens, *H, want_hdraft=True)
