@@ -41,7 +41,7 @@ int hip_fail(hipError_t e, const char* what) {
 
 size_t fmt_bytes(int fmt) { return fmt == FMT_F32 ? 4 : (fmt == FMT_BF16 ? 2 : 1); }
 
-constexpr int kHeadSplits = 8;
+constexpr int kHeadSplits = 8;      // K splits of the length head GEMM (at least)
 
 }  // namespace
 
@@ -290,6 +290,20 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
 
 // Draft model head input: the newest token's h_draft is the second half of
 // each pooled row ([mean ; newest]); bf16 weights read its hi/lo split.
+// K splits of the head GEMM over `rows` A rows: kHeadSplits, doubled up to
+// 32 while the workgroups fill at most half the CUs and every split keeps at
+// least 4 K slices of 64 (the fp32 path keeps kHeadSplits).  Measured: 32
+// splits for 64 rows take the head from 0.033 to 0.024 ms; 16 instead of 8
+// for 1,024 rows is slower (the finish reads twice the partials).
+int head_splits(const outlets_ctx* c, int rows) {
+    int s = kHeadSplits;
+    if (c->w_fmt == FMT_F32) return s;
+    const int tiles = ((rows + 255) / 256) * static_cast<int>((c->H1 + 255) / 256);
+    const int kslices = static_cast<int>(2 * c->d / 64);
+    while (s < 32 && tiles * 2 * s <= gemm_device_cus() / 2 && kslices / (2 * s) >= 4) s *= 2;
+    return s;
+}
+
 GemmA lm_input(const outlets_ctx* c) {
     return (c->w_fmt == FMT_F32) ? gemm_a(c->pooled + c->d, 2 * c->d, c->d)
                                  : gemm_a(c->pooled_bf16 + c->d, 2 * c->d, c->d);
@@ -393,6 +407,13 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
             af, c->small_fmt, n, c->n_tiles, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d,
             hdraft_out != nullptr || c->cfg.keep_intermediates != 0, req_off, req_slot, c->d_meta + c->tiles_off,
             c->pool_part, c->pool_sum, c->pooled, pb, st);
+    } else {
+        // steps (one row per request): the f32 h_draft rows are kept only
+        // with intermediates
+        KTimer t(c, OUTLETS_K_POOL, st);
+        fused_pool = launch_norm_pool_step(af, c->small_fmt, n, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d,
+                                           c->cfg.keep_intermediates ? c->r_h : nullptr, d, req_slot, req_start,
+                                           c->pool_sum, c->pooled, pb, st);
     }
     if (!fused_pool) {
         { KTimer t(c, OUTLETS_K_NORM, st);
@@ -409,9 +430,10 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
     const int head_rows = (wf == FMT_F32) ? n : 2 * n;
     GemmC hc = gemm_c(c->head_part, c->H1);
     hc.split_stride = static_cast<int64_t>(head_rows) * c->H1;
+    const int hs = head_splits(c, head_rows);
     { KTimer t(c, OUTLETS_K_HEAD, st);
-      gemm_launch(af, hf, EPI_PARTIAL, head_rows, c->H1, 2 * d, g.a_head, g.b_head, hc, kHeadSplits, st);
-      launch_head_finish(c->small_fmt, n, c->H1, kHeadSplits, c->head_part, c->w.head_b1, c->w.head_w2,
+      gemm_launch(af, hf, EPI_PARTIAL, head_rows, c->H1, 2 * d, g.a_head, g.b_head, hc, hs, st);
+      launch_head_finish(c->small_fmt, n, c->H1, hs, c->head_part, c->w.head_b1, c->w.head_w2,
                          c->w.head_b2, z_out, st); }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -578,7 +600,15 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->mlp, ab * Tm * c->F);
     ALLOC(c->pooled, sizeof(float) * Bm * 2 * c->d);
     ALLOC(c->pooled_bf16, sizeof(uint16_t) * 2 * Bm * 2 * c->d);
-    ALLOC(c->head_part, sizeof(float) * kHeadSplits * 2 * Bm * c->H1);
+    {
+        // head partials: the largest splits x rows over every batch size
+        int64_t most = 0;
+        for (int64_t b = 1; b <= Bm; ++b) {
+            const int rows = static_cast<int>((c->w_fmt == FMT_F32 ? 1 : 2) * b);
+            most = std::max<int64_t>(most, static_cast<int64_t>(head_splits(c.get(), rows)) * rows);
+        }
+        ALLOC(c->head_part, sizeof(float) * most * c->H1);
+    }
     ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->last_idx, sizeof(int32_t) * Bm);
@@ -777,8 +807,9 @@ int run_probe_head(outlets_ctx* c, int n, float* z_out, hipStream_t st) {
     const int rows = (wf == FMT_F32) ? n : 2 * n;
     GemmC hc = gemm_c(c->head_part, c->H1);
     hc.split_stride = static_cast<int64_t>(rows) * c->H1;
-    gemm_launch(af, hf, EPI_PARTIAL, rows, c->H1, 2 * d, a, b, hc, kHeadSplits, st);
-    launch_head_finish(c->small_fmt, n, c->H1, kHeadSplits, c->head_part, c->w.probe_b1, c->w.probe_w2,
+    const int hs = head_splits(c, rows);
+    gemm_launch(af, hf, EPI_PARTIAL, rows, c->H1, 2 * d, a, b, hc, hs, st);
+    launch_head_finish(c->small_fmt, n, c->H1, hs, c->head_part, c->w.probe_b1, c->w.probe_w2,
                        c->w.probe_b2, z_out, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");

@@ -179,8 +179,10 @@ constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? OUTLETS_PREFIL
 // rho of the score MFMA reads key pi(rho), pi swapping bits 2 and 3 of rho:
 // with the 32x32 output layout (row = 8 (r / 4) + 4 half + r % 4 for
 // accumulator element r) element r then holds key 16 (r / 8) + 8 half + r % 8.
-// Values are staged as V^T [hd][64 keys], which the transposed value pages
-// make a plain 16-byte copy.
+// Values are staged as the tile's four transposed value pages, [page][hd][16
+// keys], each a plain copy of its page block.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ uint4 zero_tail_bf16x8(uint4 v, int valid) {
     // keep the first `valid` (0..8) bf16 elements of v
     uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -238,35 +240,45 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
     const int arow_key = (l32 & 19) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
 
     // DMA of one 64-key tile: K rows (key, 16 chunks of 8 channels, chunk c at
-    // c ^ key%16) and V^T rows (channel, 8 chunks of 8 keys, chunk c at
-    // c ^ (channel/2)%8).  The tile's four page ids are uniform (scalar
-    // loads); pages past the prompt's last one repeat it.  Keys past the
-    // prompt are masked out of the scores and their (finite) rows get weight 0.
+    // c ^ key%16) and the four V^T page blocks as they are in the pool.  Copy
+    // cp (1 KiB) is K keys 4 cp .. 4 cp + 3 and V channels 32 (cp % 4) ..
+    // +31 of the tile's page cp / 4, so every copy reads one page: its id is
+    // uniform (read-first-lane) and the address is a scalar base plus a
+    // 32-bit lane offset.  Page ids are loaded one tile ahead; pages past the
+    // prompt's last one repeat it.  Keys past the prompt are masked out of
+    // the scores and their (finite) rows get weight 0.
     const int wu = __builtin_amdgcn_readfirstlane(w);
-    auto issue = [&](int kt, int stage) {
-        char* base = lds + stage * STAGE;
-        int pg[4];
+    // this wave's copies cover PPW pages of a tile, starting at page q0
+    constexpr int PPW = KCP >= 4 ? KCP / 4 : 1;
+    const int q0 = (wu * KCP) >> 2;
+    auto load_pages = [&](int kt, int* pg) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pg[j] = prow[min(4 * kt + j, last_page)];
+        for (int i = 0; i < PPW; ++i) pg[i] = prow[min(4 * kt + q0 + i, last_page)];
+    };
+    auto issue = [&](const int* pgv, int stage) {
+        char* base = lds + stage * STAGE;
+        int ps[PPW];
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) ps[i] = __builtin_amdgcn_readfirstlane(pgv[i]);
 #pragma unroll
         for (int j = 0; j < KCP; ++j) {
-            const int cp = wu * KCP + j;             // 4 keys per copy, all on page cp / 4
-            const int key = cp * 4 + (lane >> 4);
-            const int c = (lane & 15) ^ (key & 15);
-            const bf16_t* src = kpool + ((int64_t)pg[cp >> 2] * n_kv + g) * (16 * HD);
-            dma_16(src + (key & 15) * HD + c * 8, base + cp * 1024);
+            const int cp = wu * KCP + j;
+            const int page = ps[KCP >= 4 ? j >> 2 : 0];
+            const int key = (cp & 3) * 4 + (lane >> 4);          // key within the page
+            const int c = (lane & 15) ^ key;
+            const bf16_t* src = kpool + ((int64_t)page * n_kv + g) * (16 * HD);
+            dma_16(src + (key * HD + c * 8), base + cp * 1024);
         }
 #pragma unroll
         for (int j = 0; j < KCP; ++j) {
-            const int cp = wu * KCP + j;             // 8 channels per copy
-            const int ch = cp * 8 + (lane >> 3);
-            const int c = (lane & 7) ^ ((ch >> 1) & 7);
-            const int q2 = c >> 1;
-            const int page = q2 == 0 ? pg[0] : q2 == 1 ? pg[1] : q2 == 2 ? pg[2] : pg[3];
+            const int cp = wu * KCP + j;
+            const int page = ps[KCP >= 4 ? j >> 2 : 0];
             const bf16_t* src = vpool + ((int64_t)page * n_kv + g) * (HD * 16);
-            dma_16(src + ch * 16 + (c & 1) * 8, base + KB + cp * 1024);
+            dma_16(src + ((cp & 3) * 512 + lane * 8), base + KB + cp * 1024);
         }
     };
+
+    int pgn[PPW];   // this wave's page ids of the next tile to copy
 
     // One 64-key tile.  MASKED: apply the causal mask (tiles holding a key
     // past the tile's first query); tiles wholly before it skip the mask.
@@ -276,7 +288,8 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
         constexpr bool MASKED = decltype(masked_tag)::value;
         wait_vm0();
         block_barrier();      // tile kt is in LDS; every wave is done with tile kt-1
-        issue(min(kt + 1, ntiles - 1), (kt + 1) & 1);
+        issue(pgn, (kt + 1) & 1);                       // tile min(kt + 1, ntiles - 1)
+        load_pages(min(kt + 2, ntiles - 1), pgn);
         const char* ks = lds + (kt & 1) * STAGE;
         const char* vs = ks + KB;
         const int k0 = kt * BKV;
@@ -323,35 +336,48 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
                     for (int e = 0; e < 16; ++e) o[qb][b][e] *= corr;
             }
             const float nmn = -m[qb];
-            float ps = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const float p = fast_exp2(fmaf(sacc[kb][e], qscale, nmn));
-                    sacc[kb][e] = p;
-                    ps += p;
+                for (int e = 0; e < 16; ++e) sacc[kb][e] = fast_exp2(fmaf(sacc[kb][e], qscale, nmn));
+            // The probabilities enter the PV product as bf16; the row sum adds
+            // the same bf16 values, two per dot2 instruction, so the output is
+            // a convex combination of the value rows.
+            bf16x8 pbs[2][2];
+            float ps = 0.f;
+            const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pbs[kb][u][e] = static_cast<__bf16>(sacc[kb][8 * u + e]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const bf16x2 pr = {pbs[kb][u][2 * e], pbs[kb][u][2 * e + 1]};
+                        ps = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ps, false);
+                    }
                 }
             lsum[qb] += ps + __shfl_xor(ps, 32, 64);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
-                    bf16x8 pb;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(sacc[kb][8 * u + e]);
+                    const bf16x8 pb = pbs[kb][u];
                     const int ch = 4 * kb + 2 * u + hf;
 #pragma unroll
                     for (int b = 0; b < NB; ++b) {
                         const int row = 32 * b + l32;
-                        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vs + row * 128 + ((ch ^ ((row >> 1) & 7)) << 4)));
+                        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vs + (ch >> 1) * 4096 + row * 32 + (ch & 1) * 16));
                         o[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[qb][b], 0, 0, 0);
                     }
                 }
         }
     };
 
-    issue(0, 0);
+    load_pages(0, pgn);
+    issue(pgn, 0);
+    load_pages(min(1, ntiles - 1), pgn);
     // tiles whose last key (64 kt + 63) is at or before the first query qs
     const int nfull = min(ntiles, (qs + 1) / BKV);
     for (int kt = 0; kt < nfull; ++kt) tile(kt, std::false_type{});

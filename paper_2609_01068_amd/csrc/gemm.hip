@@ -768,6 +768,8 @@ void launch_f32(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC
 
 }  // namespace
 
+int gemm_device_cus() { return device_cus(); }
+
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
     if (w_fmt == FMT_F32 || epi == EPI_PARTIAL) return 1;
     const int tiles = ((M + 255) / 256) * (N / 256);

@@ -78,6 +78,7 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st,
                  float* ws = nullptr, size_t ws_bytes = 0);
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
+int gemm_device_cus();   // compute units of the current device
 // Whether gemm_launch takes EPI_QKV_ROPE for this layout (bf16 activations,
 // head dim 128; N = q|k|v[|gate] columns); otherwise store with
 // EPI_STORE_ACT and run launch_rope_kv.  With a K split the reduce kernel
@@ -167,6 +168,14 @@ bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles
                               int64_t ldy2, bool full_rows, const int32_t* req_off, const int32_t* req_slot,
                               const int32_t* cu_tiles, float* part, float* pool_sum, float* pooled,
                               uint16_t* pooled_bf16, hipStream_t st);
+// Decode step: final RMSNorm of x[i] (i = request) fused with its pooling;
+// y (act) / y2 (f32) receive the normed rows when non-null.  Returns false,
+// launching nothing, for shapes the fused kernel does not take (as
+// launch_norm_pool_prefill).
+bool launch_norm_pool_step(int act_fmt, int gamma_fmt, int n_req, int d, const float* x, int64_t ldx,
+                           const void* gamma, float eps, void* y, int64_t ldy, float* y2, int64_t ldy2,
+                           const int32_t* req_slot, const int32_t* req_start, float* pool_sum, float* pooled,
+                           uint16_t* pooled_bf16, hipStream_t st);
 // Step pooling: pool_sum[slot] += h[i]; pooled[i] = [pool_sum / (start + 1) ; h[i]].
 void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,

@@ -403,6 +403,85 @@ pool_step_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_slot,
     }
 }
 
+// Decode step: final RMSNorm of request i's new row x[i] and its pooling in
+// one pass: one block of NT threads per request, V float4 per thread (NT V =
+// d / 4; the few rows of a step need wide blocks to keep the CUs busy).  The
+// scaling and the pooling arithmetic are rmsnorm_vec_kernel's and
+// pool_step_kernel's; the sum of squares is taken over NT partial sums.
+// y / y2 (the h_draft row) are stored only when non-null.
+template <typename TY, typename TG, int NT, int V>
+__global__ void __launch_bounds__(NT)
+norm_pool_step_kernel(int d, int n_req, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
+                      int64_t ldy, float* y2, int64_t ldy2, const int32_t* req_slot, const int32_t* req_start,
+                      float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
+    __shared__ float red[NT / 64];
+    const int64_t row = blockIdx.x;
+    const int t = threadIdx.x;
+    const float4* xr = reinterpret_cast<const float4*>(x + row * ldx);
+    float4 v[V];
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        v[j] = xr[j * NT + t];
+        ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
+    }
+    ss = block_sum<NT>(ss, red);
+    const float inv = 1.0f / sqrtf(ss / d + eps);
+    float* ps = pool_sum + (int64_t)req_slot[row] * d;
+    const float cnt = static_cast<float>(req_start[row] + 1);
+    float* prow = pooled + row * 2 * d;
+    const int64_t lo = (int64_t)n_req * 2 * d;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        const int c = (j * NT + t) * 4;
+        float g[4];
+        if constexpr (sizeof(TG) == 4) {
+            const float4 gv = *reinterpret_cast<const float4*>(gamma + c);
+            g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
+        } else {
+            const uint2 gv = *reinterpret_cast<const uint2*>(gamma + c);
+            g[0] = __uint_as_float(gv.x << 16); g[1] = __uint_as_float(gv.x & 0xffff0000u);
+            g[2] = __uint_as_float(gv.y << 16); g[3] = __uint_as_float(gv.y & 0xffff0000u);
+        }
+        const float o[4] = {v[j].x * inv * g[0], v[j].y * inv * g[1], v[j].z * inv * g[2], v[j].w * inv * g[3]};
+        if (y) {
+            if constexpr (sizeof(TY) == 4) {
+                *reinterpret_cast<float4*>(y + row * ldy + c) = make_float4(o[0], o[1], o[2], o[3]);
+            } else {
+                uint2 pk;
+                pk.x = f32_to_bf16(o[0]) | (uint32_t(f32_to_bf16(o[1])) << 16);
+                pk.y = f32_to_bf16(o[2]) | (uint32_t(f32_to_bf16(o[3])) << 16);
+                *reinterpret_cast<uint2*>(y + row * ldy + c) = pk;
+            }
+        }
+        if (y2) *reinterpret_cast<float4*>(y2 + row * ldy2 + c) = make_float4(o[0], o[1], o[2], o[3]);
+        const float4 s0 = *reinterpret_cast<const float4*>(ps + c);
+        const float s[4] = {s0.x + o[0], s0.y + o[1], s0.z + o[2], s0.w + o[3]};
+        *reinterpret_cast<float4*>(ps + c) = make_float4(s[0], s[1], s[2], s[3]);
+        const float mean[4] = {s[0] / cnt, s[1] / cnt, s[2] / cnt, s[3] / cnt};
+        *reinterpret_cast<float4*>(prow + c) = make_float4(mean[0], mean[1], mean[2], mean[3]);
+        *reinterpret_cast<float4*>(prow + d + c) = make_float4(o[0], o[1], o[2], o[3]);
+        if (pooled_bf16) {
+            uint16_t hm[4], lm[4], hx[4], lx[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                hm[e] = f32_to_bf16(mean[e]);
+                lm[e] = f32_to_bf16(mean[e] - bf16_to_f32(hm[e]));
+                hx[e] = f32_to_bf16(o[e]);
+                lx[e] = f32_to_bf16(o[e] - bf16_to_f32(hx[e]));
+            }
+            uint16_t* pb = pooled_bf16 + row * 2 * d + c;
+            auto pack = [](const uint16_t* h) {
+                return make_uint2(h[0] | (uint32_t(h[1]) << 16), h[2] | (uint32_t(h[3]) << 16));
+            };
+            *reinterpret_cast<uint2*>(pb) = pack(hm);
+            *reinterpret_cast<uint2*>(pb + lo) = pack(lm);
+            *reinterpret_cast<uint2*>(pb + d) = pack(hx);
+            *reinterpret_cast<uint2*>(pb + d + lo) = pack(lx);
+        }
+    }
+}
+
 template <typename TW>
 __global__ void __launch_bounds__(256)
 head_finish_kernel(int h1, int splits, int n_req, int rows, const float* partial, const TW* b1,
@@ -422,33 +501,38 @@ head_finish_kernel(int h1, int splits, int n_req, int rows, const float* partial
     if (threadIdx.x == 0) z[i] = acc + load_act<TW>(b2);
 }
 
-// Same result for the fixed split count S and h1 a multiple of 4: each thread
-// takes four consecutive hidden units and issues all 2 S of its partial loads
-// (16-byte) before summing them in split order, so the block waits out one
-// memory latency instead of one per split.
+// Same result for a split count that is a multiple of S and h1 a multiple of
+// 4: each thread takes four consecutive hidden units and, per group of S
+// splits, issues all 2 S of its partial loads (16-byte) before summing them
+// in split order, so the block waits out one memory latency per group
+// instead of one per split.
 template <typename TW, int S>
 __global__ void __launch_bounds__(256)
-head_finish_vec_kernel(int h1, int n_req, int rows, const float* partial, const TW* b1, const TW* w2,
-                       const TW* b2, float* z) {
+head_finish_vec_kernel(int h1, int n_req, int rows, int splits, const float* partial, const TW* b1,
+                       const TW* w2, const TW* b2, float* z) {
     __shared__ float red[4];
     const int i = blockIdx.x;
     const bool lo = rows > n_req;
     float acc = 0.f;
     for (int j = threadIdx.x * 4; j < h1; j += 1024) {
-        float4 ph[S], pl[S];
-#pragma unroll
-        for (int sp = 0; sp < S; ++sp) {
-            ph[sp] = *reinterpret_cast<const float4*>(partial + ((int64_t)sp * rows + i) * h1 + j);
-            pl[sp] = lo ? *reinterpret_cast<const float4*>(partial + ((int64_t)sp * rows + n_req + i) * h1 + j)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = load_act<TW>(b1 + j + e);
+        // splits in groups of S (loads of a group issued together), summed in order
+        for (int s0 = 0; s0 < splits; s0 += S) {
+            float4 ph[S], pl[S];
 #pragma unroll
-        for (int sp = 0; sp < S; ++sp) {
-            v[0] += ph[sp].x; v[1] += ph[sp].y; v[2] += ph[sp].z; v[3] += ph[sp].w;
-            if (lo) { v[0] += pl[sp].x; v[1] += pl[sp].y; v[2] += pl[sp].z; v[3] += pl[sp].w; }
+            for (int q = 0; q < S; ++q) {
+                const int64_t sp = s0 + q;
+                ph[q] = *reinterpret_cast<const float4*>(partial + (sp * rows + i) * h1 + j);
+                pl[q] = lo ? *reinterpret_cast<const float4*>(partial + (sp * rows + n_req + i) * h1 + j)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int q = 0; q < S; ++q) {
+                v[0] += ph[q].x; v[1] += ph[q].y; v[2] += ph[q].z; v[3] += ph[q].w;
+                if (lo) { v[0] += pl[q].x; v[1] += pl[q].y; v[2] += pl[q].z; v[3] += pl[q].w; }
+            }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc = fmaf(fmaxf(v[e], 0.f), load_act<TW>(w2 + j + e), acc);
@@ -627,6 +711,35 @@ bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles
     return true;
 }
 
+bool launch_norm_pool_step(int act_fmt, int gamma_fmt, int n_req, int d, const float* x, int64_t ldx,
+                           const void* gamma, float eps, void* y, int64_t ldy, float* y2, int64_t ldy2,
+                           const int32_t* req_slot, const int32_t* req_start, float* pool_sum, float* pooled,
+                           uint16_t* pooled_bf16, hipStream_t st) {
+    const bool vec = d % 1024 == 0 && d <= 8192 && ldx % 4 == 0 && (!y || ldy % 4 == 0) && (!y2 || ldy2 % 4 == 0) &&
+                     reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(y2) % 16 == 0 && reinterpret_cast<uintptr_t>(gamma) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(pool_sum) % 16 == 0 && reinterpret_cast<uintptr_t>(pooled) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(pooled_bf16) % 8 == 0 && (d / 1024 & (d / 1024 - 1)) == 0;
+    if (!vec) return false;
+    if (n_req <= 0) return true;
+    const int V = d / 1024;   // d = 1024 V: NT = 256 V threads of one float4 up to d = 4096, then 2 each
+#define OUTLETS_NPS_V(TY, TG, VV, NT, PER)                                                                 \
+    case VV:                                                                                               \
+        hipLaunchKernelGGL((norm_pool_step_kernel<TY, TG, NT, PER>), dim3(n_req), dim3(NT), 0, st, d, n_req, x, \
+                           ldx, static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2, req_slot, \
+                           req_start, pool_sum, pooled, pooled_bf16);                                         \
+        break;
+#define OUTLETS_NPS(TY, TG)                                                                                \
+    switch (V) { OUTLETS_NPS_V(TY, TG, 1, 256, 1) OUTLETS_NPS_V(TY, TG, 2, 512, 1)                          \
+                 OUTLETS_NPS_V(TY, TG, 4, 1024, 1) OUTLETS_NPS_V(TY, TG, 8, 1024, 2) }
+    if (act_fmt == FMT_F32) { OUTLETS_NPS(float, float) }
+    else if (gamma_fmt == FMT_F32) { OUTLETS_NPS(bf16_t, float) }
+    else { OUTLETS_NPS(bf16_t, bf16_t) }
+#undef OUTLETS_NPS
+#undef OUTLETS_NPS_V
+    return true;
+}
+
 void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,
                       uint16_t* pooled_bf16, hipStream_t st) {
@@ -678,14 +791,14 @@ void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* 
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
                         const void* b1, const void* w2, const void* b2, float* z, hipStream_t st) {
     if (n_req <= 0) return;
-    if (splits == 8 && h1 % 4 == 0) {
+    if (splits % 8 == 0 && h1 % 4 == 0) {
         if (w_fmt == FMT_F32)
             hipLaunchKernelGGL((head_finish_vec_kernel<float, 8>), dim3(n_req), dim3(256), 0, st, h1, n_req,
-                               n_req, partial, static_cast<const float*>(b1), static_cast<const float*>(w2),
+                               n_req, splits, partial, static_cast<const float*>(b1), static_cast<const float*>(w2),
                                static_cast<const float*>(b2), z);
         else
             hipLaunchKernelGGL((head_finish_vec_kernel<bf16_t, 8>), dim3(n_req), dim3(256), 0, st, h1, n_req,
-                               2 * n_req, partial, static_cast<const bf16_t*>(b1),
+                               2 * n_req, splits, partial, static_cast<const bf16_t*>(b1),
                                static_cast<const bf16_t*>(w2), static_cast<const bf16_t*>(b2), z);
         return;
     }
