@@ -93,8 +93,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, int64_
     const uint32_t n = static_cast<uint32_t>(bytes > 0xffffffffLL ? 0xffffffffLL : bytes);
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(n), 0x00020000);
 }
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, char* lds_base) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, 0, 0, 0);
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, char* lds_base, uint32_t soff = 0) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
 }
 
 // Wait until at most N of this wave's vector-memory operations (the DMA
@@ -221,14 +221,15 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     auto issue = [&](int k0, int stage, int kpf) {
         if (DW < NW && !issuer) return;
         char* base = lds + stage * STAGE;
+        // the slice's K offset is uniform: it goes in the scalar offset
         const int sa = k0 / A.kseg;
         const __amdgpu_buffer_rsrc_t rsa = sa == 0 ? ra[0] : (sa == 1 ? ra[1] : ra[2]);
         const uint32_t ka = static_cast<uint32_t>((k0 - sa * A.kseg) * 2);
 #pragma unroll
-        for (int j = 0; j < ACP; ++j) dma16(rsa, a_voff[j] + ka, base + (dwave * ACP + j) * 1024);
+        for (int j = 0; j < ACP; ++j) dma16(rsa, a_voff[j], base + (dwave * ACP + j) * 1024, ka);
 #pragma unroll
         for (int j = 0; j < BCP; ++j)
-            dma16(rb[j], b_voff[j] + static_cast<uint32_t>(k0 * ESZ), base + A_BYTES + (dwave * BCP + j) * 1024);
+            dma16(rb[j], b_voff[j], base + A_BYTES + (dwave * BCP + j) * 1024, static_cast<uint32_t>(k0 * ESZ));
         if constexpr (PF) {
             const int sp = kpf / A.kseg;
             const __amdgpu_buffer_rsrc_t rsp = sp == 0 ? ra[0] : (sp == 1 ? ra[1] : ra[2]);
