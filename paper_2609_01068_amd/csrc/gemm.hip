@@ -147,7 +147,7 @@ __device__ __forceinline__ int swz_chunk(int row, int c) {
 template <int EPI, bool E4M3, bool PF, int WM, int WN, int BK, int STAGES>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split, int pid0) {
-    constexpr int BM = 256, BN = 256, NW = WM * WN;
+    constexpr int BM = 64 * WM, BN = 256, NW = WM * WN;   // 64-row wave tiles (FM = 4)
     constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 16, FN = TN / 16;
     constexpr int KSTEPS = BK / 32;
     constexpr int AROWB = BK * 2;                       // bytes per A row
@@ -701,6 +701,18 @@ template <int EPI, bool E4M3>
 void launch_tiles(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC& c, int splits,
                   int pid0, int ntiles, hipStream_t st) {
     const int kps = ((K / BK + splits - 1) / splits) * BK;
+#ifndef OUTLETS_GEMM_SKINNY
+#define OUTLETS_GEMM_SKINNY 3   // LDS stages of the 64-row kernel (0: off)
+#endif
+    // At most 64 rows: 64 x 256 tiles on 4 waves of 64 x 64, with more K
+    // slices in flight (the weight stream is what such calls wait on)
+    if constexpr (EPI != EPI_QKV_ROPE && EPI != EPI_PARTIAL_TILE && OUTLETS_GEMM_SKINNY > 0) {
+        if (M <= 64 && pid0 == 0) {
+            hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, false, 1, 4, OUTLETS_GEMM_BK, OUTLETS_GEMM_SKINNY>),
+                               dim3(ntiles, splits), dim3(256), 0, st, M, N, K, a, b, c, kps, pid0);
+            return;
+        }
+    }
     // A-row prefetch for narrow outputs over many row tiles (measured on the
     // d = 4096 draft layer: fused projection, O and down 3-9% faster; 1-3%
     // slower for N = 28,672 and 7% slower for the QKV GEMM with its RoPE
