@@ -697,19 +697,51 @@ gemm_f32_64x64(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_split) 
     }
 }
 
+#ifndef OUTLETS_GEMM_SKINNY
+#define OUTLETS_GEMM_SKINNY 3   // LDS stages of the 64-row kernel (0: off)
+#endif
+#ifndef OUTLETS_GEMM_MID
+#define OUTLETS_GEMM_MID 512    // calls of up to this many rows may use 128-row tiles (0: never)
+#endif
+#ifndef OUTLETS_GEMM_MIDST
+#define OUTLETS_GEMM_MIDST 3    // LDS stages of the 128-row kernel
+#endif
+
+// Row-tile height for M rows and N columns: 64 up to 64 rows; 128 up to
+// OUTLETS_GEMM_MID rows when that takes no more rounds over the CUs than
+// 256-row tiles (measured at M = 256 and 512: 8-17% faster for N = 4096 and
+// 6,144, and for gate/up at M = 256; at M = 512 gate/up needs two rounds of
+// 128-row tiles and is 25% slower); else 256.  Always 256 for the QKV RoPE
+// epilogue (it needs 128-wide wave tiles) and the tail-split blocks.
+int device_cus();
+
+int gemm_bm(int M, int N, int epi) {
+    if (epi == EPI_QKV_ROPE || epi == EPI_PARTIAL_TILE) return 256;
+    if (OUTLETS_GEMM_SKINNY > 0 && M <= 64) return 64;
+    if (OUTLETS_GEMM_MID > 0 && M <= OUTLETS_GEMM_MID) {
+        const int W = device_cus(), nt = N / 256;
+        if ((((M + 127) / 128) * nt + W - 1) / W <= (((M + 255) / 256) * nt + W - 1) / W) return 128;
+    }
+    return 256;
+}
+
 template <int EPI, bool E4M3>
 void launch_tiles(int M, int N, int K, const GemmA& a, const GemmB& b, const GemmC& c, int splits,
                   int pid0, int ntiles, hipStream_t st) {
     const int kps = ((K / BK + splits - 1) / splits) * BK;
-#ifndef OUTLETS_GEMM_SKINNY
-#define OUTLETS_GEMM_SKINNY 3   // LDS stages of the 64-row kernel (0: off)
-#endif
     // At most 64 rows: 64 x 256 tiles on 4 waves of 64 x 64, with more K
     // slices in flight (the weight stream is what such calls wait on)
     if constexpr (EPI != EPI_QKV_ROPE && EPI != EPI_PARTIAL_TILE && OUTLETS_GEMM_SKINNY > 0) {
-        if (M <= 64 && pid0 == 0) {
+        if (gemm_bm(M, N, EPI) == 64) {
             hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, false, 1, 4, OUTLETS_GEMM_BK, OUTLETS_GEMM_SKINNY>),
                                dim3(ntiles, splits), dim3(256), 0, st, M, N, K, a, b, c, kps, pid0);
+            return;
+        }
+    }
+    if constexpr (EPI != EPI_QKV_ROPE && EPI != EPI_PARTIAL_TILE && OUTLETS_GEMM_MID > 0) {
+        if (gemm_bm(M, N, EPI) == 128) {
+            hipLaunchKernelGGL((gemm_mfma_256x256<EPI, E4M3, false, 2, 4, OUTLETS_GEMM_BK, OUTLETS_GEMM_MIDST>),
+                               dim3(ntiles, splits), dim3(512), 0, st, M, N, K, a, b, c, kps, pid0);
             return;
         }
     }
@@ -747,7 +779,8 @@ template <int EPI, bool E4M3>
 void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& b,
                  const GemmC& c, int splits, hipStream_t st, float* ws, size_t ws_bytes) {
     (void)act_fmt;
-    const int mt = (M + 255) / 256, nt = N / 256, T = mt * nt;
+    const int bm = gemm_bm(M, N, EPI);
+    const int mt = (M + bm - 1) / bm, nt = N / 256, T = mt * nt;
     // With one workgroup per CU, T tiles take ceil(T / W) rounds; when the
     // last round holds only a few tiles, those tiles run instead as S K-splits
     // (S * tail <= W workgroups of 1/S the work) and are summed by
@@ -755,7 +788,7 @@ void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& 
     const int W = device_cus();
     const int full = T / W, tail = T % W;
     int S = 1;
-    if (splits == 1 && EPI != EPI_PARTIAL && EPI != EPI_QKV_ROPE && full >= 1 && full <= 64 && tail > 0 && ws) {
+    if (splits == 1 && bm == 256 && EPI != EPI_PARTIAL && EPI != EPI_QKV_ROPE && full >= 1 && full <= 64 && tail > 0 && ws) {
         S = std::min({16, W / tail, (K / BK) / 4});
         if ((size_t)S * tail * 65536 * sizeof(float) > ws_bytes) S = 1;
     }
@@ -785,14 +818,16 @@ int gemm_device_cus() { return device_cus(); }
 
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K) {
     if (w_fmt == FMT_F32 || epi == EPI_PARTIAL) return 1;
-    const int tiles = ((M + 255) / 256) * (N / 256);
+    const int bm = gemm_bm(M, N, epi);
+    const int tiles = ((M + bm - 1) / bm) * (N / 256);
     const int W = device_cus();
     if (tiles >= W) return 1;
     // Cost in units of one tile's full-K pass: ceil(tiles * s / W) rounds of
     // 1/s of a pass, plus the fp32 partials written and re-read by the reduce
     // (2 * 4 B * M * N per split at ~5 TB/s against ~1.3 us per 64-deep K
-    // slice of a tile).
-    const double alpha = 512.0 * M * N / (6.5e6 * K);
+    // slice of a 256-row tile; half that for 128-row tiles, while a 64-row
+    // tile's slice costs about as much, its weight stream being the same).
+    const double alpha = 512.0 * M * N / (6.5e6 * K) * (bm == 128 ? 2.0 : 1.0);
     const int smax = std::min(16, std::max(1, (K / BK) / 4));   // keep >= 4 K slices per split
     int best = 1;
     double best_cost = 1.0;
