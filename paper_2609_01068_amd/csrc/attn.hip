@@ -183,15 +183,6 @@ constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? OUTLETS_PREFIL
 // keys], each a plain copy of its page block.
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint4 zero_tail_bf16x8(uint4 v, int valid) {
-    // keep the first `valid` (0..8) bf16 elements of v
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        if (e >= valid) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-    return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
 template <int G, int QB>
 __global__ void __launch_bounds__(G * 64, QB == 1 ? 2 : 1)
 attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
