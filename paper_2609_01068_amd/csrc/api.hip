@@ -623,8 +623,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
                                        {(c->w_fmt == FMT_F32 ? 1 : 2) * c->F, c->d}, {c->d, c->F}};
         const int epis[5] = {EPI_STORE_F32, EPI_STORE_ACT, EPI_RESID_F32, EPI_SWIGLU, EPI_RESID_F32};
         size_t need = 0;
-        for (int64_t mt = 1; mt <= 4 && (mt - 1) * 256 < Tm; ++mt) {
-            const int64_t m = std::min<int64_t>(mt * 256, Tm);
+        for (int64_t m0 = 16; m0 <= 1024 && m0 - 16 < Tm; m0 += 16) {
+            const int64_t m = std::min<int64_t>(m0, Tm);
             for (int g = 0; g < 5; ++g) {
                 const int sk = gemm_splitk_plan(c->w_fmt, epis[g], (int)m, (int)gemm_nk[g][0], (int)gemm_nk[g][1]);
                 if (sk > 1) need = std::max(need, (size_t)sk * m * gemm_nk[g][0] * sizeof(float));
