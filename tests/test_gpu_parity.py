@@ -290,6 +290,39 @@ def test_incremental_steps_equal_prefill_recompute():
     pred.close()
 
 
+def test_step_batch_sizes_across_row_tile_variants():
+    """8B shape: a decode step of B requests in one call (B = 64, 65, 200,
+    520: the GEMMs run on 64-, 128-, 128- and 256-row tiles, with different
+    K splits) equals the same step taken one request per call (1-row calls)
+    on a second context with the same weights and history: h_draft and z per
+    request within the bf16 tolerance."""
+    import torch
+    n = 520
+    case = make_case(1, lens=[8] * n, n_req=n)
+    say(f"case: 8B bf16, {n} requests of 8 prompt tokens; batched vs one-per-call steps")
+    pa = make_predictor(case, max_slots=n, max_seq_len=64)
+    pb = make_predictor(case, max_slots=n, max_seq_len=64)
+    H = device_states(case)
+    slots = list(range(n))
+    pa.prefill(slots, case.lens, *H)
+    pb.prefill(slots, case.lens, *H)
+    for t, b in enumerate((64, 65, 200, 520), start=1):
+        S = device_states(case, step_inputs(case, t))
+        za, ha = pa.step(slots[:b], *[x[:b] for x in S], want_hdraft=True)
+        zb, hb = [], []
+        for i in range(b):
+            z1, h1 = pb.step([i], *[x[i:i + 1] for x in S], want_hdraft=True)
+            zb.append(float(z1[0]))
+            hb.append(tensor_to_f64(h1[0]))
+        za, ha, zb, hb = tensor_to_f64(za), tensor_to_f64(ha), np.array(zb), np.stack(hb)
+        eh = max(rel_fro(ha[i], hb[i]) for i in range(b))
+        ez = float(z_errors(za, zb).max())
+        say(f"  B={b}: max h_draft rel err {eh:.2e}, max z err {ez:.2e}")
+        assert eh <= TOL_HDRAFT["bf16"] and ez <= TOL_Z["bf16"], (b, eh, ez)
+    pa.close()
+    pb.close()
+
+
 def test_constant_token_prompt_at_long_length():
     say("case: 8B bf16 shape, constant-token prompts n=1 and n=4096")
     import torch
