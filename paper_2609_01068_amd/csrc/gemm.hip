@@ -141,7 +141,11 @@ __device__ __forceinline__ int swz_chunk(int row, int c) {
 // 4 st + g of a bf16 row (bytes 32 st + 8 g .. +7 of an e4m3 row).  A and B
 // use the same assignment, so every product pairs equal k.
 //
-// LDS per stage: A [256 rows][BK bf16], then B [256 rows][BK bf16] or, for
+// Tiles are BM = 64 WM rows by 256 columns on WM x WN waves: 256 x 256 on
+// 4 x 2 waves for large M, 128 x 256 on 2 x 4 and 64 x 256 on 1 x 4 for
+// calls with few rows (the kernel keeps its 256 x 256 name).
+//
+// LDS per stage: A [BM rows][BK bf16], then B [256 rows][BK bf16] or, for
 // e4m3, [256 rows][BK codes].  STAGES slices are in flight: slice k + STAGES
 // - 1 is copied while slice k is multiplied.
 template <int EPI, bool E4M3, bool PF, int WM, int WN, int BK, int STAGES>
