@@ -90,6 +90,7 @@ struct outlets_ctx {
     int64_t meta_cap = 0;        // int32 entries
     int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
     int32_t n_work = 0;
+    int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
     int32_t n_tiles = 0;
     float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
@@ -376,7 +377,7 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
       const void* gate = c->gated ? static_cast<const char*>(c->qkv) + (c->qdim + 2 * c->kvdim) * fmt_bytes(af)
                                   : nullptr;
       if (prefill && c->n_work > 0)
-          launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->qkv, c->qkv_dim, c->attn, c->qdim,
+          launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->attn_qtile, c->qkv, c->qkv_dim, c->attn, c->qdim,
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
@@ -715,8 +716,10 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
         return fail(OUTLETS_ERR_INVALID_ARG, "total prompt tokens exceed max_batch_tokens");
     }
     std::vector<int32_t> work;
-    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim))
-        work = attention_work(n_req, lens, attn_prefill_query_tile(ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads));
+    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
+        ctx->attn_qtile = attn_prefill_query_tile(ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, T, n_req);
+        work = attention_work(n_req, lens, ctx->attn_qtile);
+    }
     std::vector<int32_t> cu_tiles(n_req + 1, 0);
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
     rc = upload_meta(ctx, n_req, off, slots, start, updates, work, cu_tiles, st);

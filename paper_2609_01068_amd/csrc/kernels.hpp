@@ -116,8 +116,9 @@ void launch_rope_kv(int act_fmt, int ntok, void* qkv, int64_t ld, const int32_t*
 
 bool attn_supported(int n_q, int n_kv, int hd);
 bool attn_prefill_mfma_supported(int act_fmt, int n_q, int n_kv, int hd);
-// Queries per prefill attention work item (a multiple of 32).
-int attn_prefill_query_tile(int n_q, int n_kv);
+// Queries per prefill attention work item (a multiple of 32) for a call of
+// `tokens` prompt tokens over n_req requests.
+int attn_prefill_query_tile(int n_q, int n_kv, int64_t tokens, int n_req);
 
 // Attention kernels: `gate` (nullable) points at the Gated Attention gate
 // values of token/request row 0, laid out like q (row stride ldq, query head h
@@ -125,7 +126,7 @@ int attn_prefill_query_tile(int n_q, int n_kv);
 //
 // Causal prefill attention on MFMA (bf16, hd 128).  work[2 * i], work[2 * i + 1]
 // = (request, query tile) of workgroup row i; req_off = token offsets.
-void launch_attn_prefill(int n_work, const int32_t* work, const void* qkv, int64_t ldq, void* out,
+void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void* qkv, int64_t ldq, void* out,
                          int64_t ldo, const int32_t* req_off, const int32_t* req_slot,
                          const int32_t* page_table, int max_pages, const void* kpool,
                          const void* vpool, int n_q, int n_kv, const void* gate, hipStream_t st);
