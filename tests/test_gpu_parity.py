@@ -323,6 +323,31 @@ def test_step_batch_sizes_across_row_tile_variants():
     pb.close()
 
 
+def test_prefill_attention_query_tile_variants_agree():
+    """8B shape: two 1,500-token requests prefilled alone (prompts average
+    >= 1,024 tokens: 64-query attention work items, two 32-query blocks per
+    workgroup) and together with two 1-token requests (average 751: 32-query
+    items) give the same h_draft and z for the long requests, bit for bit: a
+    wave's arithmetic for its 32 queries does not depend on how many blocks
+    its workgroup holds, and the GEMM rows do not depend on the other rows."""
+    lens_a = [1500, 1500]
+    lens_b = [1500, 1500, 1, 1]
+    case = make_case(1, lens=lens_b, n_req=len(lens_b))
+    say(f"case: 8B bf16, lens {lens_a} (64-query items) vs {lens_b} (32-query items)")
+    pa = make_predictor(case, max_slots=4)
+    pb = make_predictor(case, max_slots=4)
+    H = device_states(case)
+    za, ha = pa.prefill([0, 1], lens_a, *[x[:3000].contiguous() for x in H], want_hdraft=True)
+    zb, hb = pb.prefill([0, 1, 2, 3], lens_b, *H, want_hdraft=True)
+    ha, hb = tensor_to_f64(ha), tensor_to_f64(hb)[:3000]
+    eh = max(rel_fro(ha[:1500], hb[:1500]), rel_fro(ha[1500:], hb[1500:3000]))
+    ez = float(z_errors(tensor_to_f64(za), tensor_to_f64(zb)[:2]).max())
+    say(f"  h_draft rel err {eh:.2e}, z err {ez:.2e}")
+    assert eh == 0.0 and ez == 0.0
+    pa.close()
+    pb.close()
+
+
 def test_constant_token_prompt_at_long_length():
     say("case: 8B bf16 shape, constant-token prompts n=1 and n=4096")
     import torch
