@@ -327,9 +327,10 @@ def test_prefill_attention_query_tile_variants_agree():
     """8B shape: two 1,500-token requests prefilled alone (prompts average
     >= 1,024 tokens: 64-query attention work items, two 32-query blocks per
     workgroup) and together with two 1-token requests (average 751: 32-query
-    items) give the same h_draft and z for the long requests, bit for bit: a
-    wave's arithmetic for its 32 queries does not depend on how many blocks
-    its workgroup holds, and the GEMM rows do not depend on the other rows."""
+    items) give the same h_draft and z for the long requests (measured: bit
+    for bit, since a wave's arithmetic for its 32 queries does not depend on
+    how many blocks its workgroup holds; the bound leaves room for a
+    different K split of a GEMM between the two batch sizes)."""
     lens_a = [1500, 1500]
     lens_b = [1500, 1500, 1, 1]
     case = make_case(1, lens=lens_b, n_req=len(lens_b))
@@ -343,7 +344,7 @@ def test_prefill_attention_query_tile_variants_agree():
     eh = max(rel_fro(ha[:1500], hb[:1500]), rel_fro(ha[1500:], hb[1500:3000]))
     ez = float(z_errors(tensor_to_f64(za), tensor_to_f64(zb)[:2]).max())
     say(f"  h_draft rel err {eh:.2e}, z err {ez:.2e}")
-    assert eh == 0.0 and ez == 0.0
+    assert eh <= TOL_HDRAFT["bf16"] and ez <= TOL_Z["bf16"]
     pa.close()
     pb.close()
 
