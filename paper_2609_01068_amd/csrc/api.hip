@@ -91,6 +91,7 @@ struct outlets_ctx {
     int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
     int32_t n_work = 0;
     int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
+    int32_t dec_chunk = 64;        // pages per decode attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
     int32_t n_tiles = 0;
     float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
@@ -381,7 +382,7 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
-          launch_attn_decode(n, c->n_work, c->d_meta + c->work_off, c->d_meta + c->tiles_off, c->qkv,
+          launch_attn_decode(n, c->n_work, c->dec_chunk, c->d_meta + c->work_off, c->d_meta + c->tiles_off, c->qkv,
                              c->qkv_dim, c->attn, c->qdim, req_slot, req_start, c->page_table,
                              c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
                              c->decode_part, gate, st);
@@ -613,7 +614,12 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->last_idx, sizeof(int32_t) * Bm);
-    const int64_t max_chunks = Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages());
+    // decode work items: chunks of the largest size, or, where the step
+    // halves the size because those fill fewer than 2 waves per CU over the
+    // KV heads, at most 4x that many (16-page chunks)
+    const int64_t max_chunks = std::max<int64_t>(
+        Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages()),
+        (int64_t)(64 / 16) * (2 * gemm_device_cus() / std::max(1, cfg->n_kv_heads) + 1));
     c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
     if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
         ALLOC(c->decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
@@ -762,11 +768,13 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
     // split-KV decode work items (request, chunk of pages), requests in order
     std::vector<int32_t> dwork, cu_chunks;
     if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
-        const int chunk = attn_decode_chunk_pages();
+        std::vector<int32_t> pages(n_req);
+        for (int i = 0; i < n_req; ++i) pages[i] = (start[i] + 1 + 15) / 16;
+        const int chunk = attn_decode_chunk_for(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus());
+        ctx->dec_chunk = chunk;
         cu_chunks.assign(n_req + 1, 0);
         for (int i = 0; i < n_req; ++i) {
-            const int pages = (start[i] + 1 + 15) / 16;
-            const int nch = (pages + chunk - 1) / chunk;
+            const int nch = (pages[i] + chunk - 1) / chunk;
             cu_chunks[i + 1] = cu_chunks[i] + nch;
             for (int c = 0; c < nch; ++c) { dwork.push_back(i); dwork.push_back(c); }
         }

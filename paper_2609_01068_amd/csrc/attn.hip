@@ -409,7 +409,7 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
 
 // ---------------------------------------------------------------- decode, MFMA
 // One query token per request (a decode step).  Split-KV: one wave per
-// (request, KV head, chunk of kDecodeChunk pages); each wave keeps an online
+// (request, KV head, chunk of up to kDecodeChunk pages); each wave keeps an online
 // softmax for the G query heads of its KV head and writes (m, l, o) partials,
 // which attn_decode_combine merges in chunk order (deterministic).
 //
@@ -435,7 +435,7 @@ template <int G>
 __global__ void __launch_bounds__(64)
 attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_t* req_slot,
                  const int32_t* req_start, const int32_t* page_table, int max_pages,
-                 const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale, float* part) {
+                 const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale, float* part, int chunk) {
     constexpr int HD = 128;
     static_assert(G <= 16, "query heads per KV head");
     const int wi = blockIdx.x, g = blockIdx.y;
@@ -443,7 +443,7 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
     const int slot = req_slot[r];
     const int nkeys = req_start[r] + 1;            // cached keys plus the new token's
     const int npages = (nkeys + 15) / 16;
-    const int p0 = c * kDecodeChunk, p1 = min(npages, p0 + kDecodeChunk);
+    const int p0 = c * chunk, p1 = min(npages, p0 + chunk);   // chunk <= kDecodeChunk
     const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
 
     bf16x8 qb[HD / 32];
@@ -668,9 +668,24 @@ void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void*
 }
 
 int attn_decode_chunk_pages() { return kDecodeChunk; }
+
+// Pages per decode work item: kDecodeChunk, halved (down to 16) while the
+// work items of the step fill fewer than two waves per CU over the KV heads,
+// so that small batches still spread over the chip (pages[i] = cached pages
+// of request i after the step's token).
+int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus) {
+    int chunk = kDecodeChunk;
+    while (chunk > 16) {
+        int64_t items = 0;
+        for (int i = 0; i < n_req; ++i) items += (pages[i] + chunk - 1) / chunk;
+        if (items * n_kv >= 2LL * cus) break;
+        chunk /= 2;
+    }
+    return chunk;
+}
 int attn_decode_record_floats() { return kDecodeRec; }
 
-void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
+void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
@@ -683,7 +698,7 @@ void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_
         hipLaunchKernelGGL((attn_decode_mfma<GG>), dim3(n_work, n_kv), dim3(64), 0, st,            \
                            static_cast<const bf16_t*>(q), ldq, work, req_slot, req_start,          \
                            page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
-                           static_cast<const bf16_t*>(vpool), n_kv, qscale, part);                 \
+                           static_cast<const bf16_t*>(vpool), n_kv, qscale, part, chunk);          \
         break;
     switch (G) {
         OUTLETS_DEC_G(1)

@@ -136,9 +136,10 @@ void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void*
 // cu_chunks[n_req + 1] = first work item of each request; part = fp32 scratch
 // [n_work, n_q, attn_decode_record_floats()].  Queries are row r of q for
 // request r.
-int attn_decode_chunk_pages();
+int attn_decode_chunk_pages();   // the largest chunk
+int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus);
 int attn_decode_record_floats();
-void launch_attn_decode(int n_req, int n_work, const int32_t* work, const int32_t* cu_chunks,
+void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
