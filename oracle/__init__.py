@@ -10,7 +10,7 @@ arithmetic.
 from .formats import decode_bf16, decode_e4m3, decode_weight, decode_states  # noqa: F401
 from .model import (OracleShape, OracleModel, RequestState, oracle_from_workload,  # noqa: F401
                     decode_weights, fuse, rms_norm, rope, causal_gqa_attention, silu,
-                    swiglu_mlp, length_head, predicted_remaining, states_to_f64,
+                    swiglu_mlp, length_head, states_to_f64,
                     sigmoid, attention_output_gate, OracleProbe, ProbeState, probe_from_stored,
                     draft_distribution, embedded_attention_input)
 from . import meta  # noqa: F401

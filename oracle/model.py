@@ -113,24 +113,29 @@ def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     query's position masked out.  q [nq_tok, Hq, hd]; k, v [nk_tok, Hkv, hd].
 
     Query rows are independent, so they are processed ``chunk`` at a time only
-    to bound memory."""
+    to bound memory.  Keys later than every query of a chunk are masked for
+    all of its rows (weight exactly zero), so they are left out of that
+    chunk's scores."""
     n_tok, n_q, hd = q.shape
     n_kv = k.shape[1]
     group = n_q // n_kv
     out = np.empty_like(q)
     scale = 1.0 / np.sqrt(hd)
-    for h in range(n_q):
-        g = h // group
-        kg, vg = k[:, g, :], v[:, g, :]
-        for s in range(0, n_tok, chunk):
-            e = min(n_tok, s + chunk)
-            scores = (q[s:e, h, :] @ kg.T) * scale
-            allowed = k_pos[None, :] <= q_pos[s:e, None]
-            scores = np.where(allowed, scores, -np.inf)
-            m = scores.max(axis=1, keepdims=True)
-            p = np.exp(scores - m)
-            p /= p.sum(axis=1, keepdims=True)
-            out[s:e, h, :] = p @ vg
+    for s in range(0, n_tok, chunk):
+        e = min(n_tok, s + chunk)
+        qp = q_pos[s:e]
+        keep = k_pos <= qp.max()
+        kp, kc, vc = (k_pos, k, v) if keep.all() else (k_pos[keep], k[keep], v[keep])
+        masked = kp[None, :] > qp[:, None]
+        for h in range(n_q):
+            g = h // group
+            scores = q[s:e, h, :] @ kc[:, g, :].T
+            scores *= scale
+            np.putmask(scores, masked, -np.inf)
+            scores -= scores.max(axis=1, keepdims=True)
+            np.exp(scores, out=scores)
+            scores /= scores.sum(axis=1, keepdims=True)
+            out[s:e, h, :] = scores @ vc[:, g, :]
     return out
 
 
@@ -177,11 +182,6 @@ def draft_distribution(h_draft: np.ndarray, w_lm: np.ndarray) -> np.ndarray:
     return e / e.sum(axis=-1, keepdims=True)
 
 
-def predicted_remaining(z_hat: np.ndarray) -> np.ndarray:
-    """r_hat = max(0, exp(z_hat) - 1): inverts the z = log(1 + length) target."""
-    return np.maximum(0.0, np.expm1(z_hat))
-
-
 # ------------------------------------------------------------------ model
 
 @dataclasses.dataclass
@@ -226,12 +226,17 @@ class OracleModel:
         x2 = x1 + swiglu_mlp(b, w["w_gate"], w["w_up"], w["w_down"])
         h_draft = rms_norm(x2, w["gamma_final"], s.rms_eps)
         if capture is not None:
+            # capture["_only"] (a set of names) limits what is stored; the
+            # SwiGLU product is recomputed only when it is asked for
+            only = capture.get("_only")
+            want = lambda name: only is None or name in only  # noqa: E731
+            vals = dict(fused=f, norm_attn=a, q=q.reshape(n, -1), k=k, v=v, attn=o, x1=x1,
+                        norm_mlp=b, x2=x2, hdraft=h_draft)
             if e is not None:
-                capture["norm_emb"] = e
-            capture.update(fused=f, norm_attn=a, q=q.reshape(n, -1), k=k, v=v,
-                           attn=o, x1=x1, norm_mlp=b,
-                           mlp_act=silu(b @ w["w_gate"].T) * (b @ w["w_up"].T), x2=x2,
-                           hdraft=h_draft)
+                vals["norm_emb"] = e
+            capture.update({k_: v_ for k_, v_ in vals.items() if want(k_)})
+            if want("mlp_act"):
+                capture["mlp_act"] = silu(b @ w["w_gate"].T) * (b @ w["w_up"].T)
         return h_draft, k_all, v_all
 
     def _head(self, pooled: np.ndarray) -> np.ndarray:
@@ -256,18 +261,22 @@ class OracleModel:
         z = float(self._head(pooled)[0])
         return z, h_draft, RequestState(k, v, pool_sum, n)
 
-    def step_one(self, st: RequestState, h_low, h_mid, h_high, token=None) -> Tuple[float, np.ndarray]:
+    def step_one(self, st: RequestState, h_low, h_mid, h_high, token=None, capture=None
+                 ) -> Tuple[float, np.ndarray]:
         """Dynamic prediction (Section 3.2, t >= 1): one new token for one request.
-        Updates ``st`` in place."""
+        Updates ``st`` in place.  ``capture`` (a dict) receives the layer's
+        intermediate activations of the new token, as in ``prefill_one``."""
         p = st.count
         pos = np.array([p])
         h_draft, k, v = self._layer(h_low[None, :], h_mid[None, :], h_high[None, :], pos,
-                                    st.k, st.v, np.arange(p), None,
+                                    st.k, st.v, np.arange(p), capture,
                                     None if token is None else [token])
         st.k, st.v = k, v
         st.pool_sum = st.pool_sum + h_draft[0]
         st.count = p + 1
         pooled = np.concatenate([st.pool_sum / st.count, h_draft[0]])[None, :]
+        if capture is not None:
+            capture["pooled"] = pooled[0]
         return float(self._head(pooled)[0]), h_draft[0]
 
     # batched API: requests one by one, packed outputs
@@ -285,12 +294,15 @@ class OracleModel:
         hd = np.concatenate(hs, axis=0) if hs else np.zeros((0, self.s.d))
         return np.array(zs), hd, states
 
-    def step(self, states: List[RequestState], h_low, h_mid, h_high, tokens=None):
-        """One decode step for every request in ``states`` (rows in order)."""
+    def step(self, states: List[RequestState], h_low, h_mid, h_high, tokens=None, captures=None):
+        """One decode step for every request in ``states`` (rows in order);
+        ``captures`` (a list of dicts, one per request) receive the
+        intermediates."""
         zs, hs = [], []
         for i, st in enumerate(states):
             z, h = self.step_one(st, h_low[i], h_mid[i], h_high[i],
-                                 None if tokens is None else int(tokens[i]))
+                                 None if tokens is None else int(tokens[i]),
+                                 None if captures is None else captures[i])
             zs.append(z)
             hs.append(h)
         return np.array(zs), (np.stack(hs) if hs else np.zeros((0, self.s.d)))
