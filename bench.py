@@ -9,7 +9,11 @@ layer against the paged KV cache), and the release of the requests' slots.
 Default workload: the 8B-shaped bf16 draft layer (d 4096, 32 q / 8 KV heads,
 head_dim 128, SwiGLU 14336, head 8192 -> 1024 -> 1) over 32 requests with
 lognormal(median 512, sigma 1.0) prompt lengths clipped to [32, 4096],
-synthetic seeded inputs resident in HBM before timing.
+synthetic seeded inputs resident in HBM before timing.  The same line
+carries, under ``decode_step``, the decode-step half of the metric on the
+HBM-bound per-step workload (512 in-flight requests with paged draft KV
+caches of U[256, 8192] tokens): ms per step, draft tokens/s, and the
+attention kernel's and the whole step's fraction of the HBM peak.
 
 Prints one JSON line (rank 0).  ``--gpus`` above 1 is refused: this build
 runs on one GPU.
@@ -28,6 +32,7 @@ if ROOT not in sys.path:
 
 METRIC = "predicted requests/sec + draft tokens/sec at 8B shape; MFMA util / HBM GB/s"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
@@ -101,6 +106,8 @@ def cpu_baseline(wl, W, lens, budget_s: float = 12.0):
         "value": tok_per_s / mean_tokens,
         "unit": "requests/s",
         "cores": threads or os.cpu_count(),
+        "blas_threads": threads,
+        "host_cpus": os.cpu_count(),
         "kind": "oracle",
         "sample": f"requests {done[0]}..{done[-1]} of the batch ({len(done)} requests, {tok} tokens, "
                   f"prefill + 1 step each, fp64 numpy, {t_total:.1f} s); rate scaled by the batch's "
@@ -114,51 +121,77 @@ def _emit(out):
     return 0
 
 
-def bench_decode(a):
-    """Dynamic re-prediction at scale: 512 in-flight requests whose paged draft
-    KV caches hold U[256, 8192] prompt tokens (filled by untimed prefill calls),
-    then `steps` decode steps of one new token per request."""
+def decode_step_bytes(shape, n_req: int, keys: float, weight_bytes: float) -> float:
+    """Algorithmic HBM bytes of one decode step: every cached key and value
+    read once (plus the new token's K/V written), the weights read once, the
+    three input state rows, the running pool sums read and written, z out."""
+    kv_read = keys * shape.n_kv * shape.head_dim * 2 * 2
+    kv_write = n_req * shape.n_kv * shape.head_dim * 2 * 2
+    states = n_req * 3 * shape.d * 2
+    pool = n_req * shape.d * 4 * 2
+    return kv_read + kv_write + weight_bytes + states + pool + 4 * n_req
+
+
+def weight_bytes(W) -> float:
+    """Bytes of every stored weight tensor (codes and row scales for e4m3)."""
+    import numpy as np
+    total = 0
+    for k, v in W.items():
+        if k == "_fmt":
+            continue
+        for arr in (v if isinstance(v, tuple) else (v,)):
+            total += np.asarray(arr).nbytes
+    return float(total)
+
+
+def measure_decode(seed: int, steps: int, warmup: int, attn_gate: bool = False):
+    """Dynamic re-prediction at scale (configuration 3): 512 in-flight
+    requests whose paged draft KV caches hold U[256, 8192] prompt tokens
+    (filled by untimed prefill calls), then ``steps`` timed decode steps of
+    one new token per request.  Returns the measurement as a dict."""
     import numpy as np
     import torch
-    from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
+    from paper_2609_01068_amd.predictor import OutletsPredictor
     from synth import device_states, make_lengths, make_weights, workload
 
-    wl = workload(3, attn_gate=a.attn_gate)
-    steps = a.steps
+    wl = workload(3, attn_gate=attn_gate)
     print(f"[bench] generating {wl.name} weights", file=sys.stderr, flush=True)
-    W = make_weights(wl, a.seed)
-    lens = make_lengths(wl, a.seed)
+    W = make_weights(wl, seed)
+    wbytes = weight_bytes(W)
+    lens = make_lengths(wl, seed)
     B = len(lens)
-    max_seq = int(lens.max()) + steps + a.warmup + 16
-    pages = int(sum((int(n) + steps + a.warmup + 15) // 16 for n in lens)) + B
+    max_seq = int(lens.max()) + steps + warmup + 16
+    pages = int(sum((int(n) + steps + warmup + 15) // 16 for n in lens)) + B
     chunk = 48
     max_chunk_tokens = max(int(lens[i:i + chunk].sum()) for i in range(0, B, chunk))
     pred = OutletsPredictor(wl.shape, wl.weight_fmt, wl.act_fmt, W, max_slots=B, max_seq_len=max_seq,
                             num_pages=pages, max_batch_tokens=max_chunk_tokens, max_batch_requests=B)
+    del W
     print(f"[bench] filling {B} KV caches ({int(lens.sum())} tokens) with prefill calls", file=sys.stderr, flush=True)
     for i in range(0, B, chunk):
         idx = list(range(i, min(B, i + chunk)))
-        H = device_states(wl, int(lens[idx].sum()), a.seed, 300, i)
+        H = device_states(wl, int(lens[idx].sum()), seed, 300, i)
         pred.prefill(idx, lens[idx], *H)
         torch.cuda.synchronize()
         del H
-        print(f"[bench]   prefilled requests {idx[0]}..{idx[-1]}", file=sys.stderr, flush=True)
-    n_in = a.warmup + steps
-    S = [device_states(wl, B, a.seed, 400, t) for t in range(n_in)]
+    print(f"[bench]   caches filled; warmup {warmup}, timed {steps} decode steps", file=sys.stderr, flush=True)
+    n_in = warmup + steps
+    S = [device_states(wl, B, seed, 400, t) for t in range(n_in)]
     slots = list(range(B))
     z = torch.empty(B, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    for t in range(a.warmup):
+    for t in range(warmup):
         pred.step(slots, *S[t], z_out=z, stream=stream)
     torch.cuda.synchronize()
-    cached0 = int(lens.sum()) + B * a.warmup
+    cached0 = int(lens.sum()) + B * warmup
     # timed region: events around the dominant kernel only (timing every
     # kernel group costs ~0.09 ms per step)
     pred.profile(True, groups=["ATTN"])
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
-    for t in range(a.warmup, n_in):
+    for t in range(warmup, n_in):
         pred.step(slots, *S[t], z_out=z, stream=stream)
     ev1.record(stream)
     torch.cuda.synchronize()
@@ -171,30 +204,49 @@ def bench_decode(a):
         pred.step(slots, *S[t], z_out=z, stream=stream)
     breakdown = pred.profile_read("step")
     pred.profile(False)
+    pred.close()
     ms_per_step = max(gpu_ms, wall * 1e3) / steps
     # keys read per step: every cached token of every request plus the new one
     keys = sum(cached0 + B * (t + 1) for t in range(steps)) / steps
     kv_bytes = keys * wl.shape.n_kv * wl.shape.head_dim * 2 * 2
     attn_ms = prof["ATTN"][0] / max(1, prof["ATTN"][1])
-    achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
+    attn_gbs = kv_bytes / (attn_ms * 1e-3) / 1e9
+    step_bytes = decode_step_bytes(wl.shape, B, keys, wbytes)
+    step_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    return {
+        "wl": wl, "requests": B, "steps": steps, "warmup": warmup, "ms_per_step": ms_per_step,
+        "draft_tokens_per_s": B / (ms_per_step / 1e3), "cached_tokens_at_start": cached0,
+        "attn": {"kernel": "decode attention over the paged KV cache", "bound": "hbm", "achieved": attn_gbs,
+                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": attn_gbs / PEAK_HBM_GBS,
+                 "traffic": recorded_traffic("decode_attention_8b_b512.md", "attn.hip", "attn"),
+                 "bytes_per_launch": kv_bytes, "avg_ms": attn_ms},
+        "step": {"bound": "hbm", "achieved": step_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                 "frac": step_gbs / PEAK_HBM_GBS, "bytes_per_step": step_bytes, "kv_bytes_per_step": kv_bytes,
+                 "weight_bytes": wbytes},
+        "kernels_step": {n: {"avg_ms": ms / k, "launches": k} for n, (ms, k) in breakdown.items() if k},
+    }
+
+
+def bench_decode(a):
+    """The configuration-3 decode steps as the bench line itself."""
+    m = measure_decode(a.seed, a.steps, a.warmup, a.attn_gate)
     out = {
-        "metric": METRIC, "value": B / (ms_per_step / 1e3), "unit": "draft tokens/s (request-steps/s)",
-        "n_gpus": 1, "steps": steps, "warmup": a.warmup, "ms_per_step": ms_per_step,
+        "metric": METRIC, "value": m["draft_tokens_per_s"], "unit": "draft tokens/s (request-steps/s)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": m["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded on device; U[256,8192] cached prompt tokens; fresh N(0,1) x (1,4,16) states per step)",
-        "config": {"workload": "8B-shaped bf16 draft layer + length head, dynamic re-prediction: 512 in-flight "
-                               "requests with paged draft KV caches of U[256, 8192] tokens (page 16), one new "
-                               "token per request per step", "requests": B, "cached_tokens_at_start": cached0,
-                   "attn_gate": wl.attn_gate},
-        "roofline": {"kernel": "decode attention over the paged KV cache", "bound": "hbm",
-                     "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                     "traffic": recorded_traffic("decode_attention_8b_b512.md", "attn.hip", "attn"),
-                     "bytes_per_launch": kv_bytes, "avg_ms": attn_ms},
-        "kernels_step": {n: {"avg_ms": ms / k, "launches": k} for n, (ms, k) in breakdown.items() if k},
+        "config": {"workload": DECODE_WORKLOAD, "requests": m["requests"],
+                   "cached_tokens_at_start": m["cached_tokens_at_start"], "attn_gate": m["wl"].attn_gate},
+        "roofline": m["attn"],
+        "step_hbm": m["step"],
+        "kernels_step": m["kernels_step"],
         "kernels_note": "per-group times from 2 untimed steps with every group timed",
     }
-    pred.close()
     return _emit(out)
+
+
+DECODE_WORKLOAD = ("8B-shaped bf16 draft layer + length head, dynamic re-prediction: 512 in-flight requests "
+                   "with paged draft KV caches of U[256, 8192] tokens (page 16), one new token per request per step")
 
 
 def bench_prefill(a, cfg_id):
@@ -264,6 +316,11 @@ def bench_prefill(a, cfg_id):
         "kernels_prefill": kernels,
         "kernels_note": "per-group times from one untimed call with every group timed",
     }
+    if wl.weight_fmt == "e4m3":
+        # the e4m3 weights are widened to bf16 exactly and multiplied on the
+        # bf16 MFMA; the fp8 MFMA peak is reported beside the bf16 one
+        out["roofline"]["peak_fp8"] = PEAK_FP8_TFLOPS
+        out["roofline"]["frac_fp8_peak"] = achieved / PEAK_FP8_TFLOPS
     pred.close()
     return _emit(out)
 
@@ -402,6 +459,10 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--decode-steps", type=int, default=20,
+                    help="prefill-8b: timed configuration-3 decode steps reported under decode_step")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="prefill-8b: skip the configuration-3 decode-step measurement")
     ap.add_argument("--workload", default="prefill-8b",
                     choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3", "probe-8b",
                              "sched-1p3d"],
@@ -559,10 +620,22 @@ def main(argv=None):
         "kernels_step": step_kernels,
         "kernels_note": "per-group times from 2 untimed steps with every group timed",
     }
+    pred.close()
+    del H, S
+    if not a.no_decode:
+        # the decode-step half of the metric (configuration 3: 512 in-flight
+        # requests, HBM-bound): ms per step, draft tokens/s, the attention
+        # kernel's and the whole step's fraction of the HBM peak
+        m = measure_decode(a.seed, a.decode_steps, a.warmup, a.attn_gate)
+        out["decode_step"] = {
+            "workload": DECODE_WORKLOAD, "requests": m["requests"], "steps": m["steps"],
+            "warmup": m["warmup"], "cached_tokens_at_start": m["cached_tokens_at_start"],
+            "ms_per_step": m["ms_per_step"], "draft_tokens_per_s": m["draft_tokens_per_s"],
+            "attention_hbm": m["attn"], "step_hbm": m["step"], "kernels_step": m["kernels_step"],
+        }
     if not a.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on a sample (cpu_baseline)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, W, lens, a.cpu_budget)
-    pred.close()
     print(json.dumps(out), flush=True)
     return 0
 

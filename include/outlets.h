@@ -314,17 +314,17 @@ enum {
     OUTLETS_BUF_HDRAFT = 8,     /* h_draft, float32 [T, d] */
     OUTLETS_BUF_POOLED = 9,     /* head input p, float32 [n_req, 2d] */
     OUTLETS_BUF_K_POOL = 10,    /* key pages, act [num_pages, n_kv, 16, hd] */
-    OUTLETS_BUF_V_POOL = 11,    /* value pages, act [num_pages, n_kv, 16, hd] */
+    OUTLETS_BUF_V_POOL = 11,    /* value pages, transposed: act [num_pages, n_kv, hd, 16] */
     OUTLETS_BUF_NORM_EMB = 12   /* RMSNorm(embed[token]) * gamma_emb, act [T, d] (input embeddings) */
 };
 
 /*
  * Copy an activation of the last call (rows of that call only) or a KV pool
  * into caller device memory `dst` (`nbytes` capacity) on `stream`;
- * *n_bytes receives the size.  Buffers 0..8 and 12 need keep_intermediates
- * (POOLED and the pools are always kept; h_draft of every row is otherwise
- * available through the predict calls' hdraft_out); NORM_EMB needs input
- * embeddings.
+ * *n_bytes receives the size.  Buffers 0..2, 4..8 and 12 need
+ * keep_intermediates (ATTN, POOLED and the pools are always kept; h_draft of
+ * every row is otherwise available through the predict calls' hdraft_out);
+ * NORM_EMB needs input embeddings.
  */
 int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbytes,
                        int64_t* n_bytes, void* stream);

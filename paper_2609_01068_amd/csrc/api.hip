@@ -987,7 +987,7 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
         case OUTLETS_BUF_FUSED: src = ctx->r_f; size = 4 * T * d; break;
         case OUTLETS_BUF_NORM_ATTN: src = ctx->a_norm; size = ab * T * d; break;
         case OUTLETS_BUF_Q: src = nullptr; size = ab * T * ctx->qdim; break;
-        case OUTLETS_BUF_ATTN: src = ctx->attn; size = ab * T * ctx->qdim; break;
+        case OUTLETS_BUF_ATTN: src = ctx->attn; size = ab * T * ctx->qdim; needs_keep = false; break;
         case OUTLETS_BUF_X1: src = ctx->r_x1; size = 4 * T * d; break;
         case OUTLETS_BUF_NORM_MLP: src = ctx->b_norm; size = ab * T * d; break;
         case OUTLETS_BUF_MLP_ACT: src = ctx->mlp; size = ab * T * ctx->F; break;

@@ -9,9 +9,9 @@ import numpy as np
 import pytest
 
 from oracle import meta
-from gpu_common import (TOL_HDRAFT, TOL_Z, device_states, device_tokens, make_case, make_predictor,
-                        oracle_for, oracle_states, reduced_shape, rel_fro, require_gpu, say, step_inputs,
-                        step_tokens, tensor_to_f64, z_errors)
+from gpu_common import (TOL_HDRAFT, TOL_VARIANT, TOL_Z, attention_rows, check_attention, device_states,
+                        device_tokens, make_case, make_predictor, oracle_for, oracle_states, reduced_shape,
+                        rel_fro, require_gpu, say, step_inputs, step_tokens, tensor_to_f64, z_errors)
 
 pytestmark = pytest.mark.gpu
 
@@ -66,6 +66,10 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
     ez = z_errors(z, z_ref)
     say(f"  prefill z max rel err {ez.max():.3e}; z_ref rms {np.sqrt(np.mean(np.square(z_ref))):.3e}")
     assert ez.max() <= TOL_Z[fmt], ez
+    # the attention output itself, per request (always kept by the library)
+    worst = check_attention(attention_rows(pred, [(off[i], off[i + 1]) for i in range(n)]),
+                            [c["attn"] for c in caps], fmt, "prefill")
+    say(f"  prefill attention worst rel err {worst:.3e}")
     if keep and check_intermediates:
         import torch
         names = [("FUSED", "fused", torch.float32), ("X1", "x1", torch.float32),
@@ -88,21 +92,26 @@ def _run_prefill_case(case, keep=True, steps=0, check_intermediates=True):
     assert alloc.prefill(slots, lens) == meta.OK
     _check_meta(pred, lens, np.array(slots), alloc)
 
+    worst_step = 0.0
     for t in range(1, steps + 1):
         S, tk = step_inputs(case, t), step_tokens(case, t)
         zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True, tokens=device_tokens(tk))
         zs, hs = tensor_to_f64(zs), tensor_to_f64(hs)
-        zr, hr = orc.step(states, *oracle_states(case, S), tokens=tk)
+        scaps = [{"_only": {"attn"}} for _ in range(n)]
+        zr, hr = orc.step(states, *oracle_states(case, S), tokens=tk, captures=scaps)
         for i in range(n):
             assert rel_fro(hs[i], hr[i]) <= TOL_HDRAFT[fmt], (t, i)
         ez = z_errors(zs, zr)
         assert ez.max() <= TOL_Z[fmt], (t, ez)
+        # decode attention (split-KV chunks and their merge) against the oracle
+        worst_step = max(worst_step, check_attention(attention_rows(pred, [(i, i + 1) for i in range(n)]),
+                                                     [c["attn"] for c in scaps], fmt, ("step", t)))
         assert alloc.step(slots) == meta.OK
         from paper_2609_01068_amd import binding as B
         assert np.array_equal(pred.meta(B.OUTLETS_META_PAGE_TABLE), alloc.table().reshape(-1))
         assert np.array_equal(pred.meta(B.OUTLETS_META_SEQ_LEN), alloc.seq_lens())
         assert np.array_equal(pred.meta(B.OUTLETS_META_DEV_POSITIONS), np.asarray(lens) + t - 1)
-    say(f"  {steps} decode steps match")
+    say(f"  {steps} decode steps match; step attention worst rel err {worst_step:.3e}")
     pred.close()
 
 
@@ -130,46 +139,66 @@ def test_bf16_head_dim_64_shape():
     _run_prefill_case(case, keep=True, steps=1)
 
 
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("variant", ["plain", "gated", "embed"])
 def test_config1_full_shape_sampled_requests(variant):
     """8B shape, the 32-request lognormal batch (also with the Gated Attention
     output gate, and with EAGLE-3 input embeddings over the 128,256-entry
-    vocabulary); the oracle recomputes a sample."""
+    vocabulary), prefill and one decode step of every request as the
+    benchmark runs them; the oracle recomputes a sample that always holds
+    the shortest and the longest prompt: h_draft, z and the attention output
+    of the prefill and of the step."""
     case = make_case(1, attn_gate=variant == "gated", input_embed=variant == "embed")
     lens = case.lens
-    say(f"case: config-1 8B bf16 ({variant}), B={len(lens)}, T={int(lens.sum())}, sampled oracle")
-    pred = make_predictor(case)
+    B_ = len(lens)
+    order = np.argsort(lens, kind="stable")
+    sample = sorted({int(order[0]), int(order[1]), int(order[B_ // 3]), int(order[-1])})
+    say(f"case: config-1 8B bf16 ({variant}), B={B_}, T={int(lens.sum())}, oracle on requests {sample} "
+        f"(lengths {[int(lens[i]) for i in sample]}; longest request {int(lens.max())})")
+    pred = make_predictor(case, max_seq_len=int(lens.max()) + 16)
     H = device_states(case)
-    z, hd = pred.prefill(list(range(len(lens))), lens, *H, want_hdraft=True,
-                         tokens=device_tokens(case.tokens))
+    slots = list(range(B_))
+    z, hd = pred.prefill(slots, lens, *H, want_hdraft=True, tokens=device_tokens(case.tokens))
     z = tensor_to_f64(z)
     assert np.all(np.isfinite(z))
-    order = np.argsort(lens)
-    sample = [int(order[0]), int(order[1]), int(order[len(order) // 3])]
-    orc = oracle_for(case)
     off = np.concatenate([[0], np.cumsum(lens)])
+    attn_pre = attention_rows(pred, [(off[i], off[i + 1]) for i in sample])
+    orc = oracle_for(case)
     from synth import make_prompt_states, make_prompt_tokens
-    sub = make_prompt_states(case.wl, lens, requests=sample)
-    sub_tok = make_prompt_tokens(case.wl, lens, requests=sample) if case.tokens is not None else None
-    O = oracle_states(case, sub)
-    z_ref = []
-    o_off = 0
-    hd64 = None
+    z_ref, states, caps = [], [], []
     for i in sample:
-        n = int(lens[i])
-        tok = None if sub_tok is None else sub_tok[o_off:o_off + n]
-        zi, hi, _ = orc.prefill_one(*(x[o_off:o_off + n] for x in O), tokens=tok)
-        o_off += n
+        O = oracle_states(case, make_prompt_states(case.wl, lens, requests=[i]))
+        tok = make_prompt_tokens(case.wl, lens, requests=[i]) if case.tokens is not None else None
+        cap = {"_only": {"attn"}}
+        zi, hi, st = orc.prefill_one(*O, capture=cap, tokens=tok)
         z_ref.append(zi)
-        hd64 = tensor_to_f64(hd[off[i]:off[i + 1]])
-        err = rel_fro(hd64, hi)
-        say(f"  request {i} (n={n}) h_draft rel err {err:.3e}")
+        states.append(st)
+        caps.append(cap)
+        err = rel_fro(tensor_to_f64(hd[off[i]:off[i + 1]]), hi)
+        say(f"  request {i} (n={int(lens[i])}) h_draft rel err {err:.3e}")
         assert err <= TOL_HDRAFT["bf16"]
-    # z tolerance floors at the batch rms of the GPU's z over all requests
-    floor = float(np.sqrt(np.mean(z ** 2)))
-    dz = np.abs(z[sample] - np.array(z_ref)) / np.maximum(np.abs(z_ref), floor)
-    say(f"  sampled z rel err {dz.max():.3e}")
-    assert dz.max() <= TOL_Z["bf16"]
+    worst = check_attention(attn_pre, [c["attn"] for c in caps], "bf16", "prefill")
+    ez = z_errors(z[sample], z_ref)
+    say(f"  sampled prefill: attention worst rel err {worst:.3e}, z worst rel err {ez.max():.3e}")
+    assert ez.max() <= TOL_Z["bf16"]
+    # one decode step of every request (16-page decode chunks at this batch)
+    S, tk = step_inputs(case, 1), step_tokens(case, 1)
+    zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True, tokens=device_tokens(tk))
+    zs, hs = tensor_to_f64(zs), tensor_to_f64(hs)
+    attn_step = attention_rows(pred, [(i, i + 1) for i in sample])
+    OS = oracle_states(case, S)
+    zr, scaps = [], []
+    for j, i in enumerate(sample):
+        cap = {"_only": {"attn"}}
+        zi, hi = orc.step_one(states[j], OS[0][i], OS[1][i], OS[2][i],
+                              None if tk is None else int(tk[i]), capture=cap)
+        zr.append(zi)
+        scaps.append(cap)
+        assert rel_fro(hs[i], hi) <= TOL_HDRAFT["bf16"], i
+    worst = check_attention(attn_step, [c["attn"] for c in scaps], "bf16", "step")
+    ez = z_errors(zs[sample], zr)
+    say(f"  sampled step: attention worst rel err {worst:.3e}, z worst rel err {ez.max():.3e}")
+    assert ez.max() <= TOL_Z["bf16"]
     pred.close()
 
 
@@ -290,35 +319,60 @@ def test_incremental_steps_equal_prefill_recompute():
     pred.close()
 
 
+@pytest.mark.timeout(600)
 def test_step_batch_sizes_across_row_tile_variants():
     """8B shape: a decode step of B requests in one call (B = 64, 65, 200,
     520: the GEMMs run on 64-, 128-, 128- and 256-row tiles, with different
     K splits) equals the same step taken one request per call (1-row calls)
-    on a second context with the same weights and history: h_draft and z per
-    request within the bf16 tolerance."""
+    on a second context with the same weights and history, to the spread of
+    fp32 summation order (TOL_VARIANT).  Sampled requests of each batched
+    step (both sides of every row-tile boundary) are also checked against
+    the oracle: h_draft, z and the attention output."""
     import torch
     n = 520
     case = make_case(1, lens=[8] * n, n_req=n)
-    say(f"case: 8B bf16, {n} requests of 8 prompt tokens; batched vs one-per-call steps")
+    sample = [0, 31, 63, 64, 127, 128, 199, 255, 256, 519]
+    say(f"case: 8B bf16, {n} requests of 8 prompt tokens; batched vs one-per-call steps; oracle on {sample}")
     pa = make_predictor(case, max_slots=n, max_seq_len=64)
     pb = make_predictor(case, max_slots=n, max_seq_len=64)
     H = device_states(case)
     slots = list(range(n))
     pa.prefill(slots, case.lens, *H)
     pb.prefill(slots, case.lens, *H)
+    orc = oracle_for(case)
+    O = oracle_states(case)
+    states = {}
+    for i in sample:
+        _, _, states[i] = orc.prefill_one(*(x[8 * i:8 * i + 8] for x in O))
     for t, b in enumerate((64, 65, 200, 520), start=1):
-        S = device_states(case, step_inputs(case, t))
-        za, ha = pa.step(slots[:b], *[x[:b] for x in S], want_hdraft=True)
+        S = step_inputs(case, t)
+        SD = device_states(case, S)
+        za, ha = pa.step(slots[:b], *[x[:b] for x in SD], want_hdraft=True)
+        attn_a = attention_rows(pa, [(i, i + 1) for i in sample if i < b])
         zb, hb = [], []
         for i in range(b):
-            z1, h1 = pb.step([i], *[x[i:i + 1] for x in S], want_hdraft=True)
+            z1, h1 = pb.step([i], *[x[i:i + 1] for x in SD], want_hdraft=True)
             zb.append(float(z1[0]))
             hb.append(tensor_to_f64(h1[0]))
         za, ha, zb, hb = tensor_to_f64(za), tensor_to_f64(ha), np.array(zb), np.stack(hb)
         eh = max(rel_fro(ha[i], hb[i]) for i in range(b))
         ez = float(z_errors(za, zb).max())
-        say(f"  B={b}: max h_draft rel err {eh:.2e}, max z err {ez:.2e}")
-        assert eh <= TOL_HDRAFT["bf16"] and ez <= TOL_Z["bf16"], (b, eh, ez)
+        OS = oracle_states(case, S)
+        zr, caps, hr = [], [], []
+        for i in sample:
+            if i >= b:
+                continue
+            cap = {"_only": {"attn"}}
+            zi, hi = orc.step_one(states[i], OS[0][i], OS[1][i], OS[2][i], capture=cap)
+            zr.append(zi)
+            caps.append(cap)
+            hr.append(rel_fro(ha[i], hi))
+        wa = check_attention(attn_a, [c["attn"] for c in caps], "bf16", ("B", b))
+        ezr = float(z_errors(za[[i for i in sample if i < b]], zr).max())
+        say(f"  B={b}: batched vs one-per-call: h_draft {eh:.2e}, z {ez:.2e}; vs oracle: h_draft "
+            f"{max(hr):.2e}, z {ezr:.2e}, attention {wa:.2e}")
+        assert eh <= TOL_VARIANT and ez <= TOL_VARIANT, (b, eh, ez)
+        assert max(hr) <= TOL_HDRAFT["bf16"] and ezr <= TOL_Z["bf16"], (b, max(hr), ezr)
     pa.close()
     pb.close()
 
@@ -327,10 +381,11 @@ def test_prefill_attention_query_tile_variants_agree():
     """8B shape: two 1,500-token requests prefilled alone (prompts average
     >= 1,024 tokens: 64-query attention work items, two 32-query blocks per
     workgroup) and together with two 1-token requests (average 751: 32-query
-    items) give the same h_draft and z for the long requests (measured: bit
-    for bit, since a wave's arithmetic for its 32 queries does not depend on
-    how many blocks its workgroup holds; the bound leaves room for a
-    different K split of a GEMM between the two batch sizes)."""
+    items) give the same attention output, h_draft and z for the long
+    requests (a wave's arithmetic for its 32 queries does not depend on how
+    many blocks its workgroup holds; the GEMM plans of the two batch sizes
+    may differ in fp32 summation order, hence TOL_VARIANT); both variants'
+    attention outputs are checked against the oracle."""
     lens_a = [1500, 1500]
     lens_b = [1500, 1500, 1, 1]
     case = make_case(1, lens=lens_b, n_req=len(lens_b))
@@ -339,12 +394,24 @@ def test_prefill_attention_query_tile_variants_agree():
     pb = make_predictor(case, max_slots=4)
     H = device_states(case)
     za, ha = pa.prefill([0, 1], lens_a, *[x[:3000].contiguous() for x in H], want_hdraft=True)
+    att_a = attention_rows(pa, [(0, 1500), (1500, 3000)])
     zb, hb = pb.prefill([0, 1, 2, 3], lens_b, *H, want_hdraft=True)
+    att_b = attention_rows(pb, [(0, 1500), (1500, 3000)])
     ha, hb = tensor_to_f64(ha), tensor_to_f64(hb)[:3000]
     eh = max(rel_fro(ha[:1500], hb[:1500]), rel_fro(ha[1500:], hb[1500:3000]))
+    ea = max(rel_fro(att_a[i], att_b[i]) for i in range(2))
     ez = float(z_errors(tensor_to_f64(za), tensor_to_f64(zb)[:2]).max())
-    say(f"  h_draft rel err {eh:.2e}, z err {ez:.2e}")
-    assert eh <= TOL_HDRAFT["bf16"] and ez <= TOL_Z["bf16"]
+    orc = oracle_for(case)
+    O = oracle_states(case)
+    caps = []
+    for i in range(2):
+        cap = {"_only": {"attn"}}
+        orc.prefill_one(*(x[1500 * i:1500 * (i + 1)] for x in O), capture=cap)
+        caps.append(cap)
+    wa = check_attention(att_a, [c["attn"] for c in caps], "bf16", "64-query items")
+    wb = check_attention(att_b, [c["attn"] for c in caps], "bf16", "32-query items")
+    say(f"  variants: attention {ea:.2e}, h_draft {eh:.2e}, z {ez:.2e}; vs oracle: attention {wa:.2e} / {wb:.2e}")
+    assert ea <= TOL_VARIANT and eh <= TOL_VARIANT and ez <= TOL_VARIANT
     pa.close()
     pb.close()
 
@@ -395,9 +462,51 @@ def test_error_paths_leave_state_unchanged():
 
 
 def test_decode_steps_over_long_caches_merge_chunks():
-    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (1024-key chunks), 3 steps")
+    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (16-page = 256-key chunks), 3 steps")
     case = make_case(1, lens=[1100, 600, 40], shape=reduced_shape(), n_req=3)
     _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
+
+
+@pytest.mark.parametrize("n_req,chunk_pages", [(100, 32), (160, 64)])
+def test_decode_chunk_sizes_against_oracle(n_req, chunk_pages):
+    """bf16 d=512 8q/2kv hd128: n_req caches of 1,030..1,100 tokens (65..69
+    pages), so the step's split-KV work items take 32-page chunks (100
+    requests: 64-page chunks would give fewer than two waves per CU) or
+    64-page chunks (160 requests), two or three chunks per request merged by
+    the combine kernel.  Two steps; the oracle recomputes sampled requests:
+    attention output, h_draft and z of every step."""
+    lens = [1030 + (37 * i) % 71 for i in range(n_req)]
+    case = make_case(1, lens=lens, shape=reduced_shape(), n_req=n_req)
+    sample = sorted({0, 1, n_req // 2, n_req - 1, int(np.argmax(lens)), int(np.argmin(lens))})
+    say(f"case: bf16 reduced shape, {n_req} caches of 1030..1100 tokens ({chunk_pages}-page decode chunks), "
+        f"2 steps, oracle on {sample}")
+    pred = make_predictor(case, max_seq_len=1100 + 16)
+    slots = list(range(n_req))
+    pred.prefill(slots, case.lens, *device_states(case))
+    orc = oracle_for(case)
+    O = oracle_states(case)
+    off = np.concatenate([[0], np.cumsum(case.lens)])
+    states = {}
+    for i in sample:
+        _, _, states[i] = orc.prefill_one(*(x[off[i]:off[i + 1]] for x in O))
+    for t in (1, 2):
+        S = step_inputs(case, t)
+        zs, hs = pred.step(slots, *device_states(case, S), want_hdraft=True)
+        zs, hs = tensor_to_f64(zs), tensor_to_f64(hs)
+        got = attention_rows(pred, [(i, i + 1) for i in sample])
+        OS = oracle_states(case, S)
+        zr, caps = [], []
+        for i in sample:
+            cap = {"_only": {"attn"}}
+            zi, hi = orc.step_one(states[i], OS[0][i], OS[1][i], OS[2][i], capture=cap)
+            zr.append(zi)
+            caps.append(cap)
+            assert rel_fro(hs[i], hi) <= TOL_HDRAFT["bf16"], (t, i)
+        wa = check_attention(got, [c["attn"] for c in caps], "bf16", ("step", t))
+        ez = float(z_errors(zs[sample], zr).max())
+        say(f"  step {t}: attention worst rel err {wa:.3e}, z {ez:.3e}")
+        assert ez <= TOL_Z["bf16"]
+    pred.close()
 
 
 def test_decode_steps_8b_shape():
@@ -427,7 +536,7 @@ def test_gated_attention_e4m3_reduced_shape_and_steps():
 
 
 def test_gated_attention_decode_over_multi_chunk_caches():
-    say("case: Gated Attention, bf16 d=512 8q/2kv hd128, caches of 2100/600/40 tokens, 3 steps")
+    say("case: Gated Attention, bf16 d=512 8q/2kv hd128, caches of 2100/600/40 tokens (256-key chunks), 3 steps")
     case = make_case(1, lens=[2100, 600, 40], shape=reduced_shape(), n_req=3, attn_gate=True)
     _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
 
@@ -675,3 +784,63 @@ def test_input_embeddings_need_token_ids_and_weights():
     with pytest.raises(B.OutletsError) as ei:
         make_predictor(bad)
     assert ei.value.rc == B.OUTLETS_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------- e4m3 weight decoding
+
+
+def test_e4m3_gemm_decodes_all_256_codes_exactly():
+    """Every OCP e4m3 code through the e4m3-weight GEMM, bit for bit: the
+    fused projection's W_proj holds the 256 codes (twice, in three
+    differently shifted columns, one per state tensor), its row scales are
+    1.0, and each token's states are one-hot on one of those columns, so the
+    fp32 FUSED row is that column's decoded codes (0 * NaN makes a row with
+    a NaN code NaN for every token).  Compared exactly with the oracle's
+    decode (fp64, exact for every e4m3 value) on a 600-token prefill
+    (256-row tiles and a ragged tail) and on a 3-request decode step (the
+    small-M split-K path)."""
+    import dataclasses
+    import torch
+    from oracle import decode_weight, fuse
+    d = 512
+    case = make_case(4, lens=[200, 250, 150], shape=reduced_shape(), n_req=3)
+    cols = [5, d + 300, 2 * d + 511]                 # one hot column in each of h_low, h_mid, h_high
+    codes = np.zeros((d, 3 * d), dtype=np.uint8)
+    for j, (c, shift) in enumerate(zip(cols, (0, 85, 170))):
+        codes[:, c] = (np.arange(d) + shift) % 256
+    W = dict(case.weights)
+    W["w_proj"] = (codes, np.full(d, 0x3F80, dtype=np.uint16))   # bf16 1.0 row scales
+    case = dataclasses.replace(case, weights=W)
+    w_ref = decode_weight(W["w_proj"], "e4m3")
+    say("case: e4m3 GEMM, all 256 codes in W_proj, one-hot states, unit scales; prefill of 600 tokens + 1 step")
+
+    def one_hot(rows, hot):
+        X = np.zeros((rows, 3 * d))
+        X[np.arange(rows), hot] = 1.0
+        bits = (X.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)     # exact in bf16
+        return X, [np.ascontiguousarray(bits[:, s * d:(s + 1) * d]) for s in range(3)]
+
+    def check(pred, X, label):
+        got = tensor_to_f64(pred.buffer("FUSED", torch.float32)).reshape(X.shape[0], d)
+        ref = fuse(w_ref, X[:, :d], X[:, d:2 * d], X[:, 2 * d:])
+        assert np.array_equal(np.isnan(got), np.isnan(ref)), label
+        assert np.array_equal(got, ref, equal_nan=True), label
+        # every finite code is read somewhere outside the NaN rows
+        ok = ~np.isnan(ref).any(axis=0)
+        seen = set()
+        for r, c in enumerate(np.asarray(X).argmax(axis=1)):
+            seen.update(int(v) for v in codes[ok, c])
+        assert seen >= set(range(256)) - {0x7F, 0xFF}, label
+        assert np.isnan(ref[:, codes[:, cols[0]] == 0x7F]).all()
+        return int(np.isnan(ref).any(axis=0).sum())
+
+    pred = make_predictor(case, keep=True, max_seq_len=300)
+    T = int(case.lens.sum())
+    X, S = one_hot(T, [cols[r % 3] for r in range(T)])
+    pred.prefill([0, 1, 2], case.lens, *device_states(case, S))
+    nan_rows = check(pred, X, "prefill")
+    Xs, Ss = one_hot(3, cols)
+    pred.step([0, 1, 2], *device_states(case, Ss))
+    check(pred, Xs, "step")
+    say(f"  FUSED bit-exact vs decoded codes on {T} + 3 rows ({nan_rows} NaN output rows from the NaN codes)")
+    pred.close()
