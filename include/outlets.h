@@ -241,6 +241,34 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
                          int64_t row_stride, const int32_t* tokens, float* z_out,
                          void* hdraft_out, void* stream);
 
+/*
+ * outlets_predict_step without device allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Arguments, results, state changes and
+ * error codes are those of outlets_predict_step (same kernels and split
+ * plans, so the same bits), except:
+ *   - the call's per-call device buffers (activations, split-K / split-KV /
+ *     head partial sums, token metadata) live in the library's static
+ *     scratch array of 256 MiB on each device, not in the context: a step
+ *     whose buffers exceed it fails with OUTLETS_ERR_INVALID_ARG and no
+ *     state change (8B shape: up to 512 requests fit);
+ *   - every no-allocation call on one device shares that array and it keeps
+ *     the last call's contents: calls that overlap on one device (several
+ *     contexts, streams or threads) race;
+ *   - contexts created with keep_intermediates are refused
+ *     (OUTLETS_ERR_UNSUPPORTED); after this call outlets_get_buffer (other
+ *     than the KV pools), the device entries of outlets_get_meta and
+ *     outlets_draft_distribution fail with OUTLETS_ERR_INVALID_ARG until the
+ *     next outlets_predict_prefill / outlets_predict_step;
+ *   - per-kernel timing (outlets_profile_enable) records nothing for it.
+ * It calls no hipMalloc / hipFree; nothing in the scratch needs clearing
+ * (every kernel writes what a later one reads).
+ */
+int outlets_predict_step_noalloc(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
+                                 const void* h_low, const void* h_mid, const void* h_high,
+                                 int64_t row_stride, const int32_t* tokens, float* z_out,
+                                 void* hdraft_out, void* stream);
+
 /* End requests: frees their pages and state.  Inactive slots are a no-op;
  * an out-of-range or repeated slot fails with no change. */
 int outlets_release(outlets_ctx* ctx, int32_t n, const int32_t* slots);

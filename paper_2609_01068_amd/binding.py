@@ -90,6 +90,7 @@ _SIGS = {
     "outlets_destroy": (C.c_int, [_P]),
     "outlets_predict_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P, _P]),
     "outlets_predict_step": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P, _P]),
+    "outlets_predict_step_noalloc": (C.c_int, [_P, C.c_int32, _I32P, _P, _P, _P, C.c_int64, _P, _P, _P, _P]),
     "outlets_release": (C.c_int, [_P, C.c_int32, _I32P]),
     "outlets_probe_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P, _P, C.c_int64, _P, _P]),
     "outlets_probe_step": (C.c_int, [_P, C.c_int32, _I32P, _P, C.c_int64, _P, _P]),
@@ -181,6 +182,13 @@ def outlets_predict_step(ctx, slots, h_low: int, h_mid: int, h_high: int, row_st
                          stream: Optional[int]) -> int:
     return lib().outlets_predict_step(ctx, len(slots), i32_array(slots), h_low, h_mid, h_high, row_stride,
                                       tokens, z_out, hdraft_out, stream)
+
+
+def outlets_predict_step_noalloc(ctx, slots, h_low: int, h_mid: int, h_high: int, row_stride: int,
+                                 tokens: Optional[int], z_out: int, hdraft_out: Optional[int],
+                                 stream: Optional[int]) -> int:
+    return lib().outlets_predict_step_noalloc(ctx, len(slots), i32_array(slots), h_low, h_mid, h_high,
+                                              row_stride, tokens, z_out, hdraft_out, stream)
 
 
 def outlets_release(ctx, slots) -> int:

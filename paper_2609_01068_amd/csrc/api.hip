@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -45,38 +46,36 @@ constexpr int kHeadSplits = 8;      // K splits of the length head GEMM (at leas
 
 }  // namespace
 
-struct outlets_ctx {
-    outlets_config cfg{};
-    outlets_weights w{};
-    int device = 0;
-    int act_fmt = 0, w_fmt = 0, small_fmt = 0;  // small_fmt: gains and head
-    int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
-    bool gated = false;          // Gated Attention: q|k|v|g rows, output gate in attention
-    bool probe = false;          // MLP probe weights present
-    bool embed_in = false;       // EAGLE-3 input embeddings: attention reads [emb ; norm(f)] (2d)
-    int64_t k_attn = 0;          // width of the attention block's input row: d or 2d
-    void* e_norm = nullptr;      // [T, d] act: RMSNorm(embed[token]) * gamma_emb
-    std::vector<int32_t> probe_count;   // per slot: tokens pooled by the probe (0 = inactive)
-    float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
-    int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
-    float* lm_logits = nullptr;  // draft model head logits [2 * max_batch_requests, V]
-    std::unique_ptr<Pager> pager;
-    int max_pages = 0;
+// Static scratch of outlets_predict_step_noalloc: one decode step's per-call
+// buffers for callers that cannot allocate device memory.  Each device that
+// loads the library holds its own copy until the process ends; every
+// no-allocation step on that device works in it, so such calls must not
+// overlap on one device.  Host code never passes `scratch` itself to a
+// kernel (in host code it names a host-side stand-in): it uses the device
+// address hipGetSymbolAddress returns, looked up once per device.
+static constexpr size_t kScratchBytes = static_cast<size_t>(256) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
-    std::vector<void*> allocs;
-    void* kpool = nullptr;
-    void* vpool = nullptr;
-    int32_t* page_table = nullptr;
-    float* pool_sum = nullptr;
-    float* cos_t = nullptr;
-    float* sin_t = nullptr;
+namespace {
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};   // device address of `scratch`, per device
+
+}  // namespace
+
+// Device buffers a predict call works in: activations, partial sums and the
+// call's metadata.  The context owns one set (sized at create for its
+// capacities); outlets_predict_step_noalloc lays another set over the
+// library's static scratch array.
+struct CallBufs {
     float* r_f = nullptr;   // residual stream: f_ctx, x1, x2, h_draft (aliases unless kept)
     float* r_x1 = nullptr;
     float* r_x2 = nullptr;
     float* r_h = nullptr;
     void* a_norm = nullptr;
     void* b_norm = nullptr;
+    void* e_norm = nullptr;      // [T, d] act: RMSNorm(embed[token]) * gamma_emb
     void* qkv = nullptr;
     void* attn = nullptr;
     void* mlp = nullptr;
@@ -88,16 +87,44 @@ struct outlets_ctx {
     int32_t* last_idx = nullptr;
     int32_t* d_meta = nullptr;   // req_off | req_slot | req_start | page updates | work list
     int64_t meta_cap = 0;        // int32 entries
+    float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
+    float* decode_part = nullptr;  // split-KV decode attention partials
+    float* splitk_ws = nullptr;  // fp32 partial sums of split-K GEMMs
+    size_t splitk_bytes = 0;
+};
+
+struct outlets_ctx {
+    outlets_config cfg{};
+    outlets_weights w{};
+    int device = 0;
+    int act_fmt = 0, w_fmt = 0, small_fmt = 0;  // small_fmt: gains and head
+    int64_t d = 0, qdim = 0, kvdim = 0, qkv_dim = 0, F = 0, H1 = 0;
+    bool gated = false;          // Gated Attention: q|k|v|g rows, output gate in attention
+    bool probe = false;          // MLP probe weights present
+    bool embed_in = false;       // EAGLE-3 input embeddings: attention reads [emb ; norm(f)] (2d)
+    int64_t k_attn = 0;          // width of the attention block's input row: d or 2d
+    std::vector<int32_t> probe_count;   // per slot: tokens pooled by the probe (0 = inactive)
+    float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
+    int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
+    float* lm_logits = nullptr;  // draft model head logits [2 * max_batch_requests, V]
+    std::unique_ptr<Pager> pager;
+    int max_pages = 0;
+
+    std::vector<void*> allocs;
+    CallBufs cb;                 // the context's own per-call buffers
+    void* kpool = nullptr;
+    void* vpool = nullptr;
+    int32_t* page_table = nullptr;
+    float* pool_sum = nullptr;
+    float* cos_t = nullptr;
+    float* sin_t = nullptr;
+
     int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
     int32_t n_work = 0;
     int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
     int32_t dec_chunk = 64;        // pages per decode attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
     int32_t n_tiles = 0;
-    float* pool_part = nullptr;  // [max tiles, d] prefill pooling partial sums
-    float* decode_part = nullptr;  // split-KV decode attention partials
-    float* splitk_ws = nullptr;  // fp32 partial sums of small-M split-K GEMMs
-    size_t splitk_bytes = 0;
 
     int32_t* h_stage[2] = {nullptr, nullptr};
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -105,6 +132,8 @@ struct outlets_ctx {
     int stage = 0;
 
     int32_t last_n = 0, last_T = 0;
+    bool last_in_scratch = false;   // the last predict call ran in the static scratch
+    void* scratch = nullptr;        // this device's address of the static scratch
 
     // per-kernel timing (outlets_profile_enable)
     bool prof_on = false;
@@ -182,6 +211,21 @@ void collect_marks(outlets_ctx* c) {
     c->marks.clear();
 }
 
+// Device address of the static scratch on `device` (the current device),
+// looked up once per device and kept.
+int scratch_address(int device, void** out) {
+    if (device < 0 || device >= kMaxDevices) return fail(OUTLETS_ERR_UNSUPPORTED, "device index above 63");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[device]) {
+        void* p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(OUTLETS_ERR_HIP, "hipGetSymbolAddress(scratch) returned null");
+        g_scratch_dev[device] = p;
+    }
+    *out = g_scratch_dev[device];
+    return OUTLETS_OK;
+}
+
 int check_config(const outlets_config& c, const char** why) {
     auto bad = [&](int rc, const char* msg) { *why = msg; return rc; };
     if (c.d_model <= 0 || c.n_q_heads <= 0 || c.n_kv_heads <= 0 || c.ffn_dim <= 0 || c.head_hidden <= 0)
@@ -238,7 +282,7 @@ struct LayerGemms {
     int64_t n_gu;
 };
 
-LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, const void* hh,
+LayerGemms layer_gemms(const outlets_ctx* c, const CallBufs& b, const void* hl, const void* hm, const void* hh,
                        int64_t row_stride) {
     LayerGemms g{};
     const auto& w = c->w;
@@ -249,10 +293,10 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
     g.b_fuse = gemm_b1(w.w_proj, w.s_proj, d, 3 * d);
     if (c->embed_in) {
         // input embeddings: K = 2d over [normed embedding | normed f_ctx]
-        g.a_qkv = gemm_a(c->e_norm, d, d);
-        g.a_qkv.p[1] = c->a_norm;
+        g.a_qkv = gemm_a(b.e_norm, d, d);
+        g.a_qkv.p[1] = b.a_norm;
     } else {
-        g.a_qkv = gemm_a(c->a_norm, d, d);
+        g.a_qkv = gemm_a(b.a_norm, d, d);
     }
     g.b_qkv = gemm_b1(w.w_q, w.s_q, c->qdim, c->k_attn);
     g.b_qkv.p[1] = w.w_k;
@@ -268,9 +312,9 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
         g.b_qkv.p[3] = w.w_attn_gate;
         g.b_qkv.scale[3] = static_cast<const uint16_t*>(w.s_attn_gate);
     }
-    g.a_o = gemm_a(c->attn, c->qdim, c->qdim);
+    g.a_o = gemm_a(b.attn, c->qdim, c->qdim);
     g.b_o = gemm_b1(w.w_o, w.s_o, d, c->qdim);
-    g.a_gu = gemm_a(c->b_norm, d, d);
+    g.a_gu = gemm_a(b.b_norm, d, d);
     g.b_gu = gemm_b1(w.w_gate, w.s_gate, c->F, d);
     g.b_gu.p[1] = w.w_up;
     g.b_gu.scale[1] = static_cast<const uint16_t*>(w.s_up);
@@ -280,12 +324,12 @@ LayerGemms layer_gemms(const outlets_ctx* c, const void* hl, const void* hm, con
         g.b_gu.paired = 1;        // 32-row gate/up interleave
         g.n_gu = 2 * c->F;
     }
-    g.a_down = gemm_a(c->mlp, c->F, c->F);
+    g.a_down = gemm_a(b.mlp, c->F, c->F);
     g.b_down = gemm_b1(w.w_down, w.s_down, d, c->F);
     if (c->w_fmt == FMT_F32)
-        g.a_head = gemm_a(c->pooled, 2 * d, 2 * d);
+        g.a_head = gemm_a(b.pooled, 2 * d, 2 * d);
     else
-        g.a_head = gemm_a(c->pooled_bf16, 2 * d, 2 * d);
+        g.a_head = gemm_a(b.pooled_bf16, 2 * d, 2 * d);
     g.b_head = gemm_b1(w.head_w1, nullptr, c->H1, 2 * d);
     return g;
 }
@@ -307,13 +351,13 @@ int head_splits(const outlets_ctx* c, int rows) {
 }
 
 GemmA lm_input(const outlets_ctx* c) {
-    return (c->w_fmt == FMT_F32) ? gemm_a(c->pooled + c->d, 2 * c->d, c->d)
-                                 : gemm_a(c->pooled_bf16 + c->d, 2 * c->d, c->d);
+    return (c->w_fmt == FMT_F32) ? gemm_a(c->cb.pooled + c->d, 2 * c->d, c->d)
+                                 : gemm_a(c->cb.pooled_bf16 + c->d, 2 * c->d, c->d);
 }
 
 int check_gemms(const outlets_ctx* c) {
     // Dummy 16-byte aligned pointers stand in for the per-call A operands.
-    LayerGemms g = layer_gemms(c, c->a_norm, c->a_norm, c->a_norm, c->d);
+    LayerGemms g = layer_gemms(c, c->cb, c->cb.a_norm, c->cb.a_norm, c->cb.a_norm, c->d);
     const char* why = nullptr;
     const int af = c->act_fmt, wf = c->w_fmt;
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
@@ -336,69 +380,69 @@ int check_gemms(const outlets_ctx* c) {
 
 // Queue the draft layer + head for `T` tokens of `n` requests whose
 // metadata is already on the device.
-int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const void* hm,
+int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, const void* hl, const void* hm,
               const void* hh, int64_t row_stride, const int32_t* tokens, float* z_out,
               void* hdraft_out, hipStream_t st) {
     const int af = c->act_fmt, wf = c->w_fmt;
     const int64_t d = c->d;
-    LayerGemms g = layer_gemms(c, hl, hm, hh, row_stride);
-    const int32_t* req_off = c->d_meta;
-    const int32_t* req_slot = c->d_meta + (n + 1);
-    const int32_t* req_start = c->d_meta + (n + 1) + n;
+    LayerGemms g = layer_gemms(c, b, hl, hm, hh, row_stride);
+    const int32_t* req_off = b.d_meta;
+    const int32_t* req_slot = b.d_meta + (n + 1);
+    const int32_t* req_start = b.d_meta + (n + 1) + n;
     const float eps = c->cfg.rms_eps;
 
     // Eq. 1: f_ctx = W_proj [h_low | h_mid | h_high]
     { KTimer t(c, OUTLETS_K_FUSE_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
+      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(b.r_f, d), 1, st, b.splitk_ws, b.splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, c->r_f, d, c->w.gamma_attn, eps, c->a_norm, d, nullptr, 0, st);
+      launch_rmsnorm(af, c->small_fmt, T, d, b.r_f, d, c->w.gamma_attn, eps, b.a_norm, d, nullptr, 0, st);
       if (c->embed_in)
           launch_embed_norm(af, c->small_fmt, T, static_cast<int>(d), c->cfg.vocab, tokens, c->w.embed,
-                            c->w.gamma_emb, eps, c->e_norm, d, st); }
+                            c->w.gamma_emb, eps, b.e_norm, d, st); }
     // QKV projection; with bf16 activations and head dim 128, RoPE and the
     // paged K/V write happen in its epilogue (or in its split-K reduce)
     if (gemm_qkv_rope_fusable(af, wf, c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim,
                               static_cast<int>(c->qkv_dim))) {
         KTimer t(c, OUTLETS_K_QKV_GEMM, st);
-        GemmC qc = gemm_c(c->qkv, c->qkv_dim);
-        qc.rope = RopeKV{c->tok_pos, c->tok_slot, c->page_table, static_cast<int32_t>(c->max_pages),
+        GemmC qc = gemm_c(b.qkv, c->qkv_dim);
+        qc.rope = RopeKV{b.tok_pos, b.tok_slot, c->page_table, static_cast<int32_t>(c->max_pages),
                          c->cfg.n_q_heads, c->cfg.n_kv_heads, static_cast<uint16_t*>(c->kpool),
                          static_cast<uint16_t*>(c->vpool), c->cos_t, c->sin_t};
         gemm_launch(af, wf, EPI_QKV_ROPE, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, qc, 1, st,
-                    c->splitk_ws, c->splitk_bytes);
+                    b.splitk_ws, b.splitk_bytes);
     } else {
         { KTimer t(c, OUTLETS_K_QKV_GEMM, st);
-          gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, gemm_c(c->qkv, c->qkv_dim), 1, st, c->splitk_ws, c->splitk_bytes); }
+          gemm_launch(af, wf, EPI_STORE_ACT, T, c->qkv_dim, static_cast<int>(c->k_attn), g.a_qkv, g.b_qkv, gemm_c(b.qkv, c->qkv_dim), 1, st, b.splitk_ws, b.splitk_bytes); }
         { KTimer t(c, OUTLETS_K_ROPE_KV, st);
-          launch_rope_kv(af, T, c->qkv, c->qkv_dim, c->tok_slot, c->tok_pos, c->page_table, c->max_pages,
+          launch_rope_kv(af, T, b.qkv, c->qkv_dim, b.tok_slot, b.tok_pos, c->page_table, c->max_pages,
                          c->kpool, c->vpool, c->cos_t, c->sin_t, c->cfg.n_q_heads, c->cfg.n_kv_heads,
                          c->cfg.head_dim, st); }
     }
     { KTimer t(c, OUTLETS_K_ATTN, st);
-      const void* gate = c->gated ? static_cast<const char*>(c->qkv) + (c->qdim + 2 * c->kvdim) * fmt_bytes(af)
+      const void* gate = c->gated ? static_cast<const char*>(b.qkv) + (c->qdim + 2 * c->kvdim) * fmt_bytes(af)
                                   : nullptr;
       if (prefill && c->n_work > 0)
-          launch_attn_prefill(c->n_work, c->d_meta + c->work_off, c->attn_qtile, c->qkv, c->qkv_dim, c->attn, c->qdim,
+          launch_attn_prefill(c->n_work, b.d_meta + c->work_off, c->attn_qtile, b.qkv, c->qkv_dim, b.attn, c->qdim,
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
-          launch_attn_decode(n, c->n_work, c->dec_chunk, c->d_meta + c->work_off, c->d_meta + c->tiles_off, c->qkv,
-                             c->qkv_dim, c->attn, c->qdim, req_slot, req_start, c->page_table,
+          launch_attn_decode(n, c->n_work, c->dec_chunk, b.d_meta + c->work_off, b.d_meta + c->tiles_off, b.qkv,
+                             c->qkv_dim, b.attn, c->qdim, req_slot, req_start, c->page_table,
                              c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
-                             c->decode_part, gate, st);
+                             b.decode_part, gate, st);
       else
-          launch_attn_paged(af, T, c->qkv, c->qkv_dim, c->attn, c->qdim, c->tok_slot, c->tok_pos,
+          launch_attn_paged(af, T, b.qkv, c->qkv_dim, b.attn, c->qdim, b.tok_slot, b.tok_pos,
                             c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
                             c->cfg.n_kv_heads, c->cfg.head_dim, gate, st); }
     { KTimer t(c, OUTLETS_K_O_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(c->r_x1, d, c->r_f, d), 1, st, c->splitk_ws, c->splitk_bytes); }
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(b.r_x1, d, b.r_f, d), 1, st, b.splitk_ws, b.splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, c->r_x1, d, c->w.gamma_mlp, eps, c->b_norm, d, nullptr, 0, st); }
+      launch_rmsnorm(af, c->small_fmt, T, d, b.r_x1, d, c->w.gamma_mlp, eps, b.b_norm, d, nullptr, 0, st); }
     { KTimer t(c, OUTLETS_K_GATE_UP_GEMM, st);
-      gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(c->mlp, c->F), 1, st, c->splitk_ws, c->splitk_bytes); }
+      gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(b.mlp, c->F), 1, st, b.splitk_ws, b.splitk_bytes); }
     { KTimer t(c, OUTLETS_K_DOWN_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(c->r_x2, d, c->r_x1, d), 1, st, c->splitk_ws, c->splitk_bytes); }
-    uint16_t* pb = (wf == FMT_F32) ? nullptr : c->pooled_bf16;
+      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(b.r_x2, d, b.r_x1, d), 1, st, b.splitk_ws, b.splitk_bytes); }
+    uint16_t* pb = (wf == FMT_F32) ? nullptr : b.pooled_bf16;
     // prefill: final RMSNorm + pooling in one pass over x2 (h_draft rows are
     // stored only when the caller wants them or intermediates are kept; the
     // pooling needs only each request's last row)
@@ -406,36 +450,36 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
     if (prefill) {
         KTimer t(c, OUTLETS_K_POOL, st);
         fused_pool = launch_norm_pool_prefill(
-            af, c->small_fmt, n, c->n_tiles, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d,
-            hdraft_out != nullptr || c->cfg.keep_intermediates != 0, req_off, req_slot, c->d_meta + c->tiles_off,
-            c->pool_part, c->pool_sum, c->pooled, pb, st);
+            af, c->small_fmt, n, c->n_tiles, d, b.r_x2, d, c->w.gamma_final, eps, hdraft_out, d, b.r_h, d,
+            hdraft_out != nullptr || c->cfg.keep_intermediates != 0, req_off, req_slot, b.d_meta + c->tiles_off,
+            b.pool_part, c->pool_sum, b.pooled, pb, st);
     } else {
         // steps (one row per request): the f32 h_draft rows are kept only
         // with intermediates
         KTimer t(c, OUTLETS_K_POOL, st);
-        fused_pool = launch_norm_pool_step(af, c->small_fmt, n, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d,
-                                           c->cfg.keep_intermediates ? c->r_h : nullptr, d, req_slot, req_start,
-                                           c->pool_sum, c->pooled, pb, st);
+        fused_pool = launch_norm_pool_step(af, c->small_fmt, n, d, b.r_x2, d, c->w.gamma_final, eps, hdraft_out, d,
+                                           c->cfg.keep_intermediates ? b.r_h : nullptr, d, req_slot, req_start,
+                                           c->pool_sum, b.pooled, pb, st);
     }
     if (!fused_pool) {
         { KTimer t(c, OUTLETS_K_NORM, st);
-          launch_rmsnorm(af, c->small_fmt, T, d, c->r_x2, d, c->w.gamma_final, eps, hdraft_out, d, c->r_h, d, st); }
+          launch_rmsnorm(af, c->small_fmt, T, d, b.r_x2, d, c->w.gamma_final, eps, hdraft_out, d, b.r_h, d, st); }
         { KTimer t(c, OUTLETS_K_POOL, st);
           if (prefill)
-              launch_pool_prefill(n, c->n_tiles, d, FMT_F32, c->r_h, d, req_off, req_slot, c->d_meta + c->tiles_off,
-                                  c->pool_part, c->pool_sum, c->pooled, pb, st);
+              launch_pool_prefill(n, c->n_tiles, d, FMT_F32, b.r_h, d, req_off, req_slot, b.d_meta + c->tiles_off,
+                                  b.pool_part, c->pool_sum, b.pooled, pb, st);
           else
-              launch_pool_step(n, d, FMT_F32, c->r_h, d, req_slot, req_start, c->pool_sum, c->pooled, pb, st); }
+              launch_pool_step(n, d, FMT_F32, b.r_h, d, req_slot, req_start, c->pool_sum, b.pooled, pb, st); }
     }
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
     // bf16 heads read the hi/lo split of the pooled vector: 2n rows
     const int head_rows = (wf == FMT_F32) ? n : 2 * n;
-    GemmC hc = gemm_c(c->head_part, c->H1);
+    GemmC hc = gemm_c(b.head_part, c->H1);
     hc.split_stride = static_cast<int64_t>(head_rows) * c->H1;
     const int hs = head_splits(c, head_rows);
     { KTimer t(c, OUTLETS_K_HEAD, st);
       gemm_launch(af, hf, EPI_PARTIAL, head_rows, c->H1, 2 * d, g.a_head, g.b_head, hc, hs, st);
-      launch_head_finish(c->small_fmt, n, c->H1, hs, c->head_part, c->w.head_b1, c->w.head_w2,
+      launch_head_finish(c->small_fmt, n, c->H1, hs, b.head_part, c->w.head_b1, c->w.head_w2,
                          c->w.head_b2, z_out, st); }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -443,13 +487,13 @@ int run_layer(outlets_ctx* c, bool prefill, int n, int T, const void* hl, const 
 }
 
 // Stage req_off | req_slot | req_start | updates into pinned memory and copy to the device.
-int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const int32_t* slots,
+int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int32_t>& off, const int32_t* slots,
                 const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
                 const std::vector<int32_t>& work, const std::vector<int32_t>& cu_tiles,
                 hipStream_t st) {
     const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size()) +
                           static_cast<int64_t>(work.size()) + static_cast<int64_t>(cu_tiles.size());
-    if (count > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
+    if (count > b.meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
     int32_t* h = c->h_stage[s];
@@ -463,15 +507,15 @@ int upload_meta(outlets_ctx* c, int n, const std::vector<int32_t>& off, const in
     c->tiles_off = c->work_off + static_cast<int64_t>(work.size());
     c->n_tiles = cu_tiles.empty() ? 0 : cu_tiles.back();
     if (!cu_tiles.empty()) std::memcpy(h + c->tiles_off, cu_tiles.data(), sizeof(int32_t) * cu_tiles.size());
-    HIP_TRY(hipMemcpyAsync(c->d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
+    HIP_TRY(hipMemcpyAsync(b.d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
     c->stage ^= 1;
     KTimer t(c, OUTLETS_K_META, st);
     if (!updates.empty())
-        launch_scatter_i32(static_cast<int>(updates.size() / 2), c->d_meta + 3 * n + 1, c->page_table, st);
-    launch_build_tokens(n, c->d_meta, c->d_meta + n + 1, c->d_meta + 2 * n + 1, c->tok_slot,
-                        c->tok_pos, c->last_idx, st);
+        launch_scatter_i32(static_cast<int>(updates.size() / 2), b.d_meta + 3 * n + 1, c->page_table, st);
+    launch_build_tokens(n, b.d_meta, b.d_meta + n + 1, b.d_meta + 2 * n + 1, b.tok_slot,
+                        b.tok_pos, b.last_idx, st);
     return OUTLETS_OK;
 }
 
@@ -501,6 +545,153 @@ int check_states(const outlets_ctx* c, const void* hl, const void* hm, const voi
     if (row_stride < c->d) return fail(OUTLETS_ERR_INVALID_ARG, "row_stride < d_model");
     if (c->act_fmt == FMT_BF16 && (row_stride % 8 || !aligned16(hl) || !aligned16(hm) || !aligned16(hh)))
         return fail(OUTLETS_ERR_UNSUPPORTED, "bf16 states need 16-byte aligned rows (row_stride % 8 == 0)");
+    return OUTLETS_OK;
+}
+
+// ---------------------------------------------------------------- decode steps
+
+// Buffers of a decode step of n requests laid over `base` (256-byte aligned
+// pieces): metadata (meta_count int32), token arrays, activations, pooled
+// rows, and one region shared by the split-K workspace (ws_bytes), the
+// split-KV attention partials and the head partials, whose uses are ordered
+// one after another on the call's stream.  With base == nullptr only the
+// size is computed.  Returns the bytes used.
+size_t layout_step(const outlets_ctx* c, int n, int64_t n_chunks, int64_t meta_count, size_t ws_bytes,
+                   char* base, CallBufs* b) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char* {
+        off = (off + 255) & ~static_cast<size_t>(255);
+        char* p = base ? base + off : nullptr;
+        off += bytes;
+        return p;
+    };
+    const size_t ab = fmt_bytes(c->act_fmt);
+    const size_t N = static_cast<size_t>(n);
+    *b = CallBufs{};
+    b->meta_cap = meta_count;
+    b->d_meta = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * meta_count));
+    b->tok_slot = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * N));
+    b->tok_pos = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * N));
+    b->last_idx = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * N));
+    b->r_f = b->r_x1 = b->r_x2 = b->r_h = reinterpret_cast<float*>(take(sizeof(float) * N * c->d));
+    b->a_norm = b->b_norm = take(ab * N * c->d);
+    if (c->embed_in) b->e_norm = take(ab * N * c->d);
+    b->qkv = take(ab * N * c->qkv_dim);
+    b->attn = take(ab * N * c->qdim);
+    b->mlp = take(ab * N * c->F);
+    b->pooled = reinterpret_cast<float*>(take(sizeof(float) * N * 2 * c->d));
+    if (c->w_fmt != FMT_F32) b->pooled_bf16 = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * 2 * N * 2 * c->d));
+    size_t region = ws_bytes;
+    if (attn_prefill_mfma_supported(c->act_fmt, c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim))
+        region = std::max(region, sizeof(float) * static_cast<size_t>(n_chunks) * c->cfg.n_q_heads *
+                                      attn_decode_record_floats());
+    const int rows = (c->w_fmt == FMT_F32 ? 1 : 2) * n;
+    region = std::max(region, sizeof(float) * static_cast<size_t>(head_splits(c, rows)) * rows * c->H1);
+    char* shared = take(region);
+    b->splitk_ws = b->decode_part = b->head_part = reinterpret_cast<float*>(shared);
+    b->splitk_bytes = ws_bytes;
+    return off;
+}
+
+// Split-K workspace the layer's GEMMs use at M rows with the context's own
+// workspace capacity (so a step in the static scratch takes the same plans,
+// and gives the same results, as one in the context's buffers).
+size_t step_splitk_bytes(const outlets_ctx* c, int M) {
+    const int qkv_epi = gemm_qkv_rope_fusable(c->act_fmt, c->w_fmt, c->cfg.n_q_heads, c->cfg.n_kv_heads,
+                                              c->cfg.head_dim, static_cast<int>(c->qkv_dim))
+                            ? EPI_QKV_ROPE : EPI_STORE_ACT;
+    const int64_t n_gu = (c->w_fmt == FMT_F32) ? c->F : 2 * c->F;
+    const int64_t nk[5][2] = {{c->d, 3 * c->d}, {c->qkv_dim, c->k_attn}, {c->d, c->qdim}, {n_gu, c->d}, {c->d, c->F}};
+    const int epis[5] = {EPI_STORE_F32, qkv_epi, EPI_RESID_F32, EPI_SWIGLU, EPI_RESID_F32};
+    size_t need = 0;
+    for (int g = 0; g < 5; ++g)
+        need = std::max(need, gemm_workspace_bytes(c->w_fmt, epis[g], M, static_cast<int>(nk[g][0]),
+                                                   static_cast<int>(nk[g][1]), c->cb.splitk_bytes));
+    return need;
+}
+
+// Suspends per-kernel timing for one call (event creation is an allocation).
+struct NoTiming {
+    outlets_ctx* c;
+    bool was;
+    explicit NoTiming(outlets_ctx* c_, bool on) : c(c_), was(c_->prof_on) { if (on) c->prof_on = false; }
+    ~NoTiming() { c->prof_on = was; }
+};
+
+// Dynamic prediction (Section 3.2, t >= 1) in the context's buffers or, with
+// noalloc, in the static scratch array.
+int predict_step_impl(outlets_ctx* ctx, bool noalloc, int32_t n_req, const int32_t* slots, const void* h_low,
+                      const void* h_mid, const void* h_high, int64_t row_stride, const int32_t* tokens,
+                      float* z_out, void* hdraft_out, void* stream) {
+    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
+    if (n_req < 0 || n_req > ctx->cfg.max_batch_requests || n_req > ctx->cfg.max_batch_tokens)
+        return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
+    if (noalloc && ctx->cfg.keep_intermediates)
+        return fail(OUTLETS_ERR_UNSUPPORTED, "the no-allocation step does not keep intermediates");
+    if (noalloc && !ctx->scratch) return fail(OUTLETS_ERR_HIP, "static scratch address unknown on this device");
+    if (n_req == 0) return OUTLETS_OK;
+    if (!slots) return fail(OUTLETS_ERR_INVALID_ARG, "null slots");
+    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, tokens, z_out);
+    if (rc) return rc;
+    if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
+        return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
+    const char* why = "";
+    rc = ctx->pager->check_step(n_req, slots, &why);
+    if (rc) return fail(rc, why);
+    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    // the new token's position is each slot's cached length before the append
+    std::vector<int32_t> off(n_req + 1), start(n_req);
+    for (int i = 0; i <= n_req; ++i) off[i] = i;
+    int32_t new_pages = 0;
+    for (int i = 0; i < n_req; ++i) {
+        start[i] = ctx->pager->seq_len(slots[i]);
+        new_pages += (start[i] % 16 == 0);
+    }
+    // split-KV decode work items (request, chunk of pages), requests in order
+    std::vector<int32_t> dwork, cu_chunks;
+    int chunk = ctx->dec_chunk;
+    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
+        std::vector<int32_t> pages(n_req);
+        for (int i = 0; i < n_req; ++i) pages[i] = (start[i] + 1 + 15) / 16;
+        chunk = attn_decode_chunk_for(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus());
+        cu_chunks.assign(n_req + 1, 0);
+        for (int i = 0; i < n_req; ++i) {
+            const int nch = (pages[i] + chunk - 1) / chunk;
+            cu_chunks[i + 1] = cu_chunks[i] + nch;
+            for (int c = 0; c < nch; ++c) { dwork.push_back(i); dwork.push_back(c); }
+        }
+    }
+    CallBufs sb;
+    const CallBufs* bufs = &ctx->cb;
+    if (noalloc) {
+        const int64_t n_chunks = static_cast<int64_t>(dwork.size() / 2);
+        const int64_t meta_count = (n_req + 1) + 2 * static_cast<int64_t>(n_req) + 2 * new_pages +
+                                   static_cast<int64_t>(dwork.size() + cu_chunks.size());
+        const size_t ws = step_splitk_bytes(ctx, n_req);
+        const size_t need = layout_step(ctx, n_req, n_chunks, meta_count, ws, nullptr, &sb);
+        if (need > kScratchBytes)
+            return fail(OUTLETS_ERR_INVALID_ARG, "the step needs " + std::to_string(need) +
+                                                     " bytes of scratch; the static scratch holds " +
+                                                     std::to_string(kScratchBytes));
+        layout_step(ctx, n_req, n_chunks, meta_count, ws, static_cast<char*>(ctx->scratch), &sb);
+        bufs = &sb;
+    }
+    std::vector<int32_t> updates;
+    ctx->prof_phase = 1;
+    rc = ctx->pager->step(n_req, slots, &updates, &why);
+    if (rc) return fail(rc, why);
+    ctx->dec_chunk = chunk;
+    NoTiming nt(ctx, noalloc);
+    rc = upload_meta(ctx, *bufs, n_req, off, slots, start, updates, dwork, cu_chunks, st);
+    if (rc == OUTLETS_OK)
+        rc = run_layer(ctx, *bufs, false, n_req, n_req, h_low, h_mid, h_high, row_stride, tokens, z_out,
+                       hdraft_out, st);
+    if (rc) return rc;   // device work may be partly queued; the slot lengths advanced
+    ctx->last_n = n_req;
+    ctx->last_T = n_req;
+    ctx->last_in_scratch = noalloc;
     return OUTLETS_OK;
 }
 
@@ -542,6 +733,8 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
             return fail(OUTLETS_ERR_INVALID_ARG, "e4m3 weights need every row-scale pointer");
     }
     HIP_TRY(hipSetDevice(device), "hipSetDevice");
+    void* scratch_ptr = nullptr;
+    if ((rc = scratch_address(device, &scratch_ptr)) != OUTLETS_OK) return rc;
 
     std::unique_ptr<outlets_ctx> c;
     try {
@@ -553,6 +746,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     c->cfg = *cfg;
     c->w = w;
     c->device = device;
+    c->scratch = scratch_ptr;
     c->act_fmt = cfg->act_fmt;
     c->w_fmt = cfg->weight_fmt;
     c->small_fmt = (cfg->weight_fmt == OUTLETS_FMT_F32) ? FMT_F32 : FMT_BF16;
@@ -585,23 +779,23 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->cos_t, sizeof(float) * cfg->max_seq_len * (hd / 2));
     ALLOC(c->sin_t, sizeof(float) * cfg->max_seq_len * (hd / 2));
     const bool keep = cfg->keep_intermediates != 0;
-    ALLOC(c->r_f, sizeof(float) * Tm * c->d);
+    ALLOC(c->cb.r_f, sizeof(float) * Tm * c->d);
     if (keep) {
-        ALLOC(c->r_x1, sizeof(float) * Tm * c->d);
-        ALLOC(c->r_x2, sizeof(float) * Tm * c->d);
-        ALLOC(c->r_h, sizeof(float) * Tm * c->d);
+        ALLOC(c->cb.r_x1, sizeof(float) * Tm * c->d);
+        ALLOC(c->cb.r_x2, sizeof(float) * Tm * c->d);
+        ALLOC(c->cb.r_h, sizeof(float) * Tm * c->d);
     } else {
-        c->r_x1 = c->r_x2 = c->r_h = c->r_f;
+        c->cb.r_x1 = c->cb.r_x2 = c->cb.r_h = c->cb.r_f;
     }
-    ALLOC(c->a_norm, ab * Tm * c->d);
-    if (c->embed_in) ALLOC(c->e_norm, ab * Tm * c->d);
-    if (keep) ALLOC(c->b_norm, ab * Tm * c->d);
-    else c->b_norm = c->a_norm;
-    ALLOC(c->qkv, ab * Tm * c->qkv_dim);
-    ALLOC(c->attn, ab * Tm * c->qdim);
-    ALLOC(c->mlp, ab * Tm * c->F);
-    ALLOC(c->pooled, sizeof(float) * Bm * 2 * c->d);
-    ALLOC(c->pooled_bf16, sizeof(uint16_t) * 2 * Bm * 2 * c->d);
+    ALLOC(c->cb.a_norm, ab * Tm * c->d);
+    if (c->embed_in) ALLOC(c->cb.e_norm, ab * Tm * c->d);
+    if (keep) ALLOC(c->cb.b_norm, ab * Tm * c->d);
+    else c->cb.b_norm = c->cb.a_norm;
+    ALLOC(c->cb.qkv, ab * Tm * c->qkv_dim);
+    ALLOC(c->cb.attn, ab * Tm * c->qdim);
+    ALLOC(c->cb.mlp, ab * Tm * c->F);
+    ALLOC(c->cb.pooled, sizeof(float) * Bm * 2 * c->d);
+    ALLOC(c->cb.pooled_bf16, sizeof(uint16_t) * 2 * Bm * 2 * c->d);
     {
         // head partials: the largest splits x rows over every batch size
         int64_t most = 0;
@@ -609,21 +803,21 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
             const int rows = static_cast<int>((c->w_fmt == FMT_F32 ? 1 : 2) * b);
             most = std::max<int64_t>(most, static_cast<int64_t>(head_splits(c.get(), rows)) * rows);
         }
-        ALLOC(c->head_part, sizeof(float) * most * c->H1);
+        ALLOC(c->cb.head_part, sizeof(float) * most * c->H1);
     }
-    ALLOC(c->tok_slot, sizeof(int32_t) * Tm);
-    ALLOC(c->tok_pos, sizeof(int32_t) * Tm);
-    ALLOC(c->last_idx, sizeof(int32_t) * Bm);
+    ALLOC(c->cb.tok_slot, sizeof(int32_t) * Tm);
+    ALLOC(c->cb.tok_pos, sizeof(int32_t) * Tm);
+    ALLOC(c->cb.last_idx, sizeof(int32_t) * Bm);
     // decode work items: chunks of the largest size, or, where the step
     // halves the size because those fill fewer than 2 waves per CU over the
     // KV heads, at most 4x that many (16-page chunks)
     const int64_t max_chunks = std::max<int64_t>(
         Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages()),
         (int64_t)(64 / 16) * (2 * gemm_device_cus() / std::max(1, cfg->n_kv_heads) + 1));
-    c->meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
+    c->cb.meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
     if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
-        ALLOC(c->decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
-    ALLOC(c->pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
+        ALLOC(c->cb.decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
+    ALLOC(c->cb.pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
     {
         // split-K scratch: the largest plan over the layer's GEMMs for M up to 1024
         const int64_t gemm_nk[5][2] = {{c->d, 3 * c->d}, {c->qkv_dim, c->k_attn}, {c->d, c->qdim},
@@ -640,19 +834,19 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
         // large GEMMs split their last round of tiles over K: up to one
         // 256 x 256 fp32 block per CU (256 CUs)
         if (Tm > 256) need = std::max(need, (size_t)256 * 65536 * sizeof(float));
-        c->splitk_bytes = need;
-        if (need) ALLOC(c->splitk_ws, need);
+        c->cb.splitk_bytes = need;
+        if (need) ALLOC(c->cb.splitk_ws, need);
     }
-    ALLOC(c->d_meta, sizeof(int32_t) * c->meta_cap);
+    ALLOC(c->cb.d_meta, sizeof(int32_t) * c->cb.meta_cap);
     if (w.w_lm) ALLOC(c->lm_logits, sizeof(float) * 2 * Bm * cfg->vocab);
     if (c->probe) {
         ALLOC(c->probe_sum, sizeof(float) * cfg->max_slots * c->d);
-        ALLOC(c->probe_meta, sizeof(int32_t) * c->meta_cap);
+        ALLOC(c->probe_meta, sizeof(int32_t) * c->cb.meta_cap);
         c->probe_count.assign(cfg->max_slots, 0);
     }
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
-        HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->meta_cap, 0),
+        HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->cb.meta_cap, 0),
                 "hipHostMalloc");
         HIP_TRY(hipEventCreateWithFlags(&c->ev[i], hipEventDisableTiming), "hipEventCreate");
     }
@@ -728,9 +922,9 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     }
     std::vector<int32_t> cu_tiles(n_req + 1, 0);
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, work, cu_tiles, st);
+    rc = upload_meta(ctx, ctx->cb, n_req, off, slots, start, updates, work, cu_tiles, st);
     if (rc == OUTLETS_OK)
-        rc = run_layer(ctx, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, tokens,
+        rc = run_layer(ctx, ctx->cb, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, tokens,
                        z_out, hdraft_out, st);
     if (rc) {
         std::string msg = g_err;
@@ -739,54 +933,22 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     }
     ctx->last_n = n_req;
     ctx->last_T = static_cast<int32_t>(T);
+    ctx->last_in_scratch = false;
     return OUTLETS_OK;
 }
 
 int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h_low,
                          const void* h_mid, const void* h_high, int64_t row_stride,
                          const int32_t* tokens, float* z_out, void* hdraft_out, void* stream) {
-    if (!ctx) return fail(OUTLETS_ERR_INVALID_ARG, "null context");
-    if (n_req < 0 || n_req > ctx->cfg.max_batch_requests || n_req > ctx->cfg.max_batch_tokens)
-        return fail(OUTLETS_ERR_INVALID_ARG, "n_req outside [0, max_batch_requests]");
-    if (n_req == 0) return OUTLETS_OK;
-    if (!slots) return fail(OUTLETS_ERR_INVALID_ARG, "null slots");
-    int rc = check_states(ctx, h_low, h_mid, h_high, row_stride, tokens, z_out);
-    if (rc) return rc;
-    if (hdraft_out && ctx->act_fmt == FMT_BF16 && !aligned16(hdraft_out))
-        return fail(OUTLETS_ERR_UNSUPPORTED, "hdraft_out must be 16-byte aligned");
-    HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    return predict_step_impl(ctx, false, n_req, slots, h_low, h_mid, h_high, row_stride, tokens, z_out,
+                             hdraft_out, stream);
+}
 
-    std::vector<int32_t> updates;
-    const char* why = "";
-    ctx->prof_phase = 1;
-    rc = ctx->pager->step(n_req, slots, &updates, &why);
-    if (rc) return fail(rc, why);
-    std::vector<int32_t> off(n_req + 1), start(n_req);
-    for (int i = 0; i <= n_req; ++i) off[i] = i;
-    for (int i = 0; i < n_req; ++i) start[i] = ctx->pager->seq_len(slots[i]) - 1;
-    // split-KV decode work items (request, chunk of pages), requests in order
-    std::vector<int32_t> dwork, cu_chunks;
-    if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
-        std::vector<int32_t> pages(n_req);
-        for (int i = 0; i < n_req; ++i) pages[i] = (start[i] + 1 + 15) / 16;
-        const int chunk = attn_decode_chunk_for(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus());
-        ctx->dec_chunk = chunk;
-        cu_chunks.assign(n_req + 1, 0);
-        for (int i = 0; i < n_req; ++i) {
-            const int nch = (pages[i] + chunk - 1) / chunk;
-            cu_chunks[i + 1] = cu_chunks[i] + nch;
-            for (int c = 0; c < nch; ++c) { dwork.push_back(i); dwork.push_back(c); }
-        }
-    }
-    rc = upload_meta(ctx, n_req, off, slots, start, updates, dwork, cu_chunks, st);
-    if (rc == OUTLETS_OK)
-        rc = run_layer(ctx, false, n_req, n_req, h_low, h_mid, h_high, row_stride, tokens, z_out,
-                       hdraft_out, st);
-    if (rc) return rc;   // device work may be partly queued; the slot lengths advanced
-    ctx->last_n = n_req;
-    ctx->last_T = n_req;
-    return OUTLETS_OK;
+int outlets_predict_step_noalloc(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, const void* h_low,
+                                 const void* h_mid, const void* h_high, int64_t row_stride,
+                                 const int32_t* tokens, float* z_out, void* hdraft_out, void* stream) {
+    return predict_step_impl(ctx, true, n_req, slots, h_low, h_mid, h_high, row_stride, tokens, z_out,
+                             hdraft_out, stream);
 }
 
 // ---------------------------------------------------------------- MLP probe
@@ -796,7 +958,7 @@ int outlets_predict_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, 
 
 // Stage int32 metadata through the pinned double buffer into probe_meta.
 int upload_probe_meta(outlets_ctx* c, const std::vector<int32_t>& v, hipStream_t st) {
-    if (static_cast<int64_t>(v.size()) > c->meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
+    if (static_cast<int64_t>(v.size()) > c->cb.meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
     std::memcpy(c->h_stage[s], v.data(), sizeof(int32_t) * v.size());
@@ -813,14 +975,14 @@ int run_probe_head(outlets_ctx* c, int n, float* z_out, hipStream_t st) {
     const int af = c->act_fmt, wf = c->w_fmt;
     const int hf = (wf == FMT_F32) ? FMT_F32 : FMT_BF16;
     const int64_t d = c->d;
-    const GemmA a = (wf == FMT_F32) ? gemm_a(c->pooled, 2 * d, 2 * d) : gemm_a(c->pooled_bf16, 2 * d, 2 * d);
+    const GemmA a = (wf == FMT_F32) ? gemm_a(c->cb.pooled, 2 * d, 2 * d) : gemm_a(c->cb.pooled_bf16, 2 * d, 2 * d);
     const GemmB b = gemm_b1(c->w.probe_w1, nullptr, c->H1, 2 * d);
     const int rows = (wf == FMT_F32) ? n : 2 * n;
-    GemmC hc = gemm_c(c->head_part, c->H1);
+    GemmC hc = gemm_c(c->cb.head_part, c->H1);
     hc.split_stride = static_cast<int64_t>(rows) * c->H1;
     const int hs = head_splits(c, rows);
     gemm_launch(af, hf, EPI_PARTIAL, rows, c->H1, 2 * d, a, b, hc, hs, st);
-    launch_head_finish(c->small_fmt, n, c->H1, hs, c->head_part, c->w.probe_b1, c->w.probe_w2,
+    launch_head_finish(c->small_fmt, n, c->H1, hs, c->cb.head_part, c->w.probe_b1, c->w.probe_w2,
                        c->w.probe_b2, z_out, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -873,8 +1035,8 @@ int outlets_probe_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slots,
     if ((rc = upload_probe_meta(ctx, v, st)) != OUTLETS_OK) return rc;
     const int32_t* d_off = ctx->probe_meta;
     launch_pool_prefill(n_req, cu[n_req], static_cast<int>(ctx->d), ctx->act_fmt, h, row_stride, d_off,
-                        d_off + n_req + 1, d_off + 2 * n_req + 1, ctx->pool_part, ctx->probe_sum, ctx->pooled,
-                        ctx->w_fmt == FMT_F32 ? nullptr : ctx->pooled_bf16, st);
+                        d_off + n_req + 1, d_off + 2 * n_req + 1, ctx->cb.pool_part, ctx->probe_sum, ctx->cb.pooled,
+                        ctx->w_fmt == FMT_F32 ? nullptr : ctx->cb.pooled_bf16, st);
     if ((rc = run_probe_head(ctx, n_req, z_out, st)) != OUTLETS_OK) return rc;
     for (int i = 0; i < n_req; ++i) ctx->probe_count[slots[i]] = lens[i];
     return OUTLETS_OK;
@@ -896,8 +1058,8 @@ int outlets_probe_step(outlets_ctx* ctx, int32_t n_req, const int32_t* slots, co
     }
     if ((rc = upload_probe_meta(ctx, v, st)) != OUTLETS_OK) return rc;
     launch_pool_step(n_req, static_cast<int>(ctx->d), ctx->act_fmt, h, row_stride, ctx->probe_meta,
-                     ctx->probe_meta + n_req, ctx->probe_sum, ctx->pooled,
-                     ctx->w_fmt == FMT_F32 ? nullptr : ctx->pooled_bf16, st);
+                     ctx->probe_meta + n_req, ctx->probe_sum, ctx->cb.pooled,
+                     ctx->w_fmt == FMT_F32 ? nullptr : ctx->cb.pooled_bf16, st);
     if ((rc = run_probe_head(ctx, n_req, z_out, st)) != OUTLETS_OK) return rc;
     for (int i = 0; i < n_req; ++i) ctx->probe_count[slots[i]] += 1;
     return OUTLETS_OK;
@@ -924,6 +1086,8 @@ int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, vo
     if (n_req <= 0 || n_req != ctx->last_n)
         return fail(OUTLETS_ERR_INVALID_ARG, "n_req must equal the last predict call's request count");
     if (!p_out) return fail(OUTLETS_ERR_INVALID_ARG, "null p_out");
+    if (ctx->last_in_scratch)
+        return fail(OUTLETS_ERR_INVALID_ARG, "the last predict call ran in the static scratch (no-allocation step)");
     HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int V = ctx->cfg.vocab;
@@ -931,7 +1095,7 @@ int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, vo
     const int rows = split ? 2 * n_req : n_req;
     gemm_launch(ctx->act_fmt, ctx->w_fmt, EPI_STORE_F32, rows, V, static_cast<int>(ctx->d), lm_input(ctx),
                 gemm_b1(ctx->w.w_lm, ctx->w.s_lm, V, ctx->d), gemm_c(ctx->lm_logits, V), 1, st,
-                ctx->splitk_ws, ctx->splitk_bytes);
+                ctx->cb.splitk_ws, ctx->cb.splitk_bytes);
     launch_lm_softmax(n_req, V, ctx->lm_logits, split, p_out, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -955,14 +1119,16 @@ int outlets_get_meta(outlets_ctx* ctx, int32_t what, int32_t* out, int64_t cap, 
         case OUTLETS_META_PAGE_TABLE: count = static_cast<int64_t>(ctx->pager->table().size()); break;
         case OUTLETS_META_SEQ_LEN: count = ctx->pager->max_slots(); break;
         case OUTLETS_META_DEV_PAGE_TABLE: count = static_cast<int64_t>(ctx->pager->table().size()); dev = ctx->page_table; break;
-        case OUTLETS_META_DEV_CU_SEQLENS: count = n + 1; dev = ctx->d_meta; break;
-        case OUTLETS_META_DEV_POSITIONS: count = T; dev = ctx->tok_pos; break;
-        case OUTLETS_META_DEV_LAST_IDX: count = n; dev = ctx->last_idx; break;
-        case OUTLETS_META_DEV_TOKEN_SLOT: count = T; dev = ctx->tok_slot; break;
+        case OUTLETS_META_DEV_CU_SEQLENS: count = n + 1; dev = ctx->cb.d_meta; break;
+        case OUTLETS_META_DEV_POSITIONS: count = T; dev = ctx->cb.tok_pos; break;
+        case OUTLETS_META_DEV_LAST_IDX: count = n; dev = ctx->cb.last_idx; break;
+        case OUTLETS_META_DEV_TOKEN_SLOT: count = T; dev = ctx->cb.tok_slot; break;
         default: return fail(OUTLETS_ERR_INVALID_ARG, "unknown metadata id");
     }
     *n_out = count;
     if (cap < count) return fail(OUTLETS_ERR_INVALID_ARG, "output capacity too small");
+    if (ctx->last_in_scratch && what >= OUTLETS_META_DEV_CU_SEQLENS)
+        return fail(OUTLETS_ERR_INVALID_ARG, "the last predict call ran in the static scratch (no-allocation step)");
     if (!dev) {
         const auto& v = (what == OUTLETS_META_PAGE_TABLE) ? ctx->pager->table() : ctx->pager->seq_lens();
         std::memcpy(out, v.data(), sizeof(int32_t) * count);
@@ -984,19 +1150,19 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
     int64_t size = 0;
     bool needs_keep = true;
     switch (which) {
-        case OUTLETS_BUF_FUSED: src = ctx->r_f; size = 4 * T * d; break;
-        case OUTLETS_BUF_NORM_ATTN: src = ctx->a_norm; size = ab * T * d; break;
+        case OUTLETS_BUF_FUSED: src = ctx->cb.r_f; size = 4 * T * d; break;
+        case OUTLETS_BUF_NORM_ATTN: src = ctx->cb.a_norm; size = ab * T * d; break;
         case OUTLETS_BUF_Q: src = nullptr; size = ab * T * ctx->qdim; break;
-        case OUTLETS_BUF_ATTN: src = ctx->attn; size = ab * T * ctx->qdim; needs_keep = false; break;
-        case OUTLETS_BUF_X1: src = ctx->r_x1; size = 4 * T * d; break;
-        case OUTLETS_BUF_NORM_MLP: src = ctx->b_norm; size = ab * T * d; break;
-        case OUTLETS_BUF_MLP_ACT: src = ctx->mlp; size = ab * T * ctx->F; break;
-        case OUTLETS_BUF_X2: src = ctx->r_x2; size = 4 * T * d; break;
-        case OUTLETS_BUF_HDRAFT: src = ctx->r_h; size = 4 * T * d; needs_keep = true; break;
-        case OUTLETS_BUF_POOLED: src = ctx->pooled; size = 4 * n * 2 * d; needs_keep = false; break;
+        case OUTLETS_BUF_ATTN: src = ctx->cb.attn; size = ab * T * ctx->qdim; needs_keep = false; break;
+        case OUTLETS_BUF_X1: src = ctx->cb.r_x1; size = 4 * T * d; break;
+        case OUTLETS_BUF_NORM_MLP: src = ctx->cb.b_norm; size = ab * T * d; break;
+        case OUTLETS_BUF_MLP_ACT: src = ctx->cb.mlp; size = ab * T * ctx->F; break;
+        case OUTLETS_BUF_X2: src = ctx->cb.r_x2; size = 4 * T * d; break;
+        case OUTLETS_BUF_HDRAFT: src = ctx->cb.r_h; size = 4 * T * d; needs_keep = true; break;
+        case OUTLETS_BUF_POOLED: src = ctx->cb.pooled; size = 4 * n * 2 * d; needs_keep = false; break;
         case OUTLETS_BUF_NORM_EMB:
             if (!ctx->embed_in) return fail(OUTLETS_ERR_INVALID_ARG, "the context has no input embeddings");
-            src = ctx->e_norm; size = ab * T * d; break;
+            src = ctx->cb.e_norm; size = ab * T * d; break;
         case OUTLETS_BUF_K_POOL:
         case OUTLETS_BUF_V_POOL:
             src = which == OUTLETS_BUF_K_POOL ? ctx->kpool : ctx->vpool;
@@ -1007,12 +1173,14 @@ int outlets_get_buffer(outlets_ctx* ctx, int32_t which, void* dst, int64_t nbyte
     }
     *n_bytes = size;
     if (needs_keep && !keep) return fail(OUTLETS_ERR_INVALID_ARG, "buffer needs keep_intermediates");
+    if (ctx->last_in_scratch && which != OUTLETS_BUF_K_POOL && which != OUTLETS_BUF_V_POOL)
+        return fail(OUTLETS_ERR_INVALID_ARG, "the last predict call ran in the static scratch (no-allocation step)");
     if (!dst || nbytes < size) return fail(OUTLETS_ERR_INVALID_ARG, "destination too small");
     HIP_TRY(hipSetDevice(ctx->device), "hipSetDevice");
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (which == OUTLETS_BUF_Q) {
         // queries live in the first n_q*hd columns of the fused qkv rows
-        HIP_TRY(hipMemcpy2DAsync(dst, ab * ctx->qdim, ctx->qkv, ab * ctx->qkv_dim, ab * ctx->qdim, T,
+        HIP_TRY(hipMemcpy2DAsync(dst, ab * ctx->qdim, ctx->cb.qkv, ab * ctx->qkv_dim, ab * ctx->qdim, T,
                                  hipMemcpyDeviceToDevice, st), "hipMemcpy2DAsync");
     } else if (size) {
         HIP_TRY(hipMemcpyAsync(dst, src, size, hipMemcpyDeviceToDevice, st), "hipMemcpyAsync");

@@ -779,23 +779,55 @@ int device_cus() {
     return cache[dev];
 }
 
-template <int EPI, bool E4M3>
-void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& b,
-                 const GemmC& c, int splits, hipStream_t st, float* ws, size_t ws_bytes) {
-    (void)act_fmt;
-    const int bm = gemm_bm(M, N, EPI);
-    const int mt = (M + bm - 1) / bm, nt = N / 256, T = mt * nt;
+// How gemm_launch uses its fp32 workspace for one call, given ws_bytes of
+// it: a small-M K split (sk > 1, sk partial [M, N] blocks), or a K split of
+// the last round of 256-row tiles (tail_s > 1 splits of `tail` tiles, one
+// 256 x 256 block each), or neither.  `bytes` is the workspace the plan uses.
+struct SplitPlan {
+    int sk, tail_s, tail;
+    size_t bytes;
+};
+
+SplitPlan split_plan(int w_fmt, int epi, int M, int N, int K, int splits, size_t ws_bytes) {
+    SplitPlan p{1, 1, 0, 0};
+    if (splits == 1) {
+        const int sk = gemm_splitk_plan(w_fmt, epi == EPI_QKV_ROPE ? EPI_STORE_ACT : epi, M, N, K);
+        const size_t need = (size_t)sk * M * N * sizeof(float);
+        if (sk > 1 && need <= ws_bytes) {
+            p.sk = sk;
+            p.bytes = need;
+            return p;
+        }
+    }
+    if (w_fmt == FMT_F32) return p;
     // With one workgroup per CU, T tiles take ceil(T / W) rounds; when the
     // last round holds only a few tiles, those tiles run instead as S K-splits
     // (S * tail <= W workgroups of 1/S the work) and are summed by
     // tile_reduce, so the last round costs about 1/S of a round.
+    const int bm = gemm_bm(M, N, epi);
+    const int T = ((M + bm - 1) / bm) * (N / 256);
     const int W = device_cus();
     const int full = T / W, tail = T % W;
-    int S = 1;
-    if (splits == 1 && bm == 256 && EPI != EPI_PARTIAL && EPI != EPI_QKV_ROPE && full >= 1 && full <= 64 && tail > 0 && ws) {
-        S = std::min({16, W / tail, (K / BK) / 4});
-        if ((size_t)S * tail * 65536 * sizeof(float) > ws_bytes) S = 1;
+    if (splits == 1 && bm == 256 && epi != EPI_PARTIAL && epi != EPI_QKV_ROPE && full >= 1 && full <= 64 &&
+        tail > 0 && ws_bytes > 0) {
+        const int S = std::min({16, W / tail, (K / BK) / 4});
+        const size_t need = (size_t)S * tail * 65536 * sizeof(float);
+        if (S >= 2 && need <= ws_bytes) {
+            p.tail_s = S;
+            p.tail = tail;
+            p.bytes = need;
+        }
     }
+    return p;
+}
+
+template <int EPI, bool E4M3>
+void launch_mfma(int act_fmt, int M, int N, int K, const GemmA& a, const GemmB& b,
+                 const GemmC& c, int splits, hipStream_t st, float* ws, const SplitPlan& pl) {
+    (void)act_fmt;
+    const int bm = gemm_bm(M, N, EPI);
+    const int mt = (M + bm - 1) / bm, nt = N / 256, T = mt * nt;
+    const int S = pl.tail_s, tail = pl.tail;
     if (S < 2) {
         launch_tiles<EPI, E4M3>(M, N, K, a, b, c, splits, 0, T, st);
         return;
@@ -872,13 +904,18 @@ int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA
     return OUTLETS_OK;
 }
 
+size_t gemm_workspace_bytes(int w_fmt, int epi, int M, int N, int K, size_t ws_bytes) {
+    return split_plan(w_fmt, epi, M, N, K, 1, ws_bytes).bytes;
+}
+
 void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st, float* ws,
                  size_t ws_bytes) {
+    const SplitPlan pl = split_plan(w_fmt, epi, M, N, K, splits, ws ? ws_bytes : 0);
     // Small M: split K over more workgroups into fp32 partials, then reduce in
     // a fixed order and apply the epilogue (deterministic).
-    const int sk = splits == 1 ? gemm_splitk_plan(w_fmt, epi == EPI_QKV_ROPE ? EPI_STORE_ACT : epi, M, N, K) : 1;
-    if (sk > 1 && ws && (size_t)sk * M * N * sizeof(float) <= ws_bytes) {
+    const int sk = pl.sk;
+    if (sk > 1) {
         GemmC pc{};
         pc.c = ws;
         pc.ldc = N;
@@ -911,8 +948,8 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
     const bool e4 = (w_fmt == FMT_E4M3);
 #define OUTLETS_GEMM_CASE(E)                                                        \
     case E:                                                                         \
-        if (e4) launch_mfma<E, true>(act_fmt, M, N, K, a, b, c, splits, st, ws, ws_bytes); \
-        else launch_mfma<E, false>(act_fmt, M, N, K, a, b, c, splits, st, ws, ws_bytes);  \
+        if (e4) launch_mfma<E, true>(act_fmt, M, N, K, a, b, c, splits, st, ws, pl);      \
+        else launch_mfma<E, false>(act_fmt, M, N, K, a, b, c, splits, st, ws, pl);       \
         break;
     switch (epi) {
         OUTLETS_GEMM_CASE(EPI_STORE_F32)

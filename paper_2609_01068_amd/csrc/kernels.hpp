@@ -78,6 +78,10 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st,
                  float* ws = nullptr, size_t ws_bytes = 0);
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
+// Bytes of fp32 workspace gemm_launch uses for this call when given ws_bytes
+// (0 when it splits nothing); a call given exactly these bytes takes the
+// same plan as with ws_bytes.
+size_t gemm_workspace_bytes(int w_fmt, int epi, int M, int N, int K, size_t ws_bytes);
 int gemm_device_cus();   // compute units of the current device
 // Whether gemm_launch takes EPI_QKV_ROPE for this layout (bf16 activations,
 // head dim 128; N = q|k|v[|gate] columns); otherwise store with

@@ -71,7 +71,7 @@ int Pager::prefill(int32_t n, const int32_t* slots, const int32_t* lens,
     return OUTLETS_OK;
 }
 
-int Pager::step(int32_t n, const int32_t* slots, std::vector<int32_t>* updates, const char** why) {
+int Pager::check_step(int32_t n, const int32_t* slots, const char** why) {
     int rc = check_slots(n, slots, why);
     if (rc != OUTLETS_OK) return rc;
     for (int32_t i = 0; i < n; ++i)
@@ -81,6 +81,12 @@ int Pager::step(int32_t n, const int32_t* slots, std::vector<int32_t>* updates, 
     int32_t need = 0;
     for (int32_t i = 0; i < n; ++i) need += (seq_len_[slots[i]] % page_size_ == 0);
     if (need > n_free()) { *why = "KV page pool exhausted"; return OUTLETS_ERR_OUT_OF_PAGES; }
+    return OUTLETS_OK;
+}
+
+int Pager::step(int32_t n, const int32_t* slots, std::vector<int32_t>* updates, const char** why) {
+    int rc = check_step(n, slots, why);
+    if (rc != OUTLETS_OK) return rc;
     for (int32_t i = 0; i < n; ++i) {
         int32_t s = slots[i];
         if (seq_len_[s] % page_size_ == 0) {

@@ -26,6 +26,8 @@ public:
                 std::vector<int32_t>* updates, const char** why);
     int step(int32_t n, const int32_t* slots, std::vector<int32_t>* updates,
              const char** why);
+    // The checks of step() alone (same order and codes); changes nothing.
+    int check_step(int32_t n, const int32_t* slots, const char** why);
     int release(int32_t n, const int32_t* slots, const char** why);
 
     int32_t max_pages_per_seq() const { return max_pages_; }

@@ -147,17 +147,20 @@ class OutletsPredictor:
     def step(self, slots: Sequence[int], h_low: torch.Tensor, h_mid: torch.Tensor,
              h_high: torch.Tensor, row_stride: Optional[int] = None, want_hdraft: bool = False,
              z_out: Optional[torch.Tensor] = None, hdraft_out: Optional[torch.Tensor] = None,
-             stream=None, tokens: Optional[torch.Tensor] = None):
+             stream=None, tokens: Optional[torch.Tensor] = None, noalloc: bool = False):
+        """``noalloc``: run outlets_predict_step_noalloc (per-call buffers in
+        the library's static scratch; pass z_out / hdraft_out to keep the
+        call itself free of allocations)."""
         n = len(slots)
         if z_out is None:
             z_out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
         if want_hdraft and hdraft_out is None:
             hdraft_out = torch.empty((max(n, 1), self.shape.d), dtype=self.act_dtype, device=self.device)
         stride = h_low.stride(0) if row_stride is None else row_stride
-        rc = B.outlets_predict_step(self.ctx, list(slots), h_low.data_ptr(), h_mid.data_ptr(),
-                                    h_high.data_ptr(), stride, _tokens_ptr(tokens), z_out.data_ptr(),
-                                    _ptr(hdraft_out), _stream_ptr(stream))
-        B.check(rc, "outlets_predict_step")
+        fn = B.outlets_predict_step_noalloc if noalloc else B.outlets_predict_step
+        rc = fn(self.ctx, list(slots), h_low.data_ptr(), h_mid.data_ptr(), h_high.data_ptr(), stride,
+                _tokens_ptr(tokens), z_out.data_ptr(), _ptr(hdraft_out), _stream_ptr(stream))
+        B.check(rc, "outlets_predict_step_noalloc" if noalloc else "outlets_predict_step")
         return z_out[:n], (hdraft_out[:n] if hdraft_out is not None else None)
 
     def release(self, slots: Sequence[int]) -> None:
