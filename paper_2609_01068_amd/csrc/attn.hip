@@ -430,6 +430,8 @@ constexpr int kDecodeChunk = OUTLETS_DECODE_CHUNK;
 constexpr int kDecodeRec = 128 + 4;   // floats per partial record: m, l, 2 pad, o[128]
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int G>
 __global__ void __launch_bounds__(64)
@@ -471,14 +473,19 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
     constexpr int PPI = OUTLETS_DECODE_PPI;
     uint4 kc[PPI][HD / 32], kn[PPI][HD / 32];
     uint2 vc[PPI][HD / 16], vn[PPI][HD / 16];
+    // K/V pages are read once per step: non-temporal loads (measured on this
+    // access pattern, loads alone: 6.6 TB/s against 5.9 TB/s with ordinary
+    // loads, which a plain sequential read of the pools does not beat)
     auto load_page = [&](int pi, uint4* kf, uint2* vf) {
         const int64_t page = __shfl(my_page, min(pi, p1 - 1) - p0, 64);
         const bf16_t* kb = kpool + (page * n_kv + g) * 16 * HD + col * HD + 8 * grp;
         const bf16_t* vb = vpool + (page * n_kv + g) * HD * 16 + col * 16 + 4 * grp;
 #pragma unroll
-        for (int b = 0; b < HD / 32; ++b) kf[b] = *reinterpret_cast<const uint4*>(kb + 32 * b);
+        for (int b = 0; b < HD / 32; ++b)
+            kf[b] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kb + 32 * b)));
 #pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb) vf[cb] = *reinterpret_cast<const uint2*>(vb + 16 * 16 * cb);
+        for (int cb = 0; cb < HD / 16; ++cb)
+            vf[cb] = __builtin_bit_cast(uint2, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(vb + 16 * 16 * cb)));
     };
     auto one_page = [&](int pi, const uint4* kf, const uint2* vf) {
         f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
