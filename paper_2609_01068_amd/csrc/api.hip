@@ -124,6 +124,8 @@ struct outlets_ctx {
     int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
     int32_t dec_chunk = 64;        // pages per decode attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
+    int64_t lanes_off = 0;       // offset of the decode waves' work lists in d_meta
+    int32_t n_lanes = 0;         // decode work lists of the current call
     int32_t n_tiles = 0;
 
     int32_t* h_stage[2] = {nullptr, nullptr};
@@ -426,7 +428,8 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
-          launch_attn_decode(n, c->n_work, c->dec_chunk, b.d_meta + c->work_off, b.d_meta + c->tiles_off, b.qkv,
+          launch_attn_decode(n, c->n_work, c->dec_chunk, b.d_meta + c->work_off, b.d_meta + c->tiles_off,
+                             c->n_lanes, b.d_meta + c->lanes_off, b.qkv,
                              c->qkv_dim, b.attn, c->qdim, req_slot, req_start, c->page_table,
                              c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
                              b.decode_part, gate, st);
@@ -490,9 +493,10 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
 int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int32_t>& off, const int32_t* slots,
                 const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
                 const std::vector<int32_t>& work, const std::vector<int32_t>& cu_tiles,
-                hipStream_t st) {
+                const std::vector<int32_t>& lanes, hipStream_t st) {
     const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size()) +
-                          static_cast<int64_t>(work.size()) + static_cast<int64_t>(cu_tiles.size());
+                          static_cast<int64_t>(work.size()) + static_cast<int64_t>(cu_tiles.size()) +
+                          static_cast<int64_t>(lanes.size());
     if (count > b.meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
@@ -507,6 +511,8 @@ int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int3
     c->tiles_off = c->work_off + static_cast<int64_t>(work.size());
     c->n_tiles = cu_tiles.empty() ? 0 : cu_tiles.back();
     if (!cu_tiles.empty()) std::memcpy(h + c->tiles_off, cu_tiles.data(), sizeof(int32_t) * cu_tiles.size());
+    c->lanes_off = c->tiles_off + static_cast<int64_t>(cu_tiles.size());
+    if (!lanes.empty()) std::memcpy(h + c->lanes_off, lanes.data(), sizeof(int32_t) * lanes.size());
     HIP_TRY(hipMemcpyAsync(b.d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
@@ -650,25 +656,31 @@ int predict_step_impl(outlets_ctx* ctx, bool noalloc, int32_t n_req, const int32
         new_pages += (start[i] % 16 == 0);
     }
     // split-KV decode work items (request, chunk of pages), requests in order
-    std::vector<int32_t> dwork, cu_chunks;
-    int chunk = ctx->dec_chunk;
+    std::vector<int32_t> dwork, cu_chunks, lanes;
+    int chunk = ctx->dec_chunk, n_lanes = 0;
     if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
-        std::vector<int32_t> pages(n_req);
+        std::vector<int32_t> pages(n_req), item_pages;
         for (int i = 0; i < n_req; ++i) pages[i] = (start[i] + 1 + 15) / 16;
         chunk = attn_decode_chunk_for(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus());
         cu_chunks.assign(n_req + 1, 0);
         for (int i = 0; i < n_req; ++i) {
             const int nch = (pages[i] + chunk - 1) / chunk;
             cu_chunks[i + 1] = cu_chunks[i] + nch;
-            for (int c = 0; c < nch; ++c) { dwork.push_back(i); dwork.push_back(c); }
+            for (int c = 0; c < nch; ++c) {
+                dwork.push_back(i);
+                dwork.push_back(c);
+                item_pages.push_back(std::min(chunk, pages[i] - c * chunk));
+            }
         }
+        n_lanes = attn_decode_lanes(static_cast<int>(item_pages.size()), item_pages.data(), ctx->cfg.n_kv_heads,
+                                    gemm_device_cus(), &lanes);
     }
     CallBufs sb;
     const CallBufs* bufs = &ctx->cb;
     if (noalloc) {
         const int64_t n_chunks = static_cast<int64_t>(dwork.size() / 2);
         const int64_t meta_count = (n_req + 1) + 2 * static_cast<int64_t>(n_req) + 2 * new_pages +
-                                   static_cast<int64_t>(dwork.size() + cu_chunks.size());
+                                   static_cast<int64_t>(dwork.size() + cu_chunks.size() + lanes.size());
         const size_t ws = step_splitk_bytes(ctx, n_req);
         const size_t need = layout_step(ctx, n_req, n_chunks, meta_count, ws, nullptr, &sb);
         if (need > kScratchBytes)
@@ -683,8 +695,9 @@ int predict_step_impl(outlets_ctx* ctx, bool noalloc, int32_t n_req, const int32
     rc = ctx->pager->step(n_req, slots, &updates, &why);
     if (rc) return fail(rc, why);
     ctx->dec_chunk = chunk;
+    ctx->n_lanes = n_lanes;
     NoTiming nt(ctx, noalloc);
-    rc = upload_meta(ctx, *bufs, n_req, off, slots, start, updates, dwork, cu_chunks, st);
+    rc = upload_meta(ctx, *bufs, n_req, off, slots, start, updates, dwork, cu_chunks, lanes, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, *bufs, false, n_req, n_req, h_low, h_mid, h_high, row_stride, tokens, z_out,
                        hdraft_out, st);
@@ -814,7 +827,10 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     const int64_t max_chunks = std::max<int64_t>(
         Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages()),
         (int64_t)(64 / 16) * (2 * gemm_device_cus() / std::max(1, cfg->n_kv_heads) + 1));
-    c->cb.meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1);
+    // req_off | req_slot | req_start | page updates | work list | cu tiles or
+    // chunks | decode work lists (at most one list per item, plus offsets)
+    c->cb.meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1) +
+                     (2 * max_chunks + 1);
     if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
         ALLOC(c->cb.decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
     ALLOC(c->cb.pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
@@ -922,7 +938,7 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     }
     std::vector<int32_t> cu_tiles(n_req + 1, 0);
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
-    rc = upload_meta(ctx, ctx->cb, n_req, off, slots, start, updates, work, cu_tiles, st);
+    rc = upload_meta(ctx, ctx->cb, n_req, off, slots, start, updates, work, cu_tiles, {}, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, ctx->cb, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, tokens,
                        z_out, hdraft_out, st);

@@ -16,6 +16,10 @@
 // Prefill (bf16, hd 128): a flash-attention kernel on MFMA, see below.
 #include <type_traits>
 
+#include <algorithm>
+#include <queue>
+#include <vector>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "outlets.h"
@@ -185,8 +189,12 @@ constexpr int prefill_blocks(int G) { return (G == 2 || G == 4) ? OUTLETS_PREFIL
 // keys], each a plain copy of its page block.
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
+// Two workgroups per CU for one 32-query block per wave and at least four
+// waves (the benchmark shapes, G = 4 and 8); the one- and two-wave groups of
+// G = 1 and 2 (reduced test shapes) need more than half a SIMD's registers,
+// so they ask for one.
 template <int G, int QB, int WB>
-__global__ void __launch_bounds__(G * WB * 64, QB == 1 ? 2 : 1)
+__global__ void __launch_bounds__(G * WB * 64, (QB == 1 && G >= 4) ? 2 : 1)
 attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, const int32_t* work,
                   const int32_t* req_off, const int32_t* req_slot, const int32_t* page_table,
                   int max_pages, const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale,
@@ -435,130 +443,151 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int G>
 __global__ void __launch_bounds__(64)
-attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_t* req_slot,
-                 const int32_t* req_start, const int32_t* page_table, int max_pages,
+attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_t* lanes,
+                 const int32_t* req_slot, const int32_t* req_start, const int32_t* page_table, int max_pages,
                  const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale, float* part, int chunk) {
     constexpr int HD = 128;
     static_assert(G <= 16, "query heads per KV head");
-    const int wi = blockIdx.x, g = blockIdx.y;
-    const int r = work[2 * wi], c = work[2 * wi + 1];
-    const int slot = req_slot[r];
-    const int nkeys = req_start[r] + 1;            // cached keys plus the new token's
-    const int npages = (nkeys + 15) / 16;
-    const int p0 = c * chunk, p1 = min(npages, p0 + chunk);   // chunk <= kDecodeChunk
+    const int g = blockIdx.y;
     const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
+    // this wave's work items: lanes[x] .. lanes[x + 1] of the item list that
+    // follows the gridDim.x + 1 offsets
+    const int32_t* items = lanes + gridDim.x + 1;
+    const int j1 = lanes[blockIdx.x + 1];
+    for (int j = lanes[blockIdx.x]; j < j1; ++j) {
+        const int wi = items[j];
+        const int r = work[2 * wi], c = work[2 * wi + 1];
+        const int slot = req_slot[r];
+        const int nkeys = req_start[r] + 1;            // cached keys plus the new token's
+        const int npages = (nkeys + 15) / 16;
+        const int p0 = c * chunk, p1 = min(npages, p0 + chunk);   // chunk <= kDecodeChunk
 
-    bf16x8 qb[HD / 32];
-    {
-        const bf16_t* qrow = q + (int64_t)r * ldq + (int64_t)(g * G + min(col, G - 1)) * HD + 8 * grp;
+        bf16x8 qb[HD / 32];
+        {
+            const bf16_t* qrow = q + (int64_t)r * ldq + (int64_t)(g * G + min(col, G - 1)) * HD + 8 * grp;
 #pragma unroll
-        for (int b = 0; b < HD / 32; ++b) {
-            uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * b);
-            if (col >= G) v = make_uint4(0u, 0u, 0u, 0u);
-            qb[b] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
-    float m = -INFINITY, l = 0.f;
-    f32x4 o[HD / 16];
-#pragma unroll
-    for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // the chunk's page ids, one per lane, fetched up front so the K/V loads of
-    // a page never wait on its page-table entry
-    const int32_t* prow = page_table + (int64_t)slot * max_pages;
-    static_assert(kDecodeChunk <= 64, "one page id per lane");
-    const int my_page = (p0 + lane < p1) ? prow[p0 + lane] : 0;
-    // PPI pages per iteration: their K/V fragments for the next iteration are
-    // loaded before this iteration's pages are used (2 * PPI pages in flight)
-    constexpr int PPI = OUTLETS_DECODE_PPI;
-    uint4 kc[PPI][HD / 32], kn[PPI][HD / 32];
-    uint2 vc[PPI][HD / 16], vn[PPI][HD / 16];
-    // K/V pages are read once per step: non-temporal loads (measured on this
-    // access pattern, loads alone: 6.6 TB/s against 5.9 TB/s with ordinary
-    // loads, which a plain sequential read of the pools does not beat)
-    auto load_page = [&](int pi, uint4* kf, uint2* vf) {
-        const int64_t page = __shfl(my_page, min(pi, p1 - 1) - p0, 64);
-        const bf16_t* kb = kpool + (page * n_kv + g) * 16 * HD + col * HD + 8 * grp;
-        const bf16_t* vb = vpool + (page * n_kv + g) * HD * 16 + col * 16 + 4 * grp;
-#pragma unroll
-        for (int b = 0; b < HD / 32; ++b)
-            kf[b] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kb + 32 * b)));
-#pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb)
-            vf[cb] = __builtin_bit_cast(uint2, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(vb + 16 * 16 * cb)));
-    };
-    auto one_page = [&](int pi, const uint4* kf, const uint2* vf) {
-        f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int b = 0; b < HD / 32; ++b)
-            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[b]), qb[b], sc, 0, 0, 0);
-        // lane: head col, keys 4 grp + i of this page
-        const int k0 = pi * 16 + 4 * grp;
-        float v[4];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            v[i] = (k0 + i < nkeys) ? sc[i] * qscale : -INFINITY;
-            mx = fmaxf(mx, v[i]);
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mn = fmaxf(m, mx);                 // finite: key 16 pi < nkeys
-        const float corr = fast_exp2(m - mn);
-        float ps = 0.f;
-        s16x4 pb;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float pv = fast_exp2(v[i] - mn);
-            ps += pv;
-            pb[i] = static_cast<short>(f32_to_bf16(pv));
-        }
-        ps += __shfl_xor(ps, 16, 64);
-        ps += __shfl_xor(ps, 32, 64);
-        l = l * corr + ps;
-        m = mn;
-        // value rows of keys past the end may hold stale data: zero them
-        const bool tail = (pi * 16 + 16 > nkeys);
-#pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb) {
-            uint2 vv = vf[cb];
-            if (tail) {
-                if (k0 + 0 >= nkeys) vv.x &= 0xFFFF0000u;
-                if (k0 + 1 >= nkeys) vv.x &= 0x0000FFFFu;
-                if (k0 + 2 >= nkeys) vv.y &= 0xFFFF0000u;
-                if (k0 + 3 >= nkeys) vv.y &= 0x0000FFFFu;
-            }
-            o[cb] = o[cb] * corr;
-            o[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, vv), pb, o[cb], 0, 0, 0);
-        }
-    };
-#pragma unroll
-    for (int u = 0; u < PPI; ++u) load_page(p0 + u, kc[u], vc[u]);
-    for (int pi = p0; pi < p1; pi += PPI) {
-        if (pi + PPI < p1) {
-#pragma unroll
-            for (int u = 0; u < PPI; ++u) load_page(pi + PPI + u, kn[u], vn[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < PPI; ++u)
-            if (pi + u < p1) one_page(pi + u, kc[u], vc[u]);
-        if (pi + PPI < p1) {
-#pragma unroll
-            for (int u = 0; u < PPI; ++u) {
-#pragma unroll
-                for (int b = 0; b < HD / 32; ++b) kc[u][b] = kn[u][b];
-#pragma unroll
-                for (int cb = 0; cb < HD / 16; ++cb) vc[u][cb] = vn[u][cb];
+            for (int b = 0; b < HD / 32; ++b) {
+                uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * b);
+                if (col >= G) v = make_uint4(0u, 0u, 0u, 0u);
+                qb[b] = __builtin_bit_cast(bf16x8, v);
             }
         }
-    }
-    // partial record [m, l, -, -, o[0..HD)] per (work item, query head
-    // g G + col); o starts 16-byte aligned
-    if (col < G) {
-        float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * kDecodeRec;
-        if (grp == 0) { rec[0] = m; rec[1] = l; }
+        float m = -INFINITY, l = 0.f;
+        f32x4 o[HD / 16];
 #pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb) *reinterpret_cast<f32x4*>(rec + 4 + 16 * cb + 4 * grp) = o[cb];
+        for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        // the chunk's page ids, one per lane, fetched up front so the K/V loads of
+        // a page never wait on its page-table entry
+        const int32_t* prow = page_table + (int64_t)slot * max_pages;
+        static_assert(kDecodeChunk <= 64, "one page id per lane");
+        const int my_page = (p0 + lane < p1) ? prow[p0 + lane] : 0;
+        // PPI pages per iteration: their K/V fragments for the next iteration are
+        // loaded before this iteration's pages are used (2 * PPI pages in flight)
+        constexpr int PPI = OUTLETS_DECODE_PPI;
+        uint4 kc[PPI][HD / 32], kn[PPI][HD / 32];
+        uint2 vc[PPI][HD / 16], vn[PPI][HD / 16];
+        // K/V pages are read once per step: non-temporal loads (measured on this
+        // access pattern, loads alone: 6.6 TB/s against 5.9 TB/s with ordinary
+        // loads, which a plain sequential read of the pools does not beat)
+        auto load_page = [&](int pi, uint4* kf, uint2* vf) {
+            const int64_t page = __shfl(my_page, min(pi, p1 - 1) - p0, 64);
+            const bf16_t* kb = kpool + (page * n_kv + g) * 16 * HD + col * HD + 8 * grp;
+            const bf16_t* vb = vpool + (page * n_kv + g) * HD * 16 + col * 16 + 4 * grp;
+#pragma unroll
+            for (int b = 0; b < HD / 32; ++b)
+                kf[b] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kb + 32 * b)));
+#pragma unroll
+            for (int cb = 0; cb < HD / 16; ++cb)
+                vf[cb] = __builtin_bit_cast(uint2, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(vb + 16 * 16 * cb)));
+        };
+        auto one_page = [&](int pi, const uint4* kf, const uint2* vf) {
+            f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int b = 0; b < HD / 32; ++b)
+                sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[b]), qb[b], sc, 0, 0, 0);
+            // lane: head col, keys 4 grp + i of this page; only the request's last
+            // page holds keys past the end (wave-uniform)
+            const int k0 = pi * 16 + 4 * grp;
+            const bool last = pi * 16 + 16 > nkeys;
+            if (last) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (k0 + i >= nkeys) sc[i] = -INFINITY;
+            }
+            float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            mx *= qscale;                                   // finite: key 16 pi < nkeys
+            // The reference max m moves only when the page's max exceeds it by
+            // more than 8 (probabilities then stay <= 2^8), so the rescaling of o
+            // and l is skipped, wave-uniformly, on most pages; o / l and the
+            // merge of the partial records do not depend on the reference.
+            const bool grow = mx > m + 8.f;
+            if (__any(grow)) {
+                const float mn = grow ? mx : m;
+                const float corr = fast_exp2(m - mn);
+                m = mn;
+                l *= corr;
+#pragma unroll
+                for (int cb = 0; cb < HD / 16; ++cb) o[cb] = o[cb] * corr;
+            }
+            // the probabilities enter the PV product as bf16 and the row sum adds
+            // the same bf16 values, so the output is a convex combination of the
+            // value rows
+            const float nm = -m;
+            float ps = 0.f;
+            s16x4 pb;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint16_t pv = f32_to_bf16(fast_exp2(fmaf(sc[i], qscale, nm)));
+                pb[i] = static_cast<short>(pv);
+                ps += bf16_to_f32(pv);
+            }
+            ps += __shfl_xor(ps, 16, 64);
+            ps += __shfl_xor(ps, 32, 64);
+            l += ps;
+            // value rows of keys past the end may hold stale data: zero them
+#pragma unroll
+            for (int cb = 0; cb < HD / 16; ++cb) {
+                uint2 vv = vf[cb];
+                if (last) {
+                    if (k0 + 0 >= nkeys) vv.x &= 0xFFFF0000u;
+                    if (k0 + 1 >= nkeys) vv.x &= 0x0000FFFFu;
+                    if (k0 + 2 >= nkeys) vv.y &= 0xFFFF0000u;
+                    if (k0 + 3 >= nkeys) vv.y &= 0x0000FFFFu;
+                }
+                o[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, vv), pb, o[cb], 0, 0, 0);
+            }
+        };
+#pragma unroll
+        for (int u = 0; u < PPI; ++u) load_page(p0 + u, kc[u], vc[u]);
+        for (int pi = p0; pi < p1; pi += PPI) {
+            if (pi + PPI < p1) {
+#pragma unroll
+                for (int u = 0; u < PPI; ++u) load_page(pi + PPI + u, kn[u], vn[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < PPI; ++u)
+                if (pi + u < p1) one_page(pi + u, kc[u], vc[u]);
+            if (pi + PPI < p1) {
+#pragma unroll
+                for (int u = 0; u < PPI; ++u) {
+#pragma unroll
+                    for (int b = 0; b < HD / 32; ++b) kc[u][b] = kn[u][b];
+#pragma unroll
+                    for (int cb = 0; cb < HD / 16; ++cb) vc[u][cb] = vn[u][cb];
+                }
+            }
+        }
+        // partial record [m, l, -, -, o[0..HD)] per (work item, query head
+        // g G + col); o starts 16-byte aligned
+        if (col < G) {
+            float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * kDecodeRec;
+            if (grp == 0) { rec[0] = m; rec[1] = l; }
+#pragma unroll
+            for (int cb = 0; cb < HD / 16; ++cb) *reinterpret_cast<f32x4*>(rec + 4 + 16 * cb + 4 * grp) = o[cb];
+        }
     }
 }
 
@@ -692,18 +721,52 @@ int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus) {
 }
 int attn_decode_record_floats() { return kDecodeRec; }
 
+// Each decode wave (per KV head) walks a list of work items, so the stores of
+// an item's partial record overlap the next item's page loads; only its last
+// item's stores delay the wave's exit.  (One short-lived wave per item spent
+// a store round trip per item at its exit, which under the saturated read
+// stream measured ~10% of the kernel's time.)  Lists are balanced by pages:
+// items longest first, each to the list with the fewest pages so far.
+int attn_decode_lanes(int n_work, const int32_t* item_pages, int n_kv, int cus, std::vector<int32_t>* out) {
+    // two waves per SIMD (the kernel's registers allow two), four SIMDs per CU
+    const int n_lanes = std::max(1, std::min(n_work, 8 * cus / std::max(1, n_kv)));
+    std::vector<int32_t> order(n_work);
+    for (int i = 0; i < n_work; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int32_t a, int32_t b) { return item_pages[a] > item_pages[b]; });
+    typedef std::pair<int64_t, int32_t> Load;   // (pages so far, lane)
+    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+    for (int l = 0; l < n_lanes; ++l) heap.push(Load(0, l));
+    std::vector<int32_t> lane_of(n_work), count(n_lanes, 0);
+    for (int32_t it : order) {
+        Load top = heap.top();
+        heap.pop();
+        lane_of[it] = top.second;
+        count[top.second] += 1;
+        heap.push(Load(top.first + item_pages[it], top.second));
+    }
+    out->assign(n_lanes + 1 + n_work, 0);
+    int32_t* off = out->data();
+    for (int l = 0; l < n_lanes; ++l) off[l + 1] = off[l] + count[l];
+    std::vector<int32_t> fill(off, off + n_lanes);
+    int32_t* items = off + n_lanes + 1;
+    for (int32_t it : order) items[fill[lane_of[it]]++] = it;   // longest first within a list
+    return n_lanes;
+}
+
 void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
+                        int n_lanes, const int32_t* lanes,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
                         const void* gate, hipStream_t st) {
-    if (n_req <= 0 || n_work <= 0) return;
+    if (n_req <= 0 || n_work <= 0 || n_lanes <= 0) return;
     const int G = n_q / n_kv;
     const float qscale = 1.4426950408889634f / sqrtf(128.0f);
 #define OUTLETS_DEC_G(GG)                                                                          \
     case GG:                                                                                       \
-        hipLaunchKernelGGL((attn_decode_mfma<GG>), dim3(n_work, n_kv), dim3(64), 0, st,            \
-                           static_cast<const bf16_t*>(q), ldq, work, req_slot, req_start,          \
+        hipLaunchKernelGGL((attn_decode_mfma<GG>), dim3(n_lanes, n_kv), dim3(64), 0, st,           \
+                           static_cast<const bf16_t*>(q), ldq, work, lanes, req_slot, req_start,   \
                            page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
                            static_cast<const bf16_t*>(vpool), n_kv, qscale, part, chunk);          \
         break;

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <vector>
 
 namespace outlets {
 
@@ -143,7 +144,12 @@ void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void*
 int attn_decode_chunk_pages();   // the largest chunk
 int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus);
 int attn_decode_record_floats();
+// Work lists of the decode waves: returns the list count L and fills `out`
+// with L + 1 offsets followed by the n_work item indices (balanced by
+// item_pages[i], the pages of item i).
+int attn_decode_lanes(int n_work, const int32_t* item_pages, int n_kv, int cus, std::vector<int32_t>* out);
 void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
+                        int n_lanes, const int32_t* lanes,
                         const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
                         const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
