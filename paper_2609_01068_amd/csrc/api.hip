@@ -42,6 +42,8 @@ int hip_fail(hipError_t e, const char* what) {
 
 size_t fmt_bytes(int fmt) { return fmt == FMT_F32 ? 4 : (fmt == FMT_BF16 ? 2 : 1); }
 
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 constexpr int kHeadSplits = 8;      // K splits of the length head GEMM (at least)
 
 }  // namespace
@@ -393,11 +395,30 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
     const int32_t* req_start = b.d_meta + (n + 1) + n;
     const float eps = c->cfg.rms_eps;
 
+    // A GEMM whose K is split (small M) followed by an RMSNorm leaves its
+    // partial sums to the norm kernel, which adds them (and the residual),
+    // stores the residual-stream row and normalises it in one pass.
+    auto fusable = [&](const void* gamma) {
+        return wf != FMT_F32 && rowsum_supported(static_cast<int>(d)) && aligned16(gamma);
+    };
+    auto rowsum = [&](int S, const float* resid, float* out) {
+        return RowSum{b.splitk_ws, S, static_cast<int64_t>(T) * d, d, resid, d, out, d};
+    };
     // Eq. 1: f_ctx = W_proj [h_low | h_mid | h_high]
+    int sk = 0;
     { KTimer t(c, OUTLETS_K_FUSE_GEMM, st);
-      gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(b.r_f, d), 1, st, b.splitk_ws, b.splitk_bytes); }
+      if (fusable(c->w.gamma_attn))
+          sk = gemm_launch_partials(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, b.splitk_ws,
+                                    b.splitk_bytes, st);
+      if (!sk)
+          gemm_launch(af, wf, EPI_STORE_F32, T, d, 3 * d, g.a_fuse, g.b_fuse, gemm_c(b.r_f, d), 1, st, b.splitk_ws,
+                      b.splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, b.r_f, d, c->w.gamma_attn, eps, b.a_norm, d, nullptr, 0, st);
+      if (sk)
+          launch_rmsnorm_sum(af, c->small_fmt, T, d, rowsum(sk, nullptr, b.r_f), c->w.gamma_attn, eps, b.a_norm, d,
+                             st);
+      else
+          launch_rmsnorm(af, c->small_fmt, T, d, b.r_f, d, c->w.gamma_attn, eps, b.a_norm, d, nullptr, 0, st);
       if (c->embed_in)
           launch_embed_norm(af, c->small_fmt, T, static_cast<int>(d), c->cfg.vocab, tokens, c->w.embed,
                             c->w.gamma_emb, eps, b.e_norm, d, st); }
@@ -437,14 +458,32 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
           launch_attn_paged(af, T, b.qkv, c->qkv_dim, b.attn, c->qdim, b.tok_slot, b.tok_pos,
                             c->page_table, c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads,
                             c->cfg.n_kv_heads, c->cfg.head_dim, gate, st); }
+    sk = 0;
     { KTimer t(c, OUTLETS_K_O_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(b.r_x1, d, b.r_f, d), 1, st, b.splitk_ws, b.splitk_bytes); }
+      if (fusable(c->w.gamma_mlp))
+          sk = gemm_launch_partials(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, b.splitk_ws, b.splitk_bytes,
+                                    st);
+      if (!sk)
+          gemm_launch(af, wf, EPI_RESID_F32, T, d, c->qdim, g.a_o, g.b_o, gemm_c(b.r_x1, d, b.r_f, d), 1, st,
+                      b.splitk_ws, b.splitk_bytes); }
     { KTimer t(c, OUTLETS_K_NORM, st);
-      launch_rmsnorm(af, c->small_fmt, T, d, b.r_x1, d, c->w.gamma_mlp, eps, b.b_norm, d, nullptr, 0, st); }
+      if (sk)
+          launch_rmsnorm_sum(af, c->small_fmt, T, d, rowsum(sk, b.r_f, b.r_x1), c->w.gamma_mlp, eps, b.b_norm, d,
+                             st);
+      else
+          launch_rmsnorm(af, c->small_fmt, T, d, b.r_x1, d, c->w.gamma_mlp, eps, b.b_norm, d, nullptr, 0, st); }
     { KTimer t(c, OUTLETS_K_GATE_UP_GEMM, st);
       gemm_launch(af, wf, EPI_SWIGLU, T, g.n_gu, d, g.a_gu, g.b_gu, gemm_c(b.mlp, c->F), 1, st, b.splitk_ws, b.splitk_bytes); }
+    // steps: the down GEMM's partials go to the final norm + pooling kernel
+    sk = 0;
     { KTimer t(c, OUTLETS_K_DOWN_GEMM, st);
-      gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(b.r_x2, d, b.r_x1, d), 1, st, b.splitk_ws, b.splitk_bytes); }
+      if (!prefill && fusable(c->w.gamma_final))
+          sk = gemm_launch_partials(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, b.splitk_ws,
+                                    b.splitk_bytes, st);
+      if (!sk)
+          gemm_launch(af, wf, EPI_RESID_F32, T, d, c->F, g.a_down, g.b_down, gemm_c(b.r_x2, d, b.r_x1, d), 1, st,
+                      b.splitk_ws, b.splitk_bytes); }
+    const RowSum down_rows = rowsum(sk, b.r_x1, c->cfg.keep_intermediates ? b.r_x2 : nullptr);
     uint16_t* pb = (wf == FMT_F32) ? nullptr : b.pooled_bf16;
     // prefill: final RMSNorm + pooling in one pass over x2 (h_draft rows are
     // stored only when the caller wants them or intermediates are kept; the
@@ -460,9 +499,10 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
         // steps (one row per request): the f32 h_draft rows are kept only
         // with intermediates
         KTimer t(c, OUTLETS_K_POOL, st);
-        fused_pool = launch_norm_pool_step(af, c->small_fmt, n, d, b.r_x2, d, c->w.gamma_final, eps, hdraft_out, d,
-                                           c->cfg.keep_intermediates ? b.r_h : nullptr, d, req_slot, req_start,
-                                           c->pool_sum, b.pooled, pb, st);
+        fused_pool = launch_norm_pool_step(af, c->small_fmt, n, d, sk ? nullptr : b.r_x2, d, c->w.gamma_final, eps,
+                                           hdraft_out, d, c->cfg.keep_intermediates ? b.r_h : nullptr, d, req_slot,
+                                           req_start, c->pool_sum, b.pooled, pb, st, sk ? &down_rows : nullptr);
+        if (sk && !fused_pool) return fail(OUTLETS_ERR_HIP, "internal: split down GEMM without its norm kernel");
     }
     if (!fused_pool) {
         { KTimer t(c, OUTLETS_K_NORM, st);
@@ -541,8 +581,6 @@ std::vector<int32_t> attention_work(int n, const int32_t* lens, int qt) {
     for (auto& it : items) { out.push_back(it.first); out.push_back(it.second); }
     return out;
 }
-
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 int check_states(const outlets_ctx* c, const void* hl, const void* hm, const void* hh,
                  int64_t row_stride, const int32_t* tokens, const float* z_out) {

@@ -904,6 +904,18 @@ int gemm_check(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA
     return OUTLETS_OK;
 }
 
+int gemm_launch_partials(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
+                         const GemmB& b, float* ws, size_t ws_bytes, hipStream_t st) {
+    const SplitPlan pl = split_plan(w_fmt, epi, M, N, K, 1, ws ? ws_bytes : 0);
+    if (pl.sk < 2) return 0;
+    GemmC pc{};
+    pc.c = ws;
+    pc.ldc = N;
+    pc.split_stride = (int64_t)M * N;
+    gemm_launch(act_fmt, w_fmt, EPI_PARTIAL, M, N, K, a, b, pc, pl.sk, st, nullptr, 0);
+    return pl.sk;
+}
+
 size_t gemm_workspace_bytes(int w_fmt, int epi, int M, int N, int K, size_t ws_bytes) {
     return split_plan(w_fmt, epi, M, N, K, 1, ws_bytes).bytes;
 }

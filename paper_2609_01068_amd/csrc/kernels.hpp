@@ -79,6 +79,13 @@ void gemm_launch(int act_fmt, int w_fmt, int epi, int M, int N, int K, const Gem
                  const GemmB& b, const GemmC& c, int splits, hipStream_t st,
                  float* ws = nullptr, size_t ws_bytes = 0);
 int gemm_splitk_plan(int w_fmt, int epi, int M, int N, int K);
+// The partial-sum half of a split-K call: when gemm_launch would split this
+// call (epilogue `epi`, workspace ws of ws_bytes), launches only the split
+// GEMM, leaving S fp32 planes [M, N] in ws (plane s at ws + s M N), and
+// returns S; otherwise launches nothing and returns 0.  A row kernel that
+// takes a RowSum then finishes the call (see launch_rmsnorm_sum).
+int gemm_launch_partials(int act_fmt, int w_fmt, int epi, int M, int N, int K, const GemmA& a,
+                         const GemmB& b, float* ws, size_t ws_bytes, hipStream_t st);
 // Bytes of fp32 workspace gemm_launch uses for this call when given ws_bytes
 // (0 when it splits nothing); a call given exactly these bytes takes the
 // same plan as with ws_bytes.
@@ -100,11 +107,31 @@ void launch_build_tokens(int n_req, const int32_t* req_off, const int32_t* req_s
                          int32_t* last_idx, hipStream_t st);
 void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStream_t st);
 
+// Row x[r] of a split-K GEMM's output: the S partial planes summed in split
+// order, plus resid[r] when resid is set (the fp32 residual the GEMM's
+// epilogue would add); stored to out[r] when out is set (it may alias resid).
+struct RowSum {
+    const float* part;
+    int S;
+    int64_t plane;   // elements between partial planes (M N)
+    int64_t ldp;     // elements between partial rows (N)
+    const float* resid;
+    int64_t ldr;
+    float* out;
+    int64_t ldo;
+};
+// Whether the row kernels take a RowSum for rows of d elements.
+bool rowsum_supported(int d);
+
 // y = x / sqrt(mean(x^2) + eps) * gamma per row; x fp32; y in act format
 // (either output may be null; y2 is an fp32 copy and may alias x).
 void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x, int64_t ldx,
                     const void* gamma, float eps, void* y, int64_t ldy, float* y2,
                     int64_t ldy2, hipStream_t st);
+
+// launch_rmsnorm of the rows a RowSum forms (rowsum_supported(d) must hold).
+void launch_rmsnorm_sum(int act_fmt, int gamma_fmt, int rows, int d, const RowSum& rs, const void* gamma,
+                        float eps, void* y, int64_t ldy, hipStream_t st);
 
 // EAGLE-3 input embeddings: y[r] = RMSNorm(embed[tok[r]]) * gamma for `rows`
 // token ids; embed [vocab, d] and y in act format, gamma in gamma_fmt.  Ids
@@ -184,10 +211,12 @@ bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles
 // y (act) / y2 (f32) receive the normed rows when non-null.  Returns false,
 // launching nothing, for shapes the fused kernel does not take (as
 // launch_norm_pool_prefill).
+// With rs (non-null; rowsum_supported(d)), row i is the RowSum's row i
+// instead of x[i].
 bool launch_norm_pool_step(int act_fmt, int gamma_fmt, int n_req, int d, const float* x, int64_t ldx,
                            const void* gamma, float eps, void* y, int64_t ldy, float* y2, int64_t ldy2,
                            const int32_t* req_slot, const int32_t* req_start, float* pool_sum, float* pooled,
-                           uint16_t* pooled_bf16, hipStream_t st);
+                           uint16_t* pooled_bf16, hipStream_t st, const RowSum* rs = nullptr);
 // Step pooling: pool_sum[slot] += h[i]; pooled[i] = [pool_sum / (start + 1) ; h[i]].
 void launch_pool_step(int n_req, int d, int h_fmt, const void* h, int64_t ldh, const int32_t* req_slot,
                       const int32_t* req_start, float* pool_sum, float* pooled,

@@ -48,14 +48,34 @@ rmsnorm_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float eps, T
     }
 }
 
+// Element group j4 (elements 4 j4 .. 4 j4 + 3) of a RowSum's row: the
+// partials added in split order, then the residual added to that sum (the
+// order of splitk_reduce), stored to rs.out when set.
+__device__ __forceinline__ float4 rowsum_load(const RowSum& rs, int64_t row, int j4) {
+    const float4* p = reinterpret_cast<const float4*>(rs.part + row * rs.ldp) + j4;
+    const int64_t step = rs.plane / 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = 0; sp < rs.S; ++sp) {
+        const float4 q = p[sp * step];
+        v.x += q.x; v.y += q.y; v.z += q.z; v.w += q.w;
+    }
+    if (rs.resid) {
+        const float4 r = reinterpret_cast<const float4*>(rs.resid + row * rs.ldr)[j4];
+        v = make_float4(r.x + v.x, r.y + v.y, r.z + v.z, r.w + v.w);
+    }
+    if (rs.out) reinterpret_cast<float4*>(rs.out + row * rs.ldo)[j4] = v;
+    return v;
+}
+
 // Vectorised form for d = 1024 V (V = 1..8 groups of 4 floats per thread):
 // the row stays in registers between the sum of squares and the scaling,
 // and every access is a 16-byte (x, y2) or 8-byte (bf16 y, gamma) access
 // with consecutive threads on consecutive addresses.
-template <typename TY, typename TG, int V>
+// With SUM the row is a RowSum's (a split-K GEMM finished here) instead of x.
+template <typename TY, typename TG, int V, bool SUM = false>
 __global__ void __launch_bounds__(256)
 rmsnorm_vec_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
-                   int64_t ldy, float* y2, int64_t ldy2) {
+                   int64_t ldy, float* y2, int64_t ldy2, RowSum rs = RowSum{}) {
     __shared__ float red[4];
     const int64_t row = blockIdx.x;
     const int t = threadIdx.x;
@@ -64,7 +84,7 @@ rmsnorm_vec_kernel(int d, const float* x, int64_t ldx, const TG* gamma, float ep
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-        v[j] = xr[j * 256 + t];
+        v[j] = SUM ? rowsum_load(rs, row, j * 256 + t) : xr[j * 256 + t];
         ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
     }
     ss = block_sum<256>(ss, red);
@@ -409,11 +429,11 @@ pool_step_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_slot,
 // scaling and the pooling arithmetic are rmsnorm_vec_kernel's and
 // pool_step_kernel's; the sum of squares is taken over NT partial sums.
 // y / y2 (the h_draft row) are stored only when non-null.
-template <typename TY, typename TG, int NT, int V>
+template <typename TY, typename TG, int NT, int V, bool SUM = false>
 __global__ void __launch_bounds__(NT)
 norm_pool_step_kernel(int d, int n_req, const float* x, int64_t ldx, const TG* gamma, float eps, TY* y,
                       int64_t ldy, float* y2, int64_t ldy2, const int32_t* req_slot, const int32_t* req_start,
-                      float* pool_sum, float* pooled, uint16_t* pooled_bf16) {
+                      float* pool_sum, float* pooled, uint16_t* pooled_bf16, RowSum rs = RowSum{}) {
     __shared__ float red[NT / 64];
     const int64_t row = blockIdx.x;
     const int t = threadIdx.x;
@@ -422,7 +442,7 @@ norm_pool_step_kernel(int d, int n_req, const float* x, int64_t ldx, const TG* g
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-        v[j] = xr[j * NT + t];
+        v[j] = SUM ? rowsum_load(rs, row, j * NT + t) : xr[j * NT + t];
         ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
     }
     ss = block_sum<NT>(ss, red);
@@ -561,6 +581,29 @@ void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStre
     if (n_pairs <= 0) return;
     hipLaunchKernelGGL(scatter_kernel, dim3((n_pairs + 255) / 256), dim3(256), 0, st, n_pairs,
                        pairs, dst);
+}
+
+bool rowsum_supported(int d) { return d == 1024 || d == 2048 || d == 4096 || d == 8192; }
+
+void launch_rmsnorm_sum(int act_fmt, int gamma_fmt, int rows, int d, const RowSum& rs, const void* gamma,
+                        float eps, void* y, int64_t ldy, hipStream_t st) {
+    if (rows <= 0) return;
+    const int V = d / 1024;
+#define OUTLETS_NORMS_V(TY, TG)                                                                            \
+    switch (V) {                                                                                           \
+        case 1: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 1, true>), dim3(rows), dim3(256), 0, st, d, nullptr, 0, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, nullptr, 0, rs); break; \
+        case 2: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 2, true>), dim3(rows), dim3(256), 0, st, d, nullptr, 0, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, nullptr, 0, rs); break; \
+        case 4: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 4, true>), dim3(rows), dim3(256), 0, st, d, nullptr, 0, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, nullptr, 0, rs); break; \
+        case 8: hipLaunchKernelGGL((rmsnorm_vec_kernel<TY, TG, 8, true>), dim3(rows), dim3(256), 0, st, d, nullptr, 0, \
+                                   static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, nullptr, 0, rs); break; \
+    }
+    if (act_fmt == FMT_F32) { OUTLETS_NORMS_V(float, float) }
+    else if (gamma_fmt == FMT_F32) { OUTLETS_NORMS_V(bf16_t, float) }
+    else { OUTLETS_NORMS_V(bf16_t, bf16_t) }
+#undef OUTLETS_NORMS_V
 }
 
 void launch_rmsnorm(int act_fmt, int gamma_fmt, int rows, int d, const float* x, int64_t ldx,
@@ -714,7 +757,7 @@ bool launch_norm_pool_prefill(int act_fmt, int gamma_fmt, int n_req, int n_tiles
 bool launch_norm_pool_step(int act_fmt, int gamma_fmt, int n_req, int d, const float* x, int64_t ldx,
                            const void* gamma, float eps, void* y, int64_t ldy, float* y2, int64_t ldy2,
                            const int32_t* req_slot, const int32_t* req_start, float* pool_sum, float* pooled,
-                           uint16_t* pooled_bf16, hipStream_t st) {
+                           uint16_t* pooled_bf16, hipStream_t st, const RowSum* rs) {
     const bool vec = d % 1024 == 0 && d <= 8192 && ldx % 4 == 0 && (!y || ldy % 4 == 0) && (!y2 || ldy2 % 4 == 0) &&
                      reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0 &&
                      reinterpret_cast<uintptr_t>(y2) % 16 == 0 && reinterpret_cast<uintptr_t>(gamma) % 16 == 0 &&
@@ -725,9 +768,14 @@ bool launch_norm_pool_step(int act_fmt, int gamma_fmt, int n_req, int d, const f
     const int V = d / 1024;   // d = 1024 V: NT = 256 V threads of one float4 up to d = 4096, then 2 each
 #define OUTLETS_NPS_V(TY, TG, VV, NT, PER)                                                                 \
     case VV:                                                                                               \
-        hipLaunchKernelGGL((norm_pool_step_kernel<TY, TG, NT, PER>), dim3(n_req), dim3(NT), 0, st, d, n_req, x, \
-                           ldx, static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2, req_slot, \
-                           req_start, pool_sum, pooled, pooled_bf16);                                         \
+        if (rs)                                                                                            \
+            hipLaunchKernelGGL((norm_pool_step_kernel<TY, TG, NT, PER, true>), dim3(n_req), dim3(NT), 0, st, d, \
+                               n_req, x, ldx, static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, \
+                               ldy2, req_slot, req_start, pool_sum, pooled, pooled_bf16, *rs);            \
+        else                                                                                               \
+            hipLaunchKernelGGL((norm_pool_step_kernel<TY, TG, NT, PER>), dim3(n_req), dim3(NT), 0, st, d, n_req, \
+                               x, ldx, static_cast<const TG*>(gamma), eps, static_cast<TY*>(y), ldy, y2, ldy2, \
+                               req_slot, req_start, pool_sum, pooled, pooled_bf16);                      \
         break;
 #define OUTLETS_NPS(TY, TG)                                                                                \
     switch (V) { OUTLETS_NPS_V(TY, TG, 1, 256, 1) OUTLETS_NPS_V(TY, TG, 2, 512, 1)                          \
