@@ -164,7 +164,9 @@ struct outlets_ctx {
     hipEvent_t take_event() {
         hipEvent_t e = nullptr;
         if (!spare.empty()) { e = spare.back(); spare.pop_back(); return e; }
-        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        // timing only: no system-scope fence (a cache write-back and
+        // invalidate per record would perturb the work being timed)
+        if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
         return e;
     }
 
