@@ -412,6 +412,29 @@ const char* outlets_last_error(void);
 int outlets_varlen_meta(int32_t n_req, const int32_t* lens, int32_t* cu_out,
                         int32_t* pos_out, int32_t* last_out);
 
+/*
+ * The split-KV work plan that outlets_predict_step uses for decode attention
+ * (bf16, head dim 128; Section 3.2 dynamic prediction reads the whole paged
+ * cache of every request at each step).  pages[i] = pages of request i's
+ * cache including the step's token (>= 1); n_kv = KV heads; cus = compute
+ * units.  The pages, requests in order, are cut into n_lanes contiguous
+ * ranges whose lengths differ by at most one page (one wave per range and
+ * KV head); a range's part in one request is a segment (one partial softmax
+ * record), walked in pieces of at most 64 pages.  Outputs (host):
+ *   counts[3] = n_pieces, n_segs, n_lanes (always written);
+ *   work [4 n_pieces] = (request, first page, end page, segment) per piece;
+ *   cu_segs [n_req + 1] = first segment of each request (segments of a
+ *   request are consecutive, in page order);
+ *   lane_off [n_lanes + 1] = first piece of each range.
+ * work, cu_segs and lane_off may all be NULL (counts only); otherwise all
+ * three are written, and capacities below 4 n_pieces (work_cap) or
+ * n_lanes + 1 (lane_cap) fail with OUTLETS_ERR_INVALID_ARG and write only
+ * counts.  Bad sizes or a page count below 1 fail with INVALID_ARG.
+ */
+int outlets_decode_plan(int32_t n_req, const int32_t* pages, int32_t n_kv, int32_t cus, int32_t* counts,
+                        int32_t* work, int64_t work_cap, int32_t* cu_segs, int32_t* lane_off,
+                        int64_t lane_cap);
+
 /* A stand-alone instance of the context's page allocator (host memory only). */
 int outlets_pager_create(int32_t num_pages, int32_t page_size, int32_t max_slots,
                          int32_t max_seq_len, outlets_pager** out);

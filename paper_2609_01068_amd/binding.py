@@ -103,6 +103,8 @@ _SIGS = {
     "outlets_profile_enable_groups": (C.c_int, [_P, C.c_uint32]),
     "outlets_profile_read": (C.c_int, [_P, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "outlets_varlen_meta": (C.c_int, [C.c_int32, _I32P, _I32P, _I32P, _I32P]),
+    "outlets_decode_plan": (C.c_int, [C.c_int32, _I32P, C.c_int32, C.c_int32, _I32P, _I32P, C.c_int64, _I32P,
+                                      _I32P, C.c_int64]),
     "outlets_pager_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(_P)]),
     "outlets_pager_destroy": (C.c_int, [_P]),
     "outlets_pager_prefill": (C.c_int, [_P, C.c_int32, _I32P, _I32P]),
@@ -252,6 +254,21 @@ def outlets_varlen_meta(lens):
     cu, pos, last = (C.c_int32 * (n + 1))(), (C.c_int32 * max(1, T))(), (C.c_int32 * max(1, n))()
     check(lib().outlets_varlen_meta(n, i32_array(lens), cu, pos, last), "outlets_varlen_meta")
     return list(cu), list(pos[:T]), list(last[:n])
+
+
+def outlets_decode_plan(pages, n_kv: int, cus: int):
+    """The decode-attention work plan of a step (host only): returns
+    (work [n_pieces, 4] rows of (request, first page, end page, segment),
+    cu_segs [n_req + 1], lane_off [n_lanes + 1])."""
+    n = len(pages)
+    pg = i32_array(pages)
+    counts = (C.c_int32 * 3)()
+    check(lib().outlets_decode_plan(n, pg, n_kv, cus, counts, None, 0, None, None, 0), "outlets_decode_plan")
+    n_pieces, n_segs, n_lanes = list(counts)
+    work, cu, lanes = (C.c_int32 * (4 * n_pieces))(), (C.c_int32 * (n + 1))(), (C.c_int32 * (n_lanes + 1))()
+    check(lib().outlets_decode_plan(n, pg, n_kv, cus, counts, work, 4 * n_pieces, cu, lanes, n_lanes + 1),
+          "outlets_decode_plan")
+    return [tuple(work[4 * i:4 * i + 4]) for i in range(n_pieces)], list(cu), list(lanes)
 
 
 class Pager:

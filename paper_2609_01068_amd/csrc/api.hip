@@ -124,7 +124,6 @@ struct outlets_ctx {
     int64_t work_off = 0;        // offset of the prefill attention work list in d_meta
     int32_t n_work = 0;
     int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
-    int32_t dec_chunk = 64;        // pages per decode attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
     int64_t lanes_off = 0;       // offset of the decode waves' work lists in d_meta
     int32_t n_lanes = 0;         // decode work lists of the current call
@@ -451,7 +450,7 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
                               req_off, req_slot, c->page_table, c->max_pages, c->kpool, c->vpool,
                               c->cfg.n_q_heads, c->cfg.n_kv_heads, gate, st);
       else if (!prefill && c->n_work > 0)
-          launch_attn_decode(n, c->n_work, c->dec_chunk, b.d_meta + c->work_off, b.d_meta + c->tiles_off,
+          launch_attn_decode(n, c->n_work, b.d_meta + c->work_off, b.d_meta + c->tiles_off,
                              c->n_lanes, b.d_meta + c->lanes_off, b.qkv,
                              c->qkv_dim, b.attn, c->qdim, req_slot, req_start, c->page_table,
                              c->max_pages, c->kpool, c->vpool, c->cfg.n_q_heads, c->cfg.n_kv_heads,
@@ -535,7 +534,7 @@ int run_layer(outlets_ctx* c, const CallBufs& b, bool prefill, int n, int T, con
 int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int32_t>& off, const int32_t* slots,
                 const std::vector<int32_t>& start, const std::vector<int32_t>& updates,
                 const std::vector<int32_t>& work, const std::vector<int32_t>& cu_tiles,
-                const std::vector<int32_t>& lanes, hipStream_t st) {
+                const std::vector<int32_t>& lanes, int work_stride, hipStream_t st) {
     const int64_t count = (n + 1) + 2 * static_cast<int64_t>(n) + static_cast<int64_t>(updates.size()) +
                           static_cast<int64_t>(work.size()) + static_cast<int64_t>(cu_tiles.size()) +
                           static_cast<int64_t>(lanes.size());
@@ -548,7 +547,7 @@ int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int3
     std::memcpy(h + 2 * n + 1, start.data(), sizeof(int32_t) * n);
     if (!updates.empty()) std::memcpy(h + 3 * n + 1, updates.data(), sizeof(int32_t) * updates.size());
     c->work_off = 3 * n + 1 + static_cast<int64_t>(updates.size());
-    c->n_work = static_cast<int32_t>(work.size() / 2);
+    c->n_work = static_cast<int32_t>(work.size() / work_stride);
     if (!work.empty()) std::memcpy(h + c->work_off, work.data(), sizeof(int32_t) * work.size());
     c->tiles_off = c->work_off + static_cast<int64_t>(work.size());
     c->n_tiles = cu_tiles.empty() ? 0 : cu_tiles.back();
@@ -602,7 +601,7 @@ int check_states(const outlets_ctx* c, const void* hl, const void* hm, const voi
 // split-KV attention partials and the head partials, whose uses are ordered
 // one after another on the call's stream.  With base == nullptr only the
 // size is computed.  Returns the bytes used.
-size_t layout_step(const outlets_ctx* c, int n, int64_t n_chunks, int64_t meta_count, size_t ws_bytes,
+size_t layout_step(const outlets_ctx* c, int n, int64_t n_records, int64_t meta_count, size_t ws_bytes,
                    char* base, CallBufs* b) {
     size_t off = 0;
     auto take = [&](size_t bytes) -> char* {
@@ -629,7 +628,7 @@ size_t layout_step(const outlets_ctx* c, int n, int64_t n_chunks, int64_t meta_c
     if (c->w_fmt != FMT_F32) b->pooled_bf16 = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * 2 * N * 2 * c->d));
     size_t region = ws_bytes;
     if (attn_prefill_mfma_supported(c->act_fmt, c->cfg.n_q_heads, c->cfg.n_kv_heads, c->cfg.head_dim))
-        region = std::max(region, sizeof(float) * static_cast<size_t>(n_chunks) * c->cfg.n_q_heads *
+        region = std::max(region, sizeof(float) * static_cast<size_t>(n_records) * c->cfg.n_q_heads *
                                       attn_decode_record_floats());
     const int rows = (c->w_fmt == FMT_F32 ? 1 : 2) * n;
     region = std::max(region, sizeof(float) * static_cast<size_t>(head_splits(c, rows)) * rows * c->H1);
@@ -695,49 +694,36 @@ int predict_step_impl(outlets_ctx* ctx, bool noalloc, int32_t n_req, const int32
         start[i] = ctx->pager->seq_len(slots[i]);
         new_pages += (start[i] % 16 == 0);
     }
-    // split-KV decode work items (request, chunk of pages), requests in order
-    std::vector<int32_t> dwork, cu_chunks, lanes;
-    int chunk = ctx->dec_chunk, n_lanes = 0;
+    // split-KV decode: the step's pages cut into equal contiguous ranges, one
+    // per wave and KV head (segments and pieces, see attn_decode_plan)
+    DecodePlan plan;
     if (attn_prefill_mfma_supported(ctx->act_fmt, ctx->cfg.n_q_heads, ctx->cfg.n_kv_heads, ctx->cfg.head_dim)) {
-        std::vector<int32_t> pages(n_req), item_pages;
+        std::vector<int32_t> pages(n_req);
         for (int i = 0; i < n_req; ++i) pages[i] = (start[i] + 1 + 15) / 16;
-        chunk = attn_decode_chunk_for(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus());
-        cu_chunks.assign(n_req + 1, 0);
-        for (int i = 0; i < n_req; ++i) {
-            const int nch = (pages[i] + chunk - 1) / chunk;
-            cu_chunks[i + 1] = cu_chunks[i] + nch;
-            for (int c = 0; c < nch; ++c) {
-                dwork.push_back(i);
-                dwork.push_back(c);
-                item_pages.push_back(std::min(chunk, pages[i] - c * chunk));
-            }
-        }
-        n_lanes = attn_decode_lanes(static_cast<int>(item_pages.size()), item_pages.data(), ctx->cfg.n_kv_heads,
-                                    gemm_device_cus(), &lanes);
+        attn_decode_plan(n_req, pages.data(), ctx->cfg.n_kv_heads, gemm_device_cus(), &plan);
     }
     CallBufs sb;
     const CallBufs* bufs = &ctx->cb;
     if (noalloc) {
-        const int64_t n_chunks = static_cast<int64_t>(dwork.size() / 2);
+        const int64_t n_records = plan.n_segs;
         const int64_t meta_count = (n_req + 1) + 2 * static_cast<int64_t>(n_req) + 2 * new_pages +
-                                   static_cast<int64_t>(dwork.size() + cu_chunks.size() + lanes.size());
+                                   static_cast<int64_t>(plan.work.size() + plan.cu_segs.size() + plan.lanes.size());
         const size_t ws = step_splitk_bytes(ctx, n_req);
-        const size_t need = layout_step(ctx, n_req, n_chunks, meta_count, ws, nullptr, &sb);
+        const size_t need = layout_step(ctx, n_req, n_records, meta_count, ws, nullptr, &sb);
         if (need > kScratchBytes)
             return fail(OUTLETS_ERR_INVALID_ARG, "the step needs " + std::to_string(need) +
                                                      " bytes of scratch; the static scratch holds " +
                                                      std::to_string(kScratchBytes));
-        layout_step(ctx, n_req, n_chunks, meta_count, ws, static_cast<char*>(ctx->scratch), &sb);
+        layout_step(ctx, n_req, n_records, meta_count, ws, static_cast<char*>(ctx->scratch), &sb);
         bufs = &sb;
     }
     std::vector<int32_t> updates;
     ctx->prof_phase = 1;
     rc = ctx->pager->step(n_req, slots, &updates, &why);
     if (rc) return fail(rc, why);
-    ctx->dec_chunk = chunk;
-    ctx->n_lanes = n_lanes;
+    ctx->n_lanes = plan.n_lanes;
     NoTiming nt(ctx, noalloc);
-    rc = upload_meta(ctx, *bufs, n_req, off, slots, start, updates, dwork, cu_chunks, lanes, st);
+    rc = upload_meta(ctx, *bufs, n_req, off, slots, start, updates, plan.work, plan.cu_segs, plan.lanes, 4, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, *bufs, false, n_req, n_req, h_low, h_mid, h_high, row_stride, tokens, z_out,
                        hdraft_out, st);
@@ -861,18 +847,16 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     ALLOC(c->cb.tok_slot, sizeof(int32_t) * Tm);
     ALLOC(c->cb.tok_pos, sizeof(int32_t) * Tm);
     ALLOC(c->cb.last_idx, sizeof(int32_t) * Bm);
-    // decode work items: chunks of the largest size, or, where the step
-    // halves the size because those fill fewer than 2 waves per CU over the
-    // KV heads, at most 4x that many (16-page chunks)
-    const int64_t max_chunks = std::max<int64_t>(
-        Bm * ((c->max_pages + attn_decode_chunk_pages() - 1) / attn_decode_chunk_pages()),
-        (int64_t)(64 / 16) * (2 * gemm_device_cus() / std::max(1, cfg->n_kv_heads) + 1));
-    // req_off | req_slot | req_start | page updates | work list | cu tiles or
-    // chunks | decode work lists (at most one list per item, plus offsets)
-    c->cb.meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + 2 * std::max(Tm / 32 + Bm, max_chunks) + (Bm + 1) +
-                     (2 * max_chunks + 1);
+    // decode plan bounds: segments (partial records) and pieces of a step
+    const int64_t max_segs = attn_decode_max_segments(Bm, cfg->n_kv_heads, gemm_device_cus());
+    const int64_t max_pieces = attn_decode_max_pieces(Bm, c->max_pages, cfg->n_kv_heads, gemm_device_cus());
+    // req_off | req_slot | req_start | page updates | work list (prefill
+    // tiles, 2 ints each, or decode pieces, 4 ints each) | cu tiles or
+    // segments | decode lane offsets (at most one lane per segment)
+    c->cb.meta_cap = 3 * Bm + 1 + 2 * (Tm / 16 + Bm) + std::max(2 * (Tm / 32 + Bm), 4 * max_pieces) + (Bm + 1) +
+                     (max_segs + 1);
     if (attn_prefill_mfma_supported(c->act_fmt, cfg->n_q_heads, cfg->n_kv_heads, cfg->head_dim))
-        ALLOC(c->cb.decode_part, sizeof(float) * max_chunks * cfg->n_q_heads * attn_decode_record_floats());
+        ALLOC(c->cb.decode_part, sizeof(float) * max_segs * cfg->n_q_heads * attn_decode_record_floats());
     ALLOC(c->cb.pool_part, sizeof(float) * (Tm / 32 + Bm) * c->d);
     {
         // split-K scratch: the largest plan over the layer's GEMMs for M up to 1024
@@ -978,7 +962,7 @@ int outlets_predict_prefill(outlets_ctx* ctx, int32_t n_req, const int32_t* slot
     }
     std::vector<int32_t> cu_tiles(n_req + 1, 0);
     for (int i = 0; i < n_req; ++i) cu_tiles[i + 1] = cu_tiles[i] + (lens[i] + 31) / 32;
-    rc = upload_meta(ctx, ctx->cb, n_req, off, slots, start, updates, work, cu_tiles, {}, st);
+    rc = upload_meta(ctx, ctx->cb, n_req, off, slots, start, updates, work, cu_tiles, {}, 2, st);
     if (rc == OUTLETS_OK)
         rc = run_layer(ctx, ctx->cb, true, n_req, static_cast<int>(T), h_low, h_mid, h_high, row_stride, tokens,
                        z_out, hdraft_out, st);
@@ -1275,6 +1259,35 @@ int outlets_varlen_meta(int32_t n_req, const int32_t* lens, int32_t* cu_out, int
     if (n_req < 0 || (n_req > 0 && !lens)) return fail(OUTLETS_ERR_INVALID_ARG, "bad lengths");
     int rc = varlen_meta(n_req, lens, cu_out, pos_out, last_out);
     return rc ? fail(rc, "lengths must be >= 1 and sum below 2^31") : OUTLETS_OK;
+}
+
+int outlets_decode_plan(int32_t n_req, const int32_t* pages, int32_t n_kv, int32_t cus, int32_t* counts,
+                        int32_t* work, int64_t work_cap, int32_t* cu_segs, int32_t* lane_off,
+                        int64_t lane_cap) {
+    if (n_req < 1 || !pages || n_kv < 1 || cus < 1 || !counts) return fail(OUTLETS_ERR_INVALID_ARG, "bad sizes");
+    int64_t total = 0;
+    for (int i = 0; i < n_req; ++i) {
+        if (pages[i] < 1) return fail(OUTLETS_ERR_INVALID_ARG, "page counts must be >= 1");
+        total += pages[i];
+    }
+    if (total > INT32_MAX) return fail(OUTLETS_ERR_INVALID_ARG, "page total exceeds 2^31");
+    DecodePlan plan;
+    try {
+        attn_decode_plan(n_req, pages, n_kv, cus, &plan);
+    } catch (const std::bad_alloc&) {
+        return fail(OUTLETS_ERR_NOMEM, "host allocation failed");
+    }
+    counts[0] = static_cast<int32_t>(plan.work.size() / 4);
+    counts[1] = plan.n_segs;
+    counts[2] = plan.n_lanes;
+    if (!work && !cu_segs && !lane_off) return OUTLETS_OK;
+    if (!work || !cu_segs || !lane_off) return fail(OUTLETS_ERR_INVALID_ARG, "give all three arrays or none");
+    if (work_cap < static_cast<int64_t>(plan.work.size()) || lane_cap < static_cast<int64_t>(plan.lanes.size()))
+        return fail(OUTLETS_ERR_INVALID_ARG, "capacity too small");
+    std::memcpy(work, plan.work.data(), sizeof(int32_t) * plan.work.size());
+    std::memcpy(cu_segs, plan.cu_segs.data(), sizeof(int32_t) * plan.cu_segs.size());
+    std::memcpy(lane_off, plan.lanes.data(), sizeof(int32_t) * plan.lanes.size());
+    return OUTLETS_OK;
 }
 
 struct outlets_pager {

@@ -17,7 +17,6 @@
 #include <type_traits>
 
 #include <algorithm>
-#include <queue>
 #include <vector>
 
 #include "common.hpp"
@@ -416,10 +415,13 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
 }
 
 // ---------------------------------------------------------------- decode, MFMA
-// One query token per request (a decode step).  Split-KV: one wave per
-// (request, KV head, chunk of up to kDecodeChunk pages); each wave keeps an online
-// softmax for the G query heads of its KV head and writes (m, l, o) partials,
-// which attn_decode_combine merges in chunk order (deterministic).
+// One query token per request (a decode step).  Split-KV over contiguous page
+// ranges: the step's pages, requests in order, are cut into equal ranges, one
+// per wave and KV head (attn_decode_plan).  A wave's range splits at request
+// ends into segments; each segment keeps one online softmax for the G query
+// heads of the KV head and leaves one (m, l, o) partial record, which
+// attn_decode_combine merges in segment order (deterministic).  Segments are
+// walked in pieces of at most kDecodeChunk pages (one page id per lane).
 //
 // Per 16-key page: S = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K rows, lane
 // l -> key l % 16; B = Q^T with the G heads in columns 0..G-1 of 16, the rest
@@ -427,7 +429,7 @@ attn_prefill_mfma(const bf16_t* qkv, int64_t ldq, bf16_t* out, int64_t ldo, cons
 // 4 (l / 16) + i, which is exactly the B-operand layout of
 // O^T += V^T P^T with v_mfma_f32_16x16x16bf16_1k (A = V^T rows from the
 // transposed value page).  The softmax is lane-local plus two xor-shuffles.
-// The next page's K/V fragments are loaded before the current page is used.
+// The next pages' K/V fragments are loaded before the current ones are used.
 #ifndef OUTLETS_DECODE_CHUNK
 #define OUTLETS_DECODE_CHUNK 64
 #endif
@@ -443,24 +445,52 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int G>
 __global__ void __launch_bounds__(64)
-attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_t* lanes,
-                 const int32_t* req_slot, const int32_t* req_start, const int32_t* page_table, int max_pages,
-                 const bf16_t* kpool, const bf16_t* vpool, int n_kv, float qscale, float* part, int chunk) {
+attn_decode_mfma(const bf16_t* __restrict__ q, int64_t ldq, const int32_t* __restrict__ work,
+                 const int32_t* __restrict__ lanes, const int32_t* __restrict__ req_slot,
+                 const int32_t* __restrict__ req_start, const int32_t* __restrict__ page_table, int max_pages,
+                 const bf16_t* __restrict__ kpool, const bf16_t* __restrict__ vpool, int n_kv, float qscale,
+                 float* __restrict__ part) {
     constexpr int HD = 128;
     static_assert(G <= 16, "query heads per KV head");
+    static_assert(kDecodeChunk <= 64, "one page id per lane");
     const int g = blockIdx.y;
     const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
-    // this wave's work items: lanes[x] .. lanes[x + 1] of the item list that
-    // follows the gridDim.x + 1 offsets
-    const int32_t* items = lanes + gridDim.x + 1;
-    const int j1 = lanes[blockIdx.x + 1];
-    for (int j = lanes[blockIdx.x]; j < j1; ++j) {
-        const int wi = items[j];
-        const int r = work[2 * wi], c = work[2 * wi + 1];
+    const int j0 = lanes[blockIdx.x], j1 = lanes[blockIdx.x + 1];   // this wave's pieces
+
+    // Partial records are staged in LDS and stored with full-wave 16-byte
+    // non-temporal stores after the next piece's first page loads are
+    // issued.  Storing them straight from the accumulators (nine partial-wave
+    // stores, whose registers the next piece overwrites at once) stalled the
+    // wave behind the saturated read stream: measured 1.52 against 1.455 ms
+    // for the configuration-3 step's attention.
+    __shared__ __attribute__((aligned(16))) float stage[G * kDecodeRec];
+    constexpr int RCH = G * kDecodeRec / 4;             // 16-byte chunks of a record block
+    int staged = -1;                                    // segment whose record sits in `stage`
+    auto flush = [&]() {
+        const f32x4* src = reinterpret_cast<const f32x4*>(stage);
+        f32x4* dst = reinterpret_cast<f32x4*>(part + ((int64_t)staged * n_kv + g) * G * kDecodeRec);
+#pragma unroll
+        for (int k = 0; k < (RCH + 63) / 64; ++k) {
+            const int ch = lane + 64 * k;
+            if (ch < RCH) __builtin_nontemporal_store(src[ch], dst + ch);
+        }
+        staged = -1;
+    };
+
+    float m = -INFINITY, l = 0.f;
+    f32x4 o[HD / 16];
+    int seg = -1;
+    for (int j = j0; j < j1; ++j) {
+        const int r = work[4 * j], p0 = work[4 * j + 1], p1 = work[4 * j + 2];
+        if (work[4 * j + 3] != seg) {                   // a new segment: fresh softmax state
+            seg = work[4 * j + 3];
+            m = -INFINITY;
+            l = 0.f;
+#pragma unroll
+            for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
         const int slot = req_slot[r];
         const int nkeys = req_start[r] + 1;            // cached keys plus the new token's
-        const int npages = (nkeys + 15) / 16;
-        const int p0 = c * chunk, p1 = min(npages, p0 + chunk);   // chunk <= kDecodeChunk
 
         bf16x8 qb[HD / 32];
         {
@@ -472,15 +502,10 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
                 qb[b] = __builtin_bit_cast(bf16x8, v);
             }
         }
-        float m = -INFINITY, l = 0.f;
-        f32x4 o[HD / 16];
-#pragma unroll
-        for (int cb = 0; cb < HD / 16; ++cb) o[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        // the chunk's page ids, one per lane, fetched up front so the K/V loads of
+        // the piece's page ids, one per lane, fetched up front so the K/V loads of
         // a page never wait on its page-table entry
         const int32_t* prow = page_table + (int64_t)slot * max_pages;
-        static_assert(kDecodeChunk <= 64, "one page id per lane");
         const int my_page = (p0 + lane < p1) ? prow[p0 + lane] : 0;
         // PPI pages per iteration: their K/V fragments for the next iteration are
         // loaded before this iteration's pages are used (2 * PPI pages in flight)
@@ -562,6 +587,7 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
         };
 #pragma unroll
         for (int u = 0; u < PPI; ++u) load_page(p0 + u, kc[u], vc[u]);
+        if (staged >= 0) flush();
         for (int pi = p0; pi < p1; pi += PPI) {
             if (pi + PPI < p1) {
 #pragma unroll
@@ -580,28 +606,32 @@ attn_decode_mfma(const bf16_t* q, int64_t ldq, const int32_t* work, const int32_
                 }
             }
         }
-        // partial record [m, l, -, -, o[0..HD)] per (work item, query head
-        // g G + col); o starts 16-byte aligned
-        if (col < G) {
-            float* rec = part + (((int64_t)wi * n_kv + g) * G + col) * kDecodeRec;
-            if (grp == 0) { rec[0] = m; rec[1] = l; }
+        // at the segment's end, its record [m, l, -, -, o[0..HD)] per query head
+        // g G + col (o 16-byte aligned) goes to the staging area
+        if (j + 1 == j1 || work[4 * (j + 1) + 3] != seg) {
+            if (col < G) {
+                float* rec = stage + col * kDecodeRec;
+                if (grp == 0) { rec[0] = m; rec[1] = l; }
 #pragma unroll
-            for (int cb = 0; cb < HD / 16; ++cb) *reinterpret_cast<f32x4*>(rec + 4 + 16 * cb + 4 * grp) = o[cb];
+                for (int cb = 0; cb < HD / 16; ++cb) *reinterpret_cast<f32x4*>(rec + 4 + 16 * cb + 4 * grp) = o[cb];
+            }
+            staged = seg;
         }
     }
+    if (staged >= 0) flush();
 }
 
-// Merge of a request's chunk partials, in chunk order (deterministic).
-// Grid (n_req, ceil(n_q / 8)), 256 threads: 32 threads per query head, 4
-// channels each.  The chunks' maxima give the common reference M; chunk c's
-// o and l enter with weight 2^(m_c - M).
+// Merge of a request's segment partials, in segment (page) order
+// (deterministic).  Grid (n_req, ceil(n_q / 8)), 256 threads: 32 threads per
+// query head, 4 channels each.  The segments' maxima give the common
+// reference M; segment c's o and l enter with weight 2^(m_c - M).
 __global__ void __launch_bounds__(256)
-attn_decode_combine(const int32_t* cu_chunks, const float* part, int n_q, bf16_t* out, int64_t ldo,
+attn_decode_combine(const int32_t* cu_segs, const float* part, int n_q, bf16_t* out, int64_t ldo,
                     const bf16_t* gate, int64_t ldg) {
     constexpr int HD = 128;
     const int r = blockIdx.x, h = blockIdx.y * 8 + (threadIdx.x >> 5), ch = (threadIdx.x & 31) * 4;
     if (h >= n_q) return;
-    const int c0 = cu_chunks[r], c1 = cu_chunks[r + 1];
+    const int c0 = cu_segs[r], c1 = cu_segs[r + 1];
     float M = -INFINITY;
     for (int c = c0; c < c1; ++c) M = fmaxf(M, part[((int64_t)c * n_q + h) * kDecodeRec]);
     float L = 0.f;
@@ -703,64 +733,68 @@ void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void*
 #undef OUTLETS_PF_G
 }
 
-int attn_decode_chunk_pages() { return kDecodeChunk; }
-
-// Pages per decode work item: kDecodeChunk, halved (down to 16) while the
-// work items of the step fill fewer than two waves per CU over the KV heads,
-// so that small batches still spread over the chip (pages[i] = cached pages
-// of request i after the step's token).
-int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus) {
-    int chunk = kDecodeChunk;
-    while (chunk > 16) {
-        int64_t items = 0;
-        for (int i = 0; i < n_req; ++i) items += (pages[i] + chunk - 1) / chunk;
-        if (items * n_kv >= 2LL * cus) break;
-        chunk /= 2;
-    }
-    return chunk;
-}
 int attn_decode_record_floats() { return kDecodeRec; }
 
-// Each decode wave (per KV head) walks a list of work items, so the stores of
-// an item's partial record overlap the next item's page loads; only its last
-// item's stores delay the wave's exit.  (One short-lived wave per item spent
-// a store round trip per item at its exit, which under the saturated read
-// stream measured ~10% of the kernel's time.)  Lists are balanced by pages:
-// items longest first, each to the list with the fewest pages so far.
-int attn_decode_lanes(int n_work, const int32_t* item_pages, int n_kv, int cus, std::vector<int32_t>* out) {
-    // two waves per SIMD (the kernel's registers allow two), four SIMDs per CU
-    const int n_lanes = std::max(1, std::min(n_work, 8 * cus / std::max(1, n_kv)));
-    std::vector<int32_t> order(n_work);
-    for (int i = 0; i < n_work; ++i) order[i] = i;
-    std::stable_sort(order.begin(), order.end(),
-                     [&](int32_t a, int32_t b) { return item_pages[a] > item_pages[b]; });
-    typedef std::pair<int64_t, int32_t> Load;   // (pages so far, lane)
-    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-    for (int l = 0; l < n_lanes; ++l) heap.push(Load(0, l));
-    std::vector<int32_t> lane_of(n_work), count(n_lanes, 0);
-    for (int32_t it : order) {
-        Load top = heap.top();
-        heap.pop();
-        lane_of[it] = top.second;
-        count[top.second] += 1;
-        heap.push(Load(top.first + item_pages[it], top.second));
-    }
-    out->assign(n_lanes + 1 + n_work, 0);
-    int32_t* off = out->data();
-    for (int l = 0; l < n_lanes; ++l) off[l + 1] = off[l] + count[l];
-    std::vector<int32_t> fill(off, off + n_lanes);
-    int32_t* items = off + n_lanes + 1;
-    for (int32_t it : order) items[fill[lane_of[it]]++] = it;   // longest first within a list
-    return n_lanes;
+// Lists of the decode waves (per KV head): at most two waves per SIMD (the
+// kernel's registers allow two), and at least ~16 pages per wave so that the
+// per-piece fixed costs stay small next to the page stream.
+static int64_t decode_lane_count(int64_t pages, int n_kv, int cus) {
+    const int64_t cap = std::max<int64_t>(1, 8LL * cus / std::max(1, n_kv));
+    return std::max<int64_t>(1, std::min<int64_t>(cap, (pages + 15) / 16));
 }
 
-void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
-                        int n_lanes, const int32_t* lanes,
-                        const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
-                        const int32_t* req_start, const int32_t* page_table, int max_pages,
+int64_t attn_decode_max_segments(int64_t max_req, int n_kv, int cus) {
+    return max_req + std::max<int64_t>(1, 8LL * cus / std::max(1, n_kv));
+}
+
+int64_t attn_decode_max_pieces(int64_t max_req, int64_t max_pages, int n_kv, int cus) {
+    return max_req * ((max_pages + kDecodeChunk - 1) / kDecodeChunk) + attn_decode_max_segments(max_req, n_kv, cus);
+}
+
+// The step's pages, requests in order, cut into L ranges whose lengths differ
+// by at most one page; a range's part in one request is a segment (one
+// partial record), walked in pieces of at most kDecodeChunk pages.  Segments
+// are numbered in page order, so each request's segments are consecutive and
+// in order.  A segment count of at most L + n_req and a piece count of at most
+// pages / kDecodeChunk + segments follow.
+void attn_decode_plan(int n_req, const int32_t* pages, int n_kv, int cus, DecodePlan* plan) {
+    plan->work.clear();
+    plan->lanes.clear();
+    plan->cu_segs.assign(n_req + 1, 0);
+    std::vector<int64_t> cum(n_req + 1, 0);
+    for (int i = 0; i < n_req; ++i) cum[i + 1] = cum[i] + pages[i];
+    const int64_t P = cum[n_req];
+    const int64_t L = decode_lane_count(P, n_kv, cus);
+    plan->n_lanes = static_cast<int>(L);
+    plan->lanes.reserve(L + 1);
+    int r = 0, n_segs = 0;
+    for (int64_t ln = 0; ln < L; ++ln) {
+        plan->lanes.push_back(static_cast<int32_t>(plan->work.size() / 4));
+        int64_t g = P * ln / L;
+        const int64_t e = P * (ln + 1) / L;
+        while (g < e) {
+            while (cum[r + 1] <= g) ++r;                // the request holding global page g
+            if (cum[r] == g) plan->cu_segs[r] = n_segs; // its first segment
+            const int64_t se = std::min(e, cum[r + 1]);
+            for (int64_t p = g - cum[r]; p < se - cum[r]; p += kDecodeChunk) {
+                const int64_t pe = std::min<int64_t>(se - cum[r], p + kDecodeChunk);
+                plan->work.insert(plan->work.end(), {r, static_cast<int32_t>(p), static_cast<int32_t>(pe), n_segs});
+            }
+            ++n_segs;
+            g = se;
+        }
+    }
+    plan->lanes.push_back(static_cast<int32_t>(plan->work.size() / 4));
+    plan->cu_segs[n_req] = n_segs;
+    plan->n_segs = n_segs;
+}
+
+void launch_attn_decode(int n_req, int n_pieces, const int32_t* work, const int32_t* cu_segs, int n_lanes,
+                        const int32_t* lanes, const void* q, int64_t ldq, void* out, int64_t ldo,
+                        const int32_t* req_slot, const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
                         const void* gate, hipStream_t st) {
-    if (n_req <= 0 || n_work <= 0 || n_lanes <= 0) return;
+    if (n_req <= 0 || n_pieces <= 0 || n_lanes <= 0) return;
     const int G = n_q / n_kv;
     const float qscale = 1.4426950408889634f / sqrtf(128.0f);
 #define OUTLETS_DEC_G(GG)                                                                          \
@@ -768,7 +802,7 @@ void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, c
         hipLaunchKernelGGL((attn_decode_mfma<GG>), dim3(n_lanes, n_kv), dim3(64), 0, st,           \
                            static_cast<const bf16_t*>(q), ldq, work, lanes, req_slot, req_start,   \
                            page_table, max_pages, static_cast<const bf16_t*>(kpool),               \
-                           static_cast<const bf16_t*>(vpool), n_kv, qscale, part, chunk);          \
+                           static_cast<const bf16_t*>(vpool), n_kv, qscale, part);                 \
         break;
     switch (G) {
         OUTLETS_DEC_G(1)
@@ -777,7 +811,7 @@ void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, c
         OUTLETS_DEC_G(8)
     }
 #undef OUTLETS_DEC_G
-    hipLaunchKernelGGL(attn_decode_combine, dim3(n_req, (n_q + 7) / 8), dim3(256), 0, st, cu_chunks, part, n_q,
+    hipLaunchKernelGGL(attn_decode_combine, dim3(n_req, (n_q + 7) / 8), dim3(256), 0, st, cu_segs, part, n_q,
                        static_cast<bf16_t*>(out), ldo, static_cast<const bf16_t*>(gate), ldq);
 }
 

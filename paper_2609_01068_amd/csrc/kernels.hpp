@@ -163,22 +163,25 @@ void launch_attn_prefill(int n_work, const int32_t* work, int qtile, const void*
                          const int32_t* page_table, int max_pages, const void* kpool,
                          const void* vpool, int n_q, int n_kv, const void* gate, hipStream_t st);
 
-// Decode attention (bf16, hd 128, one query per request, split over chunks of
-// attn_decode_chunk_pages() pages): work[2 i], work[2 i + 1] = (request, chunk);
-// cu_chunks[n_req + 1] = first work item of each request; part = fp32 scratch
-// [n_work, n_q, attn_decode_record_floats()].  Queries are row r of q for
-// request r.
-int attn_decode_chunk_pages();   // the largest chunk
-int attn_decode_chunk_for(int n_req, const int32_t* pages, int n_kv, int cus);
+// Decode attention (bf16, hd 128, one query per request).  The step's pages,
+// requests in order, are cut into n_lanes equal ranges, one per wave and KV
+// head; a range's part in one request is a segment (one fp32 partial record
+// per segment and query head), walked in pieces of at most 64 pages.
+// DecodePlan: work[4 i .. 4 i + 3] = (request, first page, end page, segment)
+// of piece i; lanes = n_lanes + 1 piece offsets; cu_segs[n_req + 1] = first
+// segment of each request; part = fp32 scratch [n_segs, n_q,
+// attn_decode_record_floats()].  Queries are row r of q for request r.
+struct DecodePlan {
+    std::vector<int32_t> work, cu_segs, lanes;
+    int n_lanes = 0, n_segs = 0;
+};
+void attn_decode_plan(int n_req, const int32_t* pages, int n_kv, int cus, DecodePlan* plan);
+int64_t attn_decode_max_segments(int64_t max_req, int n_kv, int cus);
+int64_t attn_decode_max_pieces(int64_t max_req, int64_t max_pages, int n_kv, int cus);
 int attn_decode_record_floats();
-// Work lists of the decode waves: returns the list count L and fills `out`
-// with L + 1 offsets followed by the n_work item indices (balanced by
-// item_pages[i], the pages of item i).
-int attn_decode_lanes(int n_work, const int32_t* item_pages, int n_kv, int cus, std::vector<int32_t>* out);
-void launch_attn_decode(int n_req, int n_work, int chunk, const int32_t* work, const int32_t* cu_chunks,
-                        int n_lanes, const int32_t* lanes,
-                        const void* q, int64_t ldq, void* out, int64_t ldo, const int32_t* req_slot,
-                        const int32_t* req_start, const int32_t* page_table, int max_pages,
+void launch_attn_decode(int n_req, int n_pieces, const int32_t* work, const int32_t* cu_segs, int n_lanes,
+                        const int32_t* lanes, const void* q, int64_t ldq, void* out, int64_t ldo,
+                        const int32_t* req_slot, const int32_t* req_start, const int32_t* page_table, int max_pages,
                         const void* kpool, const void* vpool, int n_q, int n_kv, float* part,
                         const void* gate, hipStream_t st);
 

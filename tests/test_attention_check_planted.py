@@ -6,7 +6,7 @@ prefill and decode step (gpu_common.check_attention).  Here plausible
 kernel faults are planted in the oracle's attention and the same check is
 run against the correct oracle: each fault must fail it.  The cases are
 those of the GPU tests: the reduced bf16 shape with caches of 1,100 / 600 /
-40 tokens (decode work items of 16 pages = 256 keys), and the 8B shape with
+40 tokens (decode ranges of ~16 pages = 256 keys), and the 8B shape with
 caches of 600 / 40 tokens.  On these cases the h_draft and z checks alone
 let several of these faults through (the residual stream dominates
 h_draft), which is why the attention output is compared directly.
@@ -20,7 +20,7 @@ import oracle.model as oracle_model
 from gpu_common import check_attention, make_case, oracle_for, oracle_states, reduced_shape, step_inputs
 
 REAL = oracle_model.causal_gqa_attention
-CHUNK = 256          # keys per decode work item at these batch sizes (16 pages)
+CHUNK = 256          # keys per decode range at these batch sizes (~16 pages)
 
 
 def _drop_first_chunk(q, k, v, q_pos, k_pos, chunk=1024):

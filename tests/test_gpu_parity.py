@@ -461,26 +461,34 @@ def test_error_paths_leave_state_unchanged():
     pred.close()
 
 
-def test_decode_steps_over_long_caches_merge_chunks():
-    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (16-page = 256-key chunks), 3 steps")
+def test_decode_steps_over_long_caches_merge_segments():
+    """Caches of 69, 38 and 3 pages: the step's ~16-page ranges split the
+    first request over five ranges (five partial records merged)."""
+    say("case: bf16 d=512 8q/2kv hd128, caches of 1100/600/40 tokens (~16-page decode ranges), 3 steps")
     case = make_case(1, lens=[1100, 600, 40], shape=reduced_shape(), n_req=3)
     _run_prefill_case(case, keep=False, steps=3, check_intermediates=False)
 
 
-@pytest.mark.parametrize("n_req,chunk_pages", [(100, 32), (160, 64)])
-def test_decode_chunk_sizes_against_oracle(n_req, chunk_pages):
-    """bf16 d=512 8q/2kv hd128: n_req caches of 1,030..1,100 tokens (65..69
-    pages), so the step's split-KV work items take 32-page chunks (100
-    requests: 64-page chunks would give fewer than two waves per CU) or
-    64-page chunks (160 requests), two or three chunks per request merged by
-    the combine kernel.  Two steps; the oracle recomputes sampled requests:
-    attention output, h_draft and z of every step."""
-    lens = [1030 + (37 * i) % 71 for i in range(n_req)]
+DECODE_PLAN_CASES = {
+    # every request over four or five ranges
+    "long_caches": lambda n: [1030 + (37 * i) % 71 for i in range(n)],
+    # several requests inside each range: segments that end mid-piece
+    "short_caches": lambda n: [20 + (29 * i) % 41 for i in range(n)],
+}
+
+
+@pytest.mark.parametrize("kind,n_req", [("long_caches", 100), ("short_caches", 300)])
+def test_decode_plan_shapes_against_oracle(kind, n_req):
+    """bf16 d=512 8q/2kv hd128, two decode steps: the step's pages are cut
+    into equal ranges (one wave per range and KV head) whose parts in each
+    request are merged by the combine kernel.  The oracle recomputes sampled
+    requests: attention output, h_draft and z of every step."""
+    lens = DECODE_PLAN_CASES[kind](n_req)
     case = make_case(1, lens=lens, shape=reduced_shape(), n_req=n_req)
     sample = sorted({0, 1, n_req // 2, n_req - 1, int(np.argmax(lens)), int(np.argmin(lens))})
-    say(f"case: bf16 reduced shape, {n_req} caches of 1030..1100 tokens ({chunk_pages}-page decode chunks), "
+    say(f"case: bf16 reduced shape, {n_req} caches of {min(lens)}..{max(lens)} tokens ({kind}), "
         f"2 steps, oracle on {sample}")
-    pred = make_predictor(case, max_seq_len=1100 + 16)
+    pred = make_predictor(case, max_seq_len=max(lens) + 16)
     slots = list(range(n_req))
     pred.prefill(slots, case.lens, *device_states(case))
     orc = oracle_for(case)

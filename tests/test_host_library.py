@@ -60,6 +60,75 @@ def test_varlen_meta_rejects_empty_prompt(lib):
     assert e.value.rc == B.OUTLETS_ERR_INVALID_ARG
 
 
+def _check_decode_plan(pages, n_kv, cus):
+    """The plan's defining properties: the step's pages (requests in order)
+    cut into L contiguous ranges of equal length (+-1); each range's part in
+    one request is one segment; segments numbered in page order; pieces of
+    at most 64 pages cover every page exactly once."""
+    work, cu, lanes = B.outlets_decode_plan(pages, n_kv, cus)
+    n, P = len(pages), int(sum(pages))
+    L = len(lanes) - 1
+    assert 1 <= L <= max(1, 8 * cus // n_kv) and L <= max(1, -(-P // 16))
+    assert lanes[0] == 0 and lanes[-1] == len(work) and all(a <= b for a, b in zip(lanes, lanes[1:]))
+    start = np.concatenate([[0], np.cumsum(pages)])
+    covered = np.zeros(P, dtype=np.int64)
+    seg_req, seg_pages = {}, {}
+    for ln in range(L):
+        lo, hi = P * ln // L, P * (ln + 1) // L
+        pos = lo
+        for (r, p0, p1, s) in work[lanes[ln]:lanes[ln + 1]]:
+            assert 0 <= r < n and 0 <= p0 < p1 <= pages[r] and p1 - p0 <= 64
+            assert start[r] + p0 == pos, "pieces of a range are contiguous and in order"
+            covered[start[r] + p0:start[r] + p1] += 1
+            pos = start[r] + p1
+            assert seg_req.setdefault(s, (r, ln)) == (r, ln), "a segment is one request within one range"
+            seg_pages.setdefault(s, []).append((p0, p1))
+        assert pos == hi
+    assert np.all(covered == 1)
+    n_segs = len(seg_req)
+    assert sorted(seg_req) == list(range(n_segs)) and n_segs <= L + n
+    # segments in page order: request-major, consecutive per request
+    assert [seg_req[s][0] for s in range(n_segs)] == sorted(seg_req[s][0] for s in range(n_segs))
+    assert cu[0] == 0 and cu[-1] == n_segs
+    for r in range(n):
+        segs = [s for s in range(n_segs) if seg_req[s][0] == r]
+        assert segs == list(range(cu[r], cu[r + 1])) and segs
+    # a range holds as many segments as requests it touches
+    for ln in range(L):
+        lo, hi = P * ln // L, P * (ln + 1) // L
+        touched = np.unique(np.searchsorted(start, np.arange(lo, hi), side="right") - 1)
+        assert len({s for (_, _, _, s) in work[lanes[ln]:lanes[ln + 1]]}) == len(touched)
+    assert len(work) <= P // 64 + n_segs
+    return work, cu, lanes
+
+
+def test_decode_plan_ranges_segments_and_pieces(lib):
+    r = np.random.default_rng(11)
+    cases = [([1], 8, 256), ([3, 1, 2], 8, 256), ([600] * 3, 8, 256), ([1] * 700, 8, 256),
+             ([1000, 1, 1, 513], 1, 4), ([64, 65, 127, 128, 129], 2, 16)]
+    for _ in range(40):
+        n = int(r.integers(1, 300))
+        cases.append((list(r.integers(1, 600, size=n)), int(r.choice([1, 2, 8])), int(r.choice([1, 4, 80, 256]))))
+    for pages, n_kv, cus in cases:
+        _check_decode_plan(pages, n_kv, cus)
+
+
+def test_decode_plan_at_the_512_request_step_shape(lib):
+    # caches of U[256, 8192] tokens plus the new one, 16-token pages
+    r = np.random.default_rng(5)
+    pages = [(int(x) + 1 + 15) // 16 for x in r.integers(256, 8193, size=512)]
+    work, cu, lanes = _check_decode_plan(pages, 8, 256)
+    assert len(lanes) - 1 == 256
+    assert cu[-1] <= 256 + 512
+
+
+def test_decode_plan_rejects_bad_sizes(lib):
+    for pages in ([], [2, 0, 1], [-3]):
+        with pytest.raises(B.OutletsError) as e:
+            B.outlets_decode_plan(pages, 8, 256)
+        assert e.value.rc == B.OUTLETS_ERR_INVALID_ARG
+
+
 def _compare(p, o):
     assert p.read(B.OUTLETS_META_PAGE_TABLE) == list(o.table().reshape(-1))
     assert p.read(B.OUTLETS_META_SEQ_LEN) == list(o.seq_lens())
