@@ -554,15 +554,17 @@ int upload_meta(outlets_ctx* c, const CallBufs& b, int n, const std::vector<int3
     if (!cu_tiles.empty()) std::memcpy(h + c->tiles_off, cu_tiles.data(), sizeof(int32_t) * cu_tiles.size());
     c->lanes_off = c->tiles_off + static_cast<int64_t>(cu_tiles.size());
     if (!lanes.empty()) std::memcpy(h + c->lanes_off, lanes.data(), sizeof(int32_t) * lanes.size());
-    HIP_TRY(hipMemcpyAsync(b.d_meta, h, sizeof(int32_t) * count, hipMemcpyHostToDevice, st), "hipMemcpyAsync");
+    {
+        // one kernel reads the staged block from host memory (no copy-engine
+        // transfer on the call's critical path), applies the page-table
+        // updates and builds the token arrays
+        KTimer t(c, OUTLETS_K_META, st);
+        launch_meta_fetch(h, static_cast<int>(count), n, static_cast<int>(updates.size() / 2), b.d_meta,
+                          c->page_table, b.tok_slot, b.tok_pos, b.last_idx, st);
+    }
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
     c->stage ^= 1;
-    KTimer t(c, OUTLETS_K_META, st);
-    if (!updates.empty())
-        launch_scatter_i32(static_cast<int>(updates.size() / 2), b.d_meta + 3 * n + 1, c->page_table, st);
-    launch_build_tokens(n, b.d_meta, b.d_meta + n + 1, b.d_meta + 2 * n + 1, b.tok_slot,
-                        b.tok_pos, b.last_idx, st);
     return OUTLETS_OK;
 }
 
@@ -886,7 +888,9 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     }
 #undef ALLOC
     for (int i = 0; i < 2; ++i) {
-        HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->cb.meta_cap, 0),
+        // host-coherent: the metadata kernel reads it in place
+        HIP_TRY(hipHostMalloc(reinterpret_cast<void**>(&c->h_stage[i]), sizeof(int32_t) * c->cb.meta_cap,
+                              hipHostMallocCoherent),
                 "hipHostMalloc");
         HIP_TRY(hipEventCreateWithFlags(&c->ev[i], hipEventDisableTiming), "hipEventCreate");
     }

@@ -98,14 +98,15 @@ int gemm_device_cus();   // compute units of the current device
 bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int n_q, int n_kv, int hd, int N);
 
 // ---------------------------------------------------------------- elementwise / rows
-// Per-call token metadata from per-request arrays:
-//   req[0..n]      : token offsets (cu), req_off
-//   req_slot[n], req_start[n] (first position of the call's tokens)
-// writes tok_slot[T], tok_pos[T], last_idx[n].
-void launch_build_tokens(int n_req, const int32_t* req_off, const int32_t* req_slot,
-                         const int32_t* req_start, int32_t* tok_slot, int32_t* tok_pos,
-                         int32_t* last_idx, hipStream_t st);
-void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStream_t st);
+// A call's metadata block from pinned host-coherent memory (`host_meta`,
+// `count` int32: req_off[n + 1] | req_slot[n] | req_start[n] | n_pairs
+// (index, page) pairs | the rest) into d_meta; applies the pairs to
+// page_table and writes tok_slot[T] (slot of each token), tok_pos[T]
+// (req_start + index within the request) and last_idx[n] (row of each
+// request's newest token).  The host must not rewrite host_meta until the
+// kernel has run.
+void launch_meta_fetch(const int32_t* host_meta, int count, int n_req, int n_pairs, int32_t* d_meta,
+                       int32_t* page_table, int32_t* tok_slot, int32_t* tok_pos, int32_t* last_idx, hipStream_t st);
 
 // Row x[r] of a split-K GEMM's output: the S partial planes summed in split
 // order, plus resid[r] when resid is set (the fp32 residual the GEMM's

@@ -1,6 +1,8 @@
 // Row-wise kernels of the draft layer and the length head (HBM-bound):
 // per-call token metadata, RMSNorm, rotary embedding + paged KV write,
 // segmented mean/last pooling and the head's ReLU + final dot product.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -8,22 +10,34 @@ namespace outlets {
 
 namespace {
 
-__global__ void build_tokens_kernel(const int32_t* req_off, const int32_t* req_slot,
-                                    const int32_t* req_start, int32_t* tok_slot,
-                                    int32_t* tok_pos, int32_t* last_idx) {
-    const int i = blockIdx.x;
-    const int b = req_off[i], e = req_off[i + 1];
-    const int slot = req_slot[i], start = req_start[i];
-    for (int t = b + threadIdx.x; t < e; t += blockDim.x) {
-        tok_slot[t] = slot;
-        tok_pos[t] = start + (t - b);
+// The call's metadata block, written by the host into pinned host-coherent
+// memory, copied into device memory together with the two things later
+// kernels need from it first: the page-table updates (the (index, page)
+// pairs after req_off | req_slot | req_start) and the per-token slot and
+// position arrays.  One launch instead of a copy-engine transfer, whose
+// completion the compute queue would wait on, and two kernels.  `host` is
+// read with vector loads (it is not restrict-qualified), so nothing of it is
+// kept in the scalar cache.
+__global__ void __launch_bounds__(256)
+meta_fetch_kernel(const int32_t* host, int count, int n_req, int n_pairs, int32_t* __restrict__ d_meta,
+                  int32_t* __restrict__ page_table, int32_t* __restrict__ tok_slot, int32_t* __restrict__ tok_pos,
+                  int32_t* __restrict__ last_idx) {
+    const int tid = blockIdx.x * blockDim.x + threadIdx.x, nth = gridDim.x * blockDim.x;
+    const int n4 = count / 4;
+    const uint4* h4 = reinterpret_cast<const uint4*>(host);
+    uint4* d4 = reinterpret_cast<uint4*>(d_meta);
+    for (int i = tid; i < n4; i += nth) d4[i] = h4[i];
+    for (int i = 4 * n4 + tid; i < count; i += nth) d_meta[i] = host[i];
+    const int32_t* pairs = host + 3 * n_req + 1;
+    for (int i = tid; i < n_pairs; i += nth) page_table[pairs[2 * i]] = pairs[2 * i + 1];
+    for (int r = blockIdx.x; r < n_req; r += gridDim.x) {
+        const int b = host[r], e = host[r + 1], slot = host[n_req + 1 + r], start = host[2 * n_req + 1 + r];
+        for (int t = b + threadIdx.x; t < e; t += blockDim.x) {
+            tok_slot[t] = slot;
+            tok_pos[t] = start + (t - b);
+        }
+        if (threadIdx.x == 0) last_idx[r] = e - 1;
     }
-    if (threadIdx.x == 0) last_idx[i] = e - 1;
-}
-
-__global__ void scatter_kernel(int n, const int32_t* pairs, int32_t* dst) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) dst[pairs[2 * i]] = pairs[2 * i + 1];
 }
 
 // One 256-thread block per row.
@@ -569,18 +583,12 @@ __global__ void copy_rows_kernel(int d, const float* src, int64_t lds, T* dst, i
 
 }  // namespace
 
-void launch_build_tokens(int n_req, const int32_t* req_off, const int32_t* req_slot,
-                         const int32_t* req_start, int32_t* tok_slot, int32_t* tok_pos,
-                         int32_t* last_idx, hipStream_t st) {
-    if (n_req <= 0) return;
-    hipLaunchKernelGGL(build_tokens_kernel, dim3(n_req), dim3(256), 0, st, req_off, req_slot,
-                       req_start, tok_slot, tok_pos, last_idx);
-}
-
-void launch_scatter_i32(int n_pairs, const int32_t* pairs, int32_t* dst, hipStream_t st) {
-    if (n_pairs <= 0) return;
-    hipLaunchKernelGGL(scatter_kernel, dim3((n_pairs + 255) / 256), dim3(256), 0, st, n_pairs,
-                       pairs, dst);
+void launch_meta_fetch(const int32_t* host_meta, int count, int n_req, int n_pairs, int32_t* d_meta,
+                       int32_t* page_table, int32_t* tok_slot, int32_t* tok_pos, int32_t* last_idx, hipStream_t st) {
+    if (count <= 0) return;
+    const int blocks = std::max(1, std::max(n_req, (count / 4 + 255) / 256));
+    hipLaunchKernelGGL(meta_fetch_kernel, dim3(blocks), dim3(256), 0, st, host_meta, count, n_req, n_pairs, d_meta,
+                       page_table, tok_slot, tok_pos, last_idx);
 }
 
 bool rowsum_supported(int d) { return d == 1024 || d == 2048 || d == 4096 || d == 8192; }
