@@ -145,7 +145,7 @@ def weight_bytes(W) -> float:
 
 
 def measure_decode(seed: int, steps: int, warmup: int, attn_gate: bool = False):
-    """Dynamic re-prediction at scale (configuration 3): 512 in-flight
+    """Dynamic re-prediction at scale: 512 in-flight
     requests whose paged draft KV caches hold U[256, 8192] prompt tokens
     (filled by untimed prefill calls), then ``steps`` timed decode steps of
     one new token per request.  Returns the measurement as a dict."""
@@ -228,7 +228,7 @@ def measure_decode(seed: int, steps: int, warmup: int, attn_gate: bool = False):
 
 
 def bench_decode(a):
-    """The configuration-3 decode steps as the bench line itself."""
+    """The 512-request decode steps as the bench line itself."""
     m = measure_decode(a.seed, a.steps, a.warmup, a.attn_gate)
     out = {
         "metric": METRIC, "value": m["draft_tokens_per_s"], "unit": "draft tokens/s (request-steps/s)",
@@ -326,7 +326,7 @@ def bench_prefill(a, cfg_id):
 
 
 def bench_probe(a):
-    """The MLP-probe baseline on the config-1 batch: probe prefill over the
+    """The MLP-probe baseline on the 32-request 8B batch: probe prefill over the
     mid-depth target state of 32 requests + one probe step + release."""
     import torch
     from paper_2609_01068_amd.predictor import OutletsPredictor, to_device
@@ -372,7 +372,7 @@ def bench_probe(a):
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; lognormal prompt lengths; N(0,1) x 4 mid-depth target states drawn on device)",
-        "config": {"workload": "MLP-probe baseline on the 8B config-1 batch: 32 requests, probe prefill on the "
+        "config": {"workload": "MLP-probe baseline on the 32-request 8B batch: probe prefill on the "
                                "mid-depth state + one probe step per request", "requests": B, "prompt_tokens": T,
                    "d": wl.shape.d, "head_hidden": wl.shape.head_hidden},
         "roofline": {"kernel": "probe call (pooling + head), whole step", "bound": "hbm", "achieved": achieved,
@@ -460,9 +460,9 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--decode-steps", type=int, default=20,
-                    help="prefill-8b: timed configuration-3 decode steps reported under decode_step")
+                    help="prefill-8b: timed 512-request decode steps reported under decode_step")
     ap.add_argument("--no-decode", action="store_true",
-                    help="prefill-8b: skip the configuration-3 decode-step measurement")
+                    help="prefill-8b: skip the 512-request decode-step measurement")
     ap.add_argument("--workload", default="prefill-8b",
                     choices=["prefill-8b", "decode-8b", "prefill-8b-large", "prefill-70b-e4m3", "probe-8b",
                              "sched-1p3d"],
@@ -470,7 +470,7 @@ def main(argv=None):
                          "in-flight requests with 256..8192 cached tokens, timed decode steps; "
                          "prefill-8b-large: 256 requests (~466k tokens) in one call; "
                          "prefill-70b-e4m3: 70B shape with e4m3 weights, 64 requests; probe-8b: the "
-                         "MLP-probe baseline on the config-1 batch; sched-1p3d: the LB + SJF control "
+                         "MLP-probe baseline on the 32-request 8B batch; sched-1p3d: the LB + SJF control "
                          "plane on the 1,914-request saturation trace (host only)")
     ap.add_argument("--attn-gate", action="store_true",
                     help="draft layer with the Gated Attention output gate (Section 4.1)")
@@ -623,7 +623,7 @@ def main(argv=None):
     pred.close()
     del H, S
     if not a.no_decode:
-        # the decode-step half of the metric (configuration 3: 512 in-flight
+        # the decode-step half of the metric (512 in-flight
         # requests, HBM-bound): ms per step, draft tokens/s, the attention
         # kernel's and the whole step's fraction of the HBM peak
         m = measure_decode(a.seed, a.decode_steps, a.warmup, a.attn_gate)

@@ -77,13 +77,13 @@ def _sample(lens, *quantiles):
 
 
 @pytest.mark.timeout(900)
-def test_config2_saturated_prefill_256_requests():
+def test_8b_256_request_prefill_in_one_call():
     from oracle import oracle_from_workload
     from synth import make_lengths, make_weights, workload
     wl = workload(2)
     lens = make_lengths(wl)
     sample = _sample(lens, 0.25)
-    say(f"case: config-2 8B bf16, B={len(lens)}, T={int(lens.sum())} in one call, oracle on requests {sample} "
+    say(f"case: 8B bf16 256-request batch, B={len(lens)}, T={int(lens.sum())} in one call, oracle on requests {sample} "
         f"(lengths {[int(lens[i]) for i in sample]}; longest request {int(lens.max())})")
     W = make_weights(wl)
     got = _gpu_prefill_sample(wl, W, lens, sample)
@@ -95,8 +95,8 @@ def test_config2_saturated_prefill_256_requests():
 
 
 @pytest.fixture(scope="module")
-def config4():
-    """Config 4 (70B shape, e4m3 weights): the whole 64-request batch in one
+def batch_70b_e4m3():
+    """70B shape with e4m3 weights: the whole 64-request batch in one
     prefill call on the GPU; the sampled requests' outputs kept on the host
     with the oracle built from the same weights."""
     from oracle import oracle_from_workload
@@ -104,7 +104,7 @@ def config4():
     wl = workload(4)
     lens = make_lengths(wl)
     sample = _sample(lens)
-    say(f"case: config-4 70B e4m3 weights, B={len(lens)}, T={int(lens.sum())} in one call, oracle on "
+    say(f"case: 70B e4m3 64-request batch, B={len(lens)}, T={int(lens.sum())} in one call, oracle on "
         f"requests {sample} (lengths {[int(lens[i]) for i in sample]}; longest request {int(lens.max())})")
     W = make_weights(wl)
     say("  weights generated")
@@ -116,16 +116,16 @@ def config4():
 
 
 @pytest.mark.timeout(900)
-def test_config4_70b_e4m3_shortest_request(config4):
-    c = config4
+def test_70b_e4m3_batch_shortest_request(batch_70b_e4m3):
+    c = batch_70b_e4m3
     c["z_ref"].update(_oracle_check(c["orc"], c["wl"], c["lens"], c["sample"], c["got"], "e4m3", [0]))
 
 
 @pytest.mark.timeout(900)
-def test_config4_70b_e4m3_longest_request(config4):
+def test_70b_e4m3_batch_longest_request(batch_70b_e4m3):
     """The 16,384-token prompt (the configuration's clip): attention over
     256 64-key tiles per query tile, two-block work items."""
-    c = config4
+    c = batch_70b_e4m3
     last = len(c["sample"]) - 1
     c["z_ref"].update(_oracle_check(c["orc"], c["wl"], c["lens"], c["sample"], c["got"], "e4m3", [last]))
     if 0 not in c["z_ref"]:
@@ -137,7 +137,7 @@ def test_config4_70b_e4m3_longest_request(config4):
 
 
 @pytest.mark.timeout(900)
-def test_config3_decode_512_slots_long_caches():
+def test_decode_512_slots_long_caches():
     """512 slots with U[256, 8192] cached tokens (64-page decode chunks);
     three steps; the oracle follows the shortest cache, one of several
     chunks and the longest cache (eight 64-page chunks merged)."""
@@ -150,7 +150,7 @@ def test_config3_decode_512_slots_long_caches():
     B = len(lens)
     sample = _sample(lens, 0.125)
     steps = 3
-    say(f"case: config-3 8B bf16, {B} slots, {int(lens.sum())} cached tokens, {steps} steps, oracle on slots "
+    say(f"case: 8B bf16 decode, {B} slots, {int(lens.sum())} cached tokens, {steps} steps, oracle on slots "
         f"{sample} (caches {[int(lens[i]) for i in sample]}; longest cache {int(lens.max())})")
     W = make_weights(wl)
     chunk = 48

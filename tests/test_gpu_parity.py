@@ -141,7 +141,7 @@ def test_bf16_head_dim_64_shape():
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("variant", ["plain", "gated", "embed"])
-def test_config1_full_shape_sampled_requests(variant):
+def test_8b_32_request_batch_sampled_requests(variant):
     """8B shape, the 32-request lognormal batch (also with the Gated Attention
     output gate, and with EAGLE-3 input embeddings over the 128,256-entry
     vocabulary), prefill and one decode step of every request as the
@@ -153,7 +153,7 @@ def test_config1_full_shape_sampled_requests(variant):
     B_ = len(lens)
     order = np.argsort(lens, kind="stable")
     sample = sorted({int(order[0]), int(order[1]), int(order[B_ // 3]), int(order[-1])})
-    say(f"case: config-1 8B bf16 ({variant}), B={B_}, T={int(lens.sum())}, oracle on requests {sample} "
+    say(f"case: 8B bf16 32-request batch ({variant}), B={B_}, T={int(lens.sum())}, oracle on requests {sample} "
         f"(lengths {[int(lens[i]) for i in sample]}; longest request {int(lens.max())})")
     pred = make_predictor(case, max_seq_len=int(lens.max()) + 16)
     H = device_states(case)
@@ -692,14 +692,14 @@ def test_draft_head_absent_without_vocab():
     pred.close()
 
 
-def test_config1_draft_head_sampled_requests():
+def test_8b_32_request_batch_draft_head_sampled_requests():
     """Eq. 2 at the 8B shape (V = 128,256) on the 32-request batch; the oracle
     recomputes two sampled requests."""
     from oracle.formats import decode_weight
     from synth import make_prompt_states
     case = _with_lm(make_case(1))
     lens = case.lens
-    say(f"case: config-1 draft model head, V={case.wl.shape.vocab}, B={len(lens)}, T={int(lens.sum())}")
+    say(f"case: 32-request 8B batch, draft model head, V={case.wl.shape.vocab}, B={len(lens)}, T={int(lens.sum())}")
     pred = make_predictor(case)
     H = device_states(case)
     pred.prefill(list(range(len(lens))), lens, *H)
