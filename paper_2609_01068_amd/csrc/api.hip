@@ -125,8 +125,8 @@ struct outlets_ctx {
     int32_t n_work = 0;
     int32_t attn_qtile = 32;       // queries per prefill attention work item of the current call
     int64_t tiles_off = 0;       // offset of cu_tiles (prefill pooling) in d_meta
-    int64_t lanes_off = 0;       // offset of the decode waves' work lists in d_meta
-    int32_t n_lanes = 0;         // decode work lists of the current call
+    int64_t lanes_off = 0;       // offset of the decode plan's range offsets in d_meta
+    int32_t n_lanes = 0;         // decode page ranges (waves per KV head) of the current call
     int32_t n_tiles = 0;
 
     int32_t* h_stage[2] = {nullptr, nullptr};

@@ -138,9 +138,11 @@ def test_70b_e4m3_batch_longest_request(batch_70b_e4m3):
 
 @pytest.mark.timeout(900)
 def test_decode_512_slots_long_caches():
-    """512 slots with U[256, 8192] cached tokens (64-page decode chunks);
-    three steps; the oracle follows the shortest cache, one of several
-    chunks and the longest cache (eight 64-page chunks merged)."""
+    """512 slots with U[256, 8192] cached tokens: the step's 137k pages cut
+    into 256 equal ranges of ~536 pages (one wave per range and KV head),
+    walked in pieces of at most 64 pages; three steps; the oracle follows
+    the shortest cache, one at the 1/8 quantile and the longest (512 pages,
+    over one or two ranges, so a segment boundary can fall inside it)."""
     import torch
     from oracle import oracle_from_workload, states_to_f64
     from synth import make_lengths, make_prompt_states, make_step_states, make_weights, workload
