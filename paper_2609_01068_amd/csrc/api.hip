@@ -1000,14 +1000,15 @@ int outlets_predict_step_noalloc(outlets_ctx* ctx, int32_t n_req, const int32_t*
 // target-model hidden state (no draft layer), with its own weights and
 // per-slot running sums.
 
-// Stage int32 metadata through the pinned double buffer into probe_meta.
+// Stage int32 metadata through the pinned double buffer into probe_meta (the
+// metadata kernel in copy-only mode: no copy-engine transfer to wait on).
 int upload_probe_meta(outlets_ctx* c, const std::vector<int32_t>& v, hipStream_t st) {
     if (static_cast<int64_t>(v.size()) > c->cb.meta_cap) return fail(OUTLETS_ERR_INVALID_ARG, "call metadata exceeds capacity");
     const int s = c->stage;
     if (c->ev_used[s]) HIP_TRY(hipEventSynchronize(c->ev[s]), "hipEventSynchronize");
     std::memcpy(c->h_stage[s], v.data(), sizeof(int32_t) * v.size());
-    HIP_TRY(hipMemcpyAsync(c->probe_meta, c->h_stage[s], sizeof(int32_t) * v.size(), hipMemcpyHostToDevice, st),
-            "hipMemcpyAsync");
+    launch_meta_fetch(c->h_stage[s], static_cast<int>(v.size()), 0, 0, c->probe_meta, nullptr, nullptr, nullptr,
+                      nullptr, st);
     HIP_TRY(hipEventRecord(c->ev[s], st), "hipEventRecord");
     c->ev_used[s] = true;
     c->stage ^= 1;

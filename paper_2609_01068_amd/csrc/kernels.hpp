@@ -103,8 +103,9 @@ bool gemm_qkv_rope_fusable(int act_fmt, int w_fmt, int n_q, int n_kv, int hd, in
 // (index, page) pairs | the rest) into d_meta; applies the pairs to
 // page_table and writes tok_slot[T] (slot of each token), tok_pos[T]
 // (req_start + index within the request) and last_idx[n] (row of each
-// request's newest token).  The host must not rewrite host_meta until the
-// kernel has run.
+// request's newest token).  With n_req = n_pairs = 0 it only copies (the
+// other pointers may then be null).  The host must not rewrite host_meta
+// until the kernel has run.
 void launch_meta_fetch(const int32_t* host_meta, int count, int n_req, int n_pairs, int32_t* d_meta,
                        int32_t* page_table, int32_t* tok_slot, int32_t* tok_pos, int32_t* last_idx, hipStream_t st);
 

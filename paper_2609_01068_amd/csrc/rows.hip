@@ -309,8 +309,18 @@ pool_tiles_kernel(int d, int n_req, const TH* h, int64_t ldh, const int32_t* req
     }
     const int b = req_off[lo] + (t - cu_tiles[lo]) * 32;
     const int e = min(b + 32, req_off[lo + 1]);
+    // rows summed in order; their loads are issued eight at a time (one
+    // dependent load per row measured 2.3 TB/s on a 237 MB bf16 state)
     float s = 0.f;
-    for (int r = b; r < e; ++r) s += load_act<TH>(h + (int64_t)r * ldh + c);
+    int r = b;
+    for (; r + 8 <= e; r += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = load_act<TH>(h + (int64_t)(r + j) * ldh + c);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    for (; r < e; ++r) s += load_act<TH>(h + (int64_t)r * ldh + c);
     part[(int64_t)t * d + c] = s;
 }
 
@@ -404,8 +414,20 @@ pool_prefill_kernel(int d, const TH* h, int64_t ldh, const int32_t* req_off,
     const int c = blockIdx.y * 256 + threadIdx.x;
     if (c >= d) return;
     const int b = req_off[i], e = req_off[i + 1];
+    // tile sums added in tile order; their loads are issued eight at a time
+    // (one dependent load per tile took 39 us for a 32-request, 28,944-token
+    // batch whose longest prompt has 128 tiles)
     float s = 0.f;
-    for (int t = cu_tiles[i]; t < cu_tiles[i + 1]; ++t) s += part[(int64_t)t * d + c];
+    int t = cu_tiles[i];
+    const int t1 = cu_tiles[i + 1];
+    for (; t + 8 <= t1; t += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = part[(int64_t)(t + j) * d + c];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    for (; t < t1; ++t) s += part[(int64_t)t * d + c];
     pool_sum[(int64_t)req_slot[i] * d + c] = s;
     const float mean = s / static_cast<float>(e - b);
     const float last = load_act<TH>(h + (int64_t)(e - 1) * ldh + c);
