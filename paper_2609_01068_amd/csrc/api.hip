@@ -109,6 +109,7 @@ struct outlets_ctx {
     float* probe_sum = nullptr;  // [max_slots, d] running sums of the probe's input rows
     int32_t* probe_meta = nullptr;   // req_off | req_slot | req_start | cu_tiles of a probe call
     float* lm_logits = nullptr;  // draft model head logits [2 * max_batch_requests, V]
+    float* lm_stats = nullptr;   // draft model head softmax: per-chunk max and sum
     std::unique_ptr<Pager> pager;
     int max_pages = 0;
 
@@ -881,6 +882,7 @@ int outlets_create(const outlets_config* cfg, const outlets_weights* weights, in
     }
     ALLOC(c->cb.d_meta, sizeof(int32_t) * c->cb.meta_cap);
     if (w.w_lm) ALLOC(c->lm_logits, sizeof(float) * 2 * Bm * cfg->vocab);
+    if (w.w_lm) ALLOC(c->lm_stats, sizeof(float) * lm_softmax_stats_floats(Bm));
     if (c->probe) {
         ALLOC(c->probe_sum, sizeof(float) * cfg->max_slots * c->d);
         ALLOC(c->probe_meta, sizeof(int32_t) * c->cb.meta_cap);
@@ -1141,7 +1143,7 @@ int outlets_draft_distribution(outlets_ctx* ctx, int32_t n_req, float* p_out, vo
     gemm_launch(ctx->act_fmt, ctx->w_fmt, EPI_STORE_F32, rows, V, static_cast<int>(ctx->d), lm_input(ctx),
                 gemm_b1(ctx->w.w_lm, ctx->w.s_lm, V, ctx->d), gemm_c(ctx->lm_logits, V), 1, st,
                 ctx->cb.splitk_ws, ctx->cb.splitk_bytes);
-    launch_lm_softmax(n_req, V, ctx->lm_logits, split, p_out, st);
+    launch_lm_softmax(n_req, V, ctx->lm_logits, split, ctx->lm_stats, p_out, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return OUTLETS_OK;

@@ -234,7 +234,9 @@ void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* p
 
 // Draft model head (Eq. 2): p[i] = softmax over v of logits row i (plus row
 // n + i when two_rows: the hi/lo halves of a bf16-split input).
-void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* p, hipStream_t st);
+// stats: fp32 scratch of lm_softmax_stats_floats(n) floats (per-chunk max and sum).
+int lm_softmax_stats_floats(int n);
+void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* stats, float* p, hipStream_t st);
 
 void launch_copy_rows_act(int act_fmt, int rows, int d, const float* src, int64_t lds,
                           void* dst, int64_t ldd, hipStream_t st);

@@ -836,34 +836,77 @@ namespace {
 // Draft model head softmax (Eq. 2): one 1024-thread block per request over
 // its V logits; with two_rows the logits are the sum of row i (bf16 hi part
 // of the draft state) and row n + i (lo part).
-__global__ void __launch_bounds__(1024)
-lm_softmax_kernel(int n, int v, const float* logits, int two_rows, float* p) {
-    __shared__ float red[16];
-    const int i = blockIdx.x;
+// Softmax over the draft model head's logits, request i's logits being row i
+// (plus row n + i, the lo half of the bf16 hi/lo input split).  Each request's
+// v logits are cut into kLmChunks chunks, one 256-thread block each: stage 1
+// writes each chunk's max and sum of exp(x - max); stage 2 combines the
+// request's chunk statistics in chunk order (every block the same way, so the
+// result is deterministic) and writes the probabilities of its chunk.  (One
+// block per request kept 32 CUs busy: 135 us for 32 requests over 128,256
+// logits, against 179 us for the head's 1 GB weight stream.)
+constexpr int kLmChunks = 32;
+
+__device__ __forceinline__ void lm_chunk(int v, int c, int& j0, int& j1) {
+    const int per = (v + kLmChunks - 1) / kLmChunks;
+    j0 = min(v, c * per);
+    j1 = min(v, j0 + per);
+}
+
+__global__ void __launch_bounds__(256)
+lm_softmax_stats_kernel(int n, int v, const float* __restrict__ logits, int two_rows, float* __restrict__ stats) {
+    __shared__ float red[4];
+    const int i = blockIdx.x, c = blockIdx.y;
     const float* hi = logits + (int64_t)i * v;
     const float* lo = logits + (int64_t)(n + i) * v;
-    auto x = [&](int j) { return two_rows ? hi[j] + lo[j] : hi[j]; };
+    int j0, j1;
+    lm_chunk(v, c, j0, j1);
     float mx = -INFINITY;
-    for (int j = threadIdx.x; j < v; j += 1024) mx = fmaxf(mx, x(j));
+    for (int j = j0 + threadIdx.x; j < j1; j += 256) mx = fmaxf(mx, two_rows ? hi[j] + lo[j] : hi[j]);
     mx = wave_max(mx);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
     __syncthreads();
-    mx = red[0];
-    for (int k = 1; k < 16; ++k) mx = fmaxf(mx, red[k]);
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
     __syncthreads();
     float sum = 0.f;
-    for (int j = threadIdx.x; j < v; j += 1024) sum += __expf(x(j) - mx);
-    sum = block_sum<1024>(sum, red);
-    const float inv = 1.0f / sum;
+    if (mx > -INFINITY)
+        for (int j = j0 + threadIdx.x; j < j1; j += 256) sum += __expf((two_rows ? hi[j] + lo[j] : hi[j]) - mx);
+    sum = block_sum<256>(sum, red);
+    if (threadIdx.x == 0) {
+        stats[((int64_t)i * kLmChunks + c) * 2] = mx;
+        stats[((int64_t)i * kLmChunks + c) * 2 + 1] = sum;
+    }
+}
+
+__global__ void __launch_bounds__(256)
+lm_softmax_norm_kernel(int n, int v, const float* __restrict__ logits, int two_rows,
+                       const float* __restrict__ stats, float* __restrict__ p) {
+    const int i = blockIdx.x, c = blockIdx.y;
+    const float* st = stats + (int64_t)i * kLmChunks * 2;
+    float M = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kLmChunks; ++k) M = fmaxf(M, st[2 * k]);
+    float S = 0.f;
+#pragma unroll
+    for (int k = 0; k < kLmChunks; ++k)
+        if (st[2 * k] > -INFINITY) S += st[2 * k + 1] * __expf(st[2 * k] - M);
+    const float inv = 1.0f / S;
+    const float* hi = logits + (int64_t)i * v;
+    const float* lo = logits + (int64_t)(n + i) * v;
     float* pr = p + (int64_t)i * v;
-    for (int j = threadIdx.x; j < v; j += 1024) pr[j] = __expf(x(j) - mx) * inv;
+    int j0, j1;
+    lm_chunk(v, c, j0, j1);
+    for (int j = j0 + threadIdx.x; j < j1; j += 256) pr[j] = __expf((two_rows ? hi[j] + lo[j] : hi[j]) - M) * inv;
 }
 
 }  // namespace
 
-void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* p, hipStream_t st) {
-    if (n <= 0) return;
-    hipLaunchKernelGGL(lm_softmax_kernel, dim3(n), dim3(1024), 0, st, n, v, logits, two_rows ? 1 : 0, p);
+int lm_softmax_stats_floats(int n) { return 2 * kLmChunks * n; }
+
+void launch_lm_softmax(int n, int v, const float* logits, bool two_rows, float* stats, float* p, hipStream_t st) {
+    if (n <= 0 || v <= 0) return;
+    const dim3 grid(n, kLmChunks);
+    hipLaunchKernelGGL(lm_softmax_stats_kernel, grid, dim3(256), 0, st, n, v, logits, two_rows ? 1 : 0, stats);
+    hipLaunchKernelGGL(lm_softmax_norm_kernel, grid, dim3(256), 0, st, n, v, logits, two_rows ? 1 : 0, stats, p);
 }
 
 void launch_head_finish(int w_fmt, int n_req, int h1, int splits, const float* partial,
