@@ -41,6 +41,12 @@ namespace {
 #ifndef OUTLETS_GEMM_IGLP
 #define OUTLETS_GEMM_IGLP 0
 #endif
+#ifndef OUTLETS_GEMM_SPLITMAP
+#define OUTLETS_GEMM_SPLITMAP 2   // K-split launches dealt split-major over the XCDs (0 = by tile; 1 = small-M splits only)
+#endif
+#ifndef OUTLETS_GEMM_GMFULL
+#define OUTLETS_GEMM_GMFULL 4     // up to this many row tiles, one group holds them all (0 = off)
+#endif
 #ifndef OUTLETS_GEMM_DMAW
 #define OUTLETS_GEMM_DMAW 4   // waves that issue the LDS copies (0 = all)
 #endif
@@ -65,9 +71,11 @@ __device__ __forceinline__ float silu_f(float g) { return g * __builtin_amdgcn_r
 // Tile order: pid walks GM row-tiles before moving along N, so A rows and
 // B columns are reused from L2.  GM = 3 for wide outputs (>= 64 column
 // tiles) and 2 otherwise (measured best among 1-16 on the draft layer's
-// shapes).
+// shapes); with at most OUTLETS_GEMM_GMFULL row tiles (a decode step's few
+// hundred rows) all of them, so each weight column tile is wanted by one
+// run of pids, i.e. by one XCD.
 __host__ __device__ __forceinline__ void tile_coords(int pid, int mt, int nt, int& tm, int& tn) {
-    const int GM = nt >= 64 ? 3 : 2;
+    const int GM = (mt >= 1 && mt <= OUTLETS_GEMM_GMFULL) ? mt : (nt >= 64 ? 3 : 2);
     const int group = pid / (GM * nt);
     const int first = group * GM;
     const int gsize = (mt - first < GM) ? mt - first : GM;
@@ -170,12 +178,29 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGE + (PF ? 1024 : 0)];
 
     // this launch covers tiles pid0 .. pid0 + gridDim.x - 1 of the tile order
+    // in gridDim.y K splits.  Workgroups reach the XCDs round-robin in
+    // linear order; a K-split launch deals its (split, tile) pairs
+    // split-major, so each XCD's contiguous run covers one or two splits of
+    // many tiles: its A rows and weight columns are those splits' K range
+    // only, and each weight byte is fetched by one XCD (dealt by tile, every
+    // XCD would read all of K for its tiles).
     const int mt = (M + BM - 1) / BM, nt = N / BN;
-    const int tpid = pid0 + xcd_pid(blockIdx.x, gridDim.x);
+    constexpr bool SPLIT_MAJOR = OUTLETS_GEMM_SPLITMAP == 2 ? (EPI == EPI_PARTIAL || EPI == EPI_PARTIAL_TILE)
+                                                            : (OUTLETS_GEMM_SPLITMAP == 1 && EPI == EPI_PARTIAL);
+    int bx = 0, split = 0;
+    if (SPLIT_MAJOR) {
+        const int v = xcd_pid(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+        split = v / gridDim.x;
+        bx = v - split * gridDim.x;
+    } else {
+        bx = xcd_pid(blockIdx.x, gridDim.x);
+        split = blockIdx.y;
+    }
+    const int tpid = pid0 + bx;
     int tm, tn;
     tile_coords(tpid, mt, nt, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-    const int kb = blockIdx.y * k_per_split;
+    const int kb = split * k_per_split;
     const int ke = min(K, kb + k_per_split);
     const int nk = (ke - kb) / BK;
 
@@ -348,9 +373,9 @@ gemm_mfma_256x256(int M, int N, int K, GemmA A, GemmB B, GemmC C, int k_per_spli
     const int ncol0 = EPI == EPI_PARTIAL_TILE ? n0 : 0;       // column origin of the output block
     char* cbase =
         EPI == EPI_PARTIAL_TILE
-            ? static_cast<char*>(C.c) + ((int64_t)blockIdx.y * gridDim.x + (tpid - pid0)) * (BM * BN * 4)
+            ? static_cast<char*>(C.c) + ((int64_t)split * gridDim.x + (tpid - pid0)) * (BM * BN * 4)
             : static_cast<char*>(C.c) +
-                  ((EPI == EPI_PARTIAL ? (int64_t)blockIdx.y * C.split_stride : 0) + (int64_t)m0 * C.ldc) * OSZ;
+                  ((EPI == EPI_PARTIAL ? (int64_t)split * C.split_stride : 0) + (int64_t)m0 * C.ldc) * OSZ;
     const __amdgpu_buffer_rsrc_t rc = buf_rsrc(cbase, (int64_t)rows_valid * ldc * OSZ);
     const int ldr = static_cast<int>(C.ldr);
     const __amdgpu_buffer_rsrc_t rr =
