@@ -15,8 +15,8 @@ HBM-bound per-step workload (512 in-flight requests with paged draft KV
 caches of U[256, 8192] tokens): ms per step, draft tokens/s, and the
 attention kernel's and the whole step's fraction of the HBM peak.
 
-Prints one JSON line (rank 0).  ``--gpus`` above 1 is refused: this build
-runs on one GPU.
+Prints one JSON line (rank 0).  ``--gpus`` above 1 is refused: the
+benchmark measures one GPU's share of the request-parallel path.
 """
 from __future__ import annotations
 
@@ -486,7 +486,7 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the path shards over "
-              "requests and this build measures one GPU's share", file=sys.stderr)
+              "requests, and this benchmark measures one GPU's share", file=sys.stderr)
         return 2
 
     if a.input_embed and a.workload != "prefill-8b":
